@@ -1,0 +1,290 @@
+"""KroQuant CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+Plain, slow, obviously-correct reference for the online activation quantizer of
+"KroQuant: Kronecker-Structured Block Transforms for Efficient Post-Training
+Quantization of Diffusion Transformers".  Only ``tests/``, the smoke check in
+``__graft_entry__`` and the CPU-baseline leg of ``bench.py`` may import it.  It
+shares no code with the HIP library and never imports it.
+
+Two layers:
+
+* ``kq_oracle.c`` (built here with gcc into ``libkqoracle.so``): the scalar
+  per-block definition in the canonical fp32 order -- the Kronecker transform
+  of Sec. 3.2 and the OCP MX v1.0 MXFP4 encode of Sec. 3.1 -- plus the
+  SmoothQuant, Hadamard-32 and plain-MXFP4 comparators of Sec. 4.4.
+* numpy helpers below: fp64 forms used to pin the C code (dense
+  ``numpy.kron`` transform, Sylvester Hadamard), the offline weight side of
+  Sec. 3.4 (W~ = W T^-T with an fp64 LAPACK inverse), the LU factor
+  construction of Sec. 3.2 and the dequantizer Q_b of Sec. 3.1.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from functools import lru_cache
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "kq_oracle.c")
+_LIB = os.path.join(_HERE, "libkqoracle.so")
+
+# E2M1 magnitudes indexed by the low three code bits (OCP MX v1.0 FP4 E2M1).
+E2M1_MAGNITUDES = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0], dtype=np.float64)
+
+
+def build(force: bool = True) -> str:
+    """Compile the C oracle with gcc.  ``-ffp-contract=off`` so that only the
+    explicit ``fmaf`` calls fuse; OpenMP over rows."""
+    if force or not os.path.exists(_LIB):
+        cmd = ["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-shared",
+               "-fPIC", "-std=c11", "-Wall", "-Wextra", _SRC, "-o", _LIB + ".tmp", "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+@lru_cache(maxsize=1)
+def _lib():
+    if not os.path.exists(_LIB):
+        build(force=False)
+    lib = ctypes.CDLL(_LIB)
+    P, I64, I = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    lib.kqo_quantize.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P]
+    lib.kqo_quantize_f32.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P]
+    lib.kqo_smoothquant.argtypes = [P, I64, I64, P, P, P, P]
+    lib.kqo_hadamard32.argtypes = [P, I64, I64, P, P, P]
+    lib.kqo_mxfp4.argtypes = [P, I64, I64, P, P]
+    lib.kqo_e2m1_codes.argtypes = [P, I64, I, P]
+    lib.kqo_e8m0_scales.argtypes = [P, I64, P]
+    lib.kqo_num_threads.argtypes = []
+    lib.kqo_set_num_threads.argtypes = [I]
+    for name in ("kqo_quantize", "kqo_quantize_f32", "kqo_smoothquant", "kqo_hadamard32",
+                 "kqo_mxfp4", "kqo_e2m1_codes", "kqo_e8m0_scales", "kqo_num_threads"):
+        getattr(lib, name).restype = ctypes.c_int
+    lib.kqo_set_num_threads.restype = None
+    return lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(rc, name):
+    if rc != 0:
+        raise ValueError(f"{name}: oracle rejected the arguments (code {rc})")
+
+
+def _outputs(M, d, want_y):
+    codes = np.empty((M, d // 2), dtype=np.uint8)
+    scales = np.empty((M, d // 32), dtype=np.uint8)
+    y = np.empty((M, d), dtype=np.float32) if want_y else None
+    return codes, scales, y
+
+
+def _bf16_bits(X):
+    X = np.ascontiguousarray(X)
+    if X.dtype != np.uint16 or X.ndim != 2:
+        raise TypeError("X must be a 2-D uint16 array of bf16 bit patterns")
+    return X
+
+
+def _factors(A, B, a, b):
+    A = np.ascontiguousarray(A, dtype=np.float32).reshape(-1, a, a)
+    B = np.ascontiguousarray(B, dtype=np.float32).reshape(-1, b, b)
+    if A.shape[0] != B.shape[0]:
+        raise ValueError("A and B must hold the same number of factor pairs")
+    return A, B
+
+
+# ---------------------------------------------------------------- C entry points
+def quantize(X, A, B, want_y=False):
+    """KroQuant quantizer (Sec. 3.2 transform + Sec. 3.1 MXFP4): returns
+    (codes[M, d/2], scales[M, d/32], y[M, d] fp32 or None)."""
+    X = _bf16_bits(X)
+    A = np.asarray(A, dtype=np.float32)
+    B = np.asarray(B, dtype=np.float32)
+    a, b = A.shape[-1], B.shape[-1]
+    A, B = _factors(A, B, a, b)
+    M, d = X.shape
+    codes, scales, y = _outputs(M, d, want_y)
+    _check(_lib().kqo_quantize(_ptr(X), M, d, _ptr(A), _ptr(B), a, b, A.shape[0], _ptr(codes),
+                               _ptr(scales), _ptr(y)), "quantize")
+    return codes, scales, y
+
+
+def quantize_f32(X32, A, B, want_y=False):
+    """Same as ``quantize`` on fp32 rows (no bf16 rounding of the input)."""
+    X32 = np.ascontiguousarray(X32, dtype=np.float32)
+    A = np.asarray(A, dtype=np.float32)
+    B = np.asarray(B, dtype=np.float32)
+    a, b = A.shape[-1], B.shape[-1]
+    A, B = _factors(A, B, a, b)
+    M, d = X32.shape
+    codes, scales, y = _outputs(M, d, want_y)
+    _check(_lib().kqo_quantize_f32(_ptr(X32), M, d, _ptr(A), _ptr(B), a, b, A.shape[0],
+                                   _ptr(codes), _ptr(scales), _ptr(y)), "quantize_f32")
+    return codes, scales, y
+
+
+def smoothquant(X, mult, want_y=False):
+    """SmoothQuant comparator: y_c = x_c * mult_c then MXFP4 (Appendix D)."""
+    X = _bf16_bits(X)
+    mult = np.ascontiguousarray(mult, dtype=np.float32)
+    M, d = X.shape
+    if mult.shape != (d,):
+        raise ValueError("mult must have shape [d]")
+    codes, scales, y = _outputs(M, d, want_y)
+    _check(_lib().kqo_smoothquant(_ptr(X), M, d, _ptr(mult), _ptr(codes), _ptr(scales), _ptr(y)),
+           "smoothquant")
+    return codes, scales, y
+
+
+def hadamard32(X, want_y=False):
+    """Hadamard-32 comparator: y = H32 x / sqrt(32) then MXFP4."""
+    X = _bf16_bits(X)
+    M, d = X.shape
+    codes, scales, y = _outputs(M, d, want_y)
+    _check(_lib().kqo_hadamard32(_ptr(X), M, d, _ptr(codes), _ptr(scales), _ptr(y)), "hadamard32")
+    return codes, scales, y
+
+
+def mxfp4(X):
+    """Plain MXFP4 of the bf16 input (Q4)."""
+    X = _bf16_bits(X)
+    M, d = X.shape
+    codes, scales, _ = _outputs(M, d, False)
+    _check(_lib().kqo_mxfp4(_ptr(X), M, d, _ptr(codes), _ptr(scales)), "mxfp4")
+    return codes, scales
+
+
+def e2m1_codes(v, s=127):
+    """Unpacked E2M1 code (sign in bit 3) of every fp32 value at E8M0 byte s."""
+    v = np.ascontiguousarray(v, dtype=np.float32).ravel()
+    out = np.empty(v.shape, dtype=np.uint8)
+    _check(_lib().kqo_e2m1_codes(_ptr(v), v.size, int(s), _ptr(out)), "e2m1_codes")
+    return out
+
+
+def e8m0_scales(amax):
+    """E8M0 byte of each block maximum."""
+    amax = np.ascontiguousarray(amax, dtype=np.float32).ravel()
+    out = np.empty(amax.shape, dtype=np.uint8)
+    _check(_lib().kqo_e8m0_scales(_ptr(amax), amax.size, _ptr(out)), "e8m0_scales")
+    return out
+
+
+def num_threads():
+    return int(_lib().kqo_num_threads())
+
+
+def set_num_threads(n):
+    _lib().kqo_set_num_threads(int(n))
+
+
+# ---------------------------------------------------------------- numpy, fp64
+def bf16_to_f32(X):
+    """Widen bf16 bit patterns to fp32 (exact)."""
+    return (np.asarray(X, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def unpack_codes(codes):
+    """[.., n/2] packed bytes -> [.., n] codes; element 2i is the low nibble."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    out = np.empty(codes.shape[:-1] + (codes.shape[-1] * 2,), dtype=np.uint8)
+    out[..., 0::2] = codes & 0xF
+    out[..., 1::2] = codes >> 4
+    return out
+
+
+def dequantize(codes, scales):
+    """Q_b of Sec. 3.1: value = (-1)^sign * E2M1[mag] * 2^(s-127), fp64."""
+    c = unpack_codes(codes)
+    mag = E2M1_MAGNITUDES[c & 7]
+    sign = np.where(c & 8, -1.0, 1.0)
+    s = np.repeat(np.asarray(scales, dtype=np.int64), 32, axis=-1)
+    return sign * mag * np.exp2(s - 127.0)
+
+
+def kron_dense(A, B):
+    """Materialised 32x32 blocks K = A (x) B, fp64, numpy.kron index order
+    (row index = i_A * b + i_B): [nfac, 32, 32]."""
+    A = np.asarray(A, dtype=np.float64)
+    B = np.asarray(B, dtype=np.float64)
+    A = A.reshape(-1, A.shape[-1], A.shape[-1])
+    B = B.reshape(-1, B.shape[-1], B.shape[-1])
+    return np.stack([np.kron(A[f], B[f]) for f in range(A.shape[0])])
+
+
+def transform_f64(X, A, B):
+    """y = (A (x) B) x per 32-block in fp64 through the dense Kronecker
+    product (Sec. 3.2).  X: [M, d] bf16 bits or any float array."""
+    Xf = bf16_to_f32(X) if np.asarray(X).dtype == np.uint16 else np.asarray(X)
+    Xf = Xf.astype(np.float64)
+    M, d = Xf.shape
+    K = kron_dense(A, B)
+    blocks = Xf.reshape(M, d // 32, 32)
+    if K.shape[0] == 1:
+        y = blocks @ K[0].T
+    else:
+        y = np.einsum("fij,mfj->mfi", K, blocks)
+    return y.reshape(M, d)
+
+
+def hadamard32_f64(X):
+    """y = H32 x / sqrt(32) per block in fp64 with the Sylvester H32."""
+    from scipy.linalg import hadamard
+    Xf = bf16_to_f32(X).astype(np.float64)
+    M, d = Xf.shape
+    H = hadamard(32).astype(np.float64) / np.sqrt(32.0)
+    return (Xf.reshape(M, d // 32, 32) @ H.T).reshape(M, d)
+
+
+def factors_inverse_transpose(A, B):
+    """(A^-T, B^-T) in fp64 via LAPACK, rounded to fp32, so that
+    (A (x) B)^-T = A^-T (x) B^-T (Sec. 3.2: the inverse of a Kronecker product
+    is the Kronecker product of the inverses)."""
+    A64 = np.asarray(A, dtype=np.float64)
+    B64 = np.asarray(B, dtype=np.float64)
+    Ai = np.swapaxes(np.linalg.inv(A64), -1, -2)
+    Bi = np.swapaxes(np.linalg.inv(B64), -1, -2)
+    return Ai.astype(np.float32), Bi.astype(np.float32)
+
+
+def weight_transform(W, A, B, want_codes=True):
+    """Offline weight side, Sec. 3.4 / eq. (1): W~ = W T^-T, i.e. per block
+    w' = (A (x) B)^-T w; returns (W~ fp32, codes, scales)."""
+    Ait, Bit = factors_inverse_transpose(A, B)
+    codes, scales, y = quantize(W, Ait, Bit, want_y=True)
+    return (y, codes, scales) if want_codes else (y, None, None)
+
+
+def lu_factor(a, b, c):
+    """G = L U with L = [[1, 0], [c, 1]], U = [[a, b], [0, -1/a]] (Sec. 3.2)."""
+    L = np.array([[1.0, 0.0], [c, 1.0]])
+    U = np.array([[a, b], [0.0, -1.0 / a]])
+    return L @ U
+
+
+def lu_to_factors(abc, a_dim):
+    """Paper parameters (a_k, b_k, c_k), k = 1..5, per block -> library
+    factors (A, B) with A (x) B = K^T, K = G1 (x) ... (x) G5.
+
+    The paper right-multiplies row activations (A -> A T, eq. (1)), so a
+    block row x^T maps to x^T K, i.e. y = K^T x; (G1 (x) .. (x) G5)^T =
+    G1^T (x) .. (x) G5^T, split after log2(a_dim) factors."""
+    abc = np.asarray(abc, dtype=np.float64).reshape(-1, 5, 3)
+    na = int(round(np.log2(a_dim)))
+    As, Bs = [], []
+    for blk in abc:
+        Gs = [lu_factor(*blk[k]) for k in range(5)]
+        Ka = np.ones((1, 1))
+        for G in Gs[:na]:
+            Ka = np.kron(Ka, G)
+        Kb = np.ones((1, 1))
+        for G in Gs[na:]:
+            Kb = np.kron(Kb, G)
+        As.append(Ka.T)
+        Bs.append(Kb.T)
+    return np.array(As, dtype=np.float32), np.array(Bs, dtype=np.float32)

@@ -1,0 +1,263 @@
+/*
+ * KroQuant CPU oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * This file is the plain, slow, obviously-correct reference for the online
+ * activation quantizer of "KroQuant: Kronecker-Structured Block Transforms for
+ * Efficient Post-Training Quantization of Diffusion Transformers".  Only the
+ * test suite, the smoke check and the benchmark's CPU-baseline leg may load it.
+ * It shares no code, header, table or constant with the HIP library: every
+ * rule below is written out again from the paper and from the OCP
+ * Microscaling (MX) v1.0 format that the paper quantizes to.
+ *
+ * Build (see oracle/__init__.py):  gcc -O2 -ffp-contract=off -fopenmp -shared -fPIC
+ * -ffp-contract=off keeps the compiler from fusing a*b+c on its own; every
+ * fused multiply-add below is an explicit fmaf() and every other product and
+ * sum is rounded to fp32 on its own.
+ *
+ * What is computed, per row r of X[M, d] (bf16) and per column block j of 32
+ * elements (Sec. 3.1 "Quantization setup": row-wise blocks of n = 32 sharing
+ * one scale; block-diagonal T = diag(K^(1), ..., K^(d/32)), Sec. 3.1 "Goal"):
+ *
+ *   1. x = the 32 bf16 values widened to fp32 (exact).
+ *   2. y = (A (x) B) x, the Kronecker-structured block transform of Sec. 3.2,
+ *      evaluated through the identity (A (x) B) vec(X) = vec(B X A^T) on the
+ *      block reshaped row-major to a x b (Xm[p][q] = x[p*b+q]), i.e.
+ *      Ym = A . Xm . B^T.  Evaluation order (the canonical fp32 order):
+ *        Z[p][i] = B[i][0]*Xm[p][0];  Z[p][i] = fmaf(B[i][q], Xm[p][q], Z[p][i]), q = 1..b-1
+ *        Y[o][i] = A[o][0]*Z[0][i];   Y[o][i] = fmaf(A[o][p], Z[p][i],  Y[o][i]), p = 1..a-1
+ *        y[o*b+i] = Y[o][i].
+ *      The paper leaves the fp32 order open (Sec. 3.5 only says fp32
+ *      accumulation); this order is the reading adopted for parity.
+ *   3. MXFP4 encode of the fp32 y (Sec. 3.1; format per OCP MX v1.0, which
+ *      the paper cites for MXFP4):
+ *        shared exponent E = floor(log2(max_k |y_k|)) - 2   (2 = emax of E2M1)
+ *        stored E8M0 byte  s = clamp(E + 127, 0, 254);  s = 0 for an all-zero block
+ *        element code      = sign bit (bit 3) | index of the E2M1 magnitude
+ *                            {0, .5, 1, 1.5, 2, 3, 4, 6} nearest to |y_k| / 2^(s-127),
+ *                            ties to the even index, saturating at 6.
+ *        packing           codes[r, 16j + i] = code(2i) | code(2i+1) << 4.
+ *
+ * Comparators (Sec. 4.4 and the ablation of Sec. 4.3):
+ *   SmoothQuant   y_c = x_c * m_c (per-channel multiplier m = 1/s, Appendix D "Smoothing").
+ *   Hadamard-32   y = H32 x / sqrt(32), H32 the Sylvester matrix = H2 (x) ... (x) H2 (Sec. 3.2
+ *                 "Hadamard initialization"), evaluated by add/subtract butterflies with
+ *                 strides 1, 2, 4, 8, 16 followed by one multiply by fp32(1/sqrt(32)).
+ *   plain MXFP4   y = x (the bare quantizer, "Q4" of Sec. 4.4).
+ *
+ * Every entry point returns 0 on success and a negative value on a bad
+ * argument; it never allocates beyond the stack.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#define BLK 32
+
+/* --- bf16 -> fp32: the bf16 bit pattern is the upper half of the fp32 one. */
+static float bf16_to_f32(uint16_t h) {
+    uint32_t u = ((uint32_t)h) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+/* --- E8M0 shared scale of one block (OCP MX v1.0; Sec. 3.1 shared scale s).
+ * floor(log2(amax)) comes from frexp, which returns amax = m * 2^e with
+ * m in [0.5, 1), so floor(log2(amax)) = e - 1 for every finite amax > 0,
+ * subnormals included. */
+static int e8m0_scale(float amax) {
+    if (!(amax > 0.0f)) return 0;              /* all-zero block: smallest scale */
+    int e;
+    (void)frexp((double)amax, &e);
+    int shared = (e - 1) - 2;                  /* floor(log2 amax) - emax(E2M1) */
+    int s = shared + 127;
+    if (s < 0) s = 0;
+    if (s > 254) s = 254;
+    return s;
+}
+
+/* --- E2M1 element code (OCP MX v1.0 FP4 E2M1: 1 sign, 2 exponent, 1 mantissa
+ * bit; magnitudes indexed by the 3 low code bits).  Brute-force nearest over
+ * the eight magnitudes, exact in double; on a tie the even index wins (round
+ * half to even on the code).  Values above 6 pick 6 (saturation). */
+static const double kE2M1[8] = {0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0};
+
+static int e2m1_code(float y, int s) {
+    double v = ldexp(fabs((double)y), 127 - s); /* exact: a power-of-two rescale in double */
+    int best = 0;
+    double bestd = fabs(v - kE2M1[0]);
+    for (int k = 1; k < 8; ++k) {
+        double dk = fabs(v - kE2M1[k]);
+        if (dk < bestd || (dk == bestd && (k % 2 == 0) && (best % 2 == 1))) {
+            best = k;
+            bestd = dk;
+        }
+    }
+    return best | (signbit(y) ? 8 : 0);
+}
+
+/* --- encode one block of 32 fp32 values: scale byte + 16 packed bytes. */
+static void encode_block(const float* y, uint8_t* codes16, uint8_t* scale) {
+    float amax = 0.0f;
+    for (int k = 0; k < BLK; ++k) {
+        float a = fabsf(y[k]);
+        if (a > amax) amax = a;
+    }
+    int s = e8m0_scale(amax);
+    *scale = (uint8_t)s;
+    for (int i = 0; i < BLK / 2; ++i) {
+        int lo = e2m1_code(y[2 * i], s);
+        int hi = e2m1_code(y[2 * i + 1], s);
+        codes16[i] = (uint8_t)(lo | (hi << 4));
+    }
+}
+
+/* --- y = (A (x) B) x for one block, canonical order (see header). */
+static void kron_block(const float* x, const float* A, const float* B, int a, int b, float* y) {
+    float Z[BLK];
+    for (int p = 0; p < a; ++p) {
+        for (int i = 0; i < b; ++i) {
+            float z = B[i * b + 0] * x[p * b + 0];
+            for (int q = 1; q < b; ++q) z = fmaf(B[i * b + q], x[p * b + q], z);
+            Z[p * b + i] = z;
+        }
+    }
+    for (int o = 0; o < a; ++o) {
+        for (int i = 0; i < b; ++i) {
+            float acc = A[o * a + 0] * Z[0 * b + i];
+            for (int p = 1; p < a; ++p) acc = fmaf(A[o * a + p], Z[p * b + i], acc);
+            y[o * b + i] = acc;
+        }
+    }
+}
+
+/* --- Hadamard-32 of one block: Sylvester butterflies, then 1/sqrt(32). */
+static void hadamard32_block(const float* x, float* y) {
+    float u[BLK];
+    for (int k = 0; k < BLK; ++k) u[k] = x[k];
+    for (int h = 1; h < BLK; h <<= 1) {
+        for (int i = 0; i < BLK; ++i) {
+            if (i & h) continue;
+            float s0 = u[i] + u[i + h];
+            float s1 = u[i] - u[i + h];
+            u[i] = s0;
+            u[i + h] = s1;
+        }
+    }
+    const float inv_sqrt32 = (float)(1.0 / sqrt(32.0)); /* nearest fp32 to 1/sqrt(32) */
+    for (int k = 0; k < BLK; ++k) y[k] = u[k] * inv_sqrt32;
+}
+
+static int valid_ab(int a, int b) {
+    return (a == 4 && b == 8) || (a == 2 && b == 16) || (a == 8 && b == 4) || (a == 1 && b == 32);
+}
+
+enum { KIND_KRON = 0, KIND_SMOOTH = 1, KIND_HAD = 2, KIND_PLAIN = 3, KIND_KRON_F32IN = 4 };
+
+/* Shared driver: rows in parallel; each output element is produced by
+ * exactly one iteration and its value does not depend on the thread count. */
+static int run(int kind, const void* Xv, int64_t M, int64_t d, const float* A, const float* B,
+               int a, int b, int64_t nfac, const float* mult, uint8_t* codes, uint8_t* scales,
+               float* yout) {
+    if (M < 0 || d <= 0 || d % BLK != 0) return -1;
+    if (!Xv || !codes || !scales) return -2;
+    int64_t nb = d / BLK;
+    if (kind == KIND_KRON || kind == KIND_KRON_F32IN) {
+        if (!A || !B) return -2;
+        if (!valid_ab(a, b)) return -3;
+        if (nfac != 1 && nfac != nb) return -4;
+    }
+    if (kind == KIND_SMOOTH && !mult) return -2;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < M; ++r) {
+        float x[BLK], y[BLK];
+        for (int64_t j = 0; j < nb; ++j) {
+            int64_t base = r * d + j * BLK;
+            for (int k = 0; k < BLK; ++k) {
+                if (kind == KIND_KRON_F32IN)
+                    x[k] = ((const float*)Xv)[base + k];
+                else
+                    x[k] = bf16_to_f32(((const uint16_t*)Xv)[base + k]);
+            }
+            switch (kind) {
+                case KIND_KRON:
+                case KIND_KRON_F32IN: {
+                    int64_t f = (nfac == 1) ? 0 : j;
+                    kron_block(x, A + f * a * a, B + f * b * b, a, b, y);
+                    break;
+                }
+                case KIND_SMOOTH:
+                    for (int k = 0; k < BLK; ++k) y[k] = x[k] * mult[j * BLK + k];
+                    break;
+                case KIND_HAD:
+                    hadamard32_block(x, y);
+                    break;
+                default:
+                    for (int k = 0; k < BLK; ++k) y[k] = x[k];
+                    break;
+            }
+            encode_block(y, codes + r * (d / 2) + j * (BLK / 2), scales + r * nb + j);
+            if (yout)
+                for (int k = 0; k < BLK; ++k) yout[base + k] = y[k];
+        }
+    }
+    return 0;
+}
+
+/* KroQuant quantizer: per block y = (A (x) B) x, then MXFP4 (Sec. 3.2, 3.5).
+ * A: [nfac, a, a], B: [nfac, b, b] fp32 row-major; nfac = 1 (shared) or d/32. */
+int kqo_quantize(const uint16_t* X, int64_t M, int64_t d, const float* A, const float* B, int a,
+                 int b, int64_t nfac, uint8_t* codes, uint8_t* scales, float* yout) {
+    return run(KIND_KRON, X, M, d, A, B, a, b, nfac, NULL, codes, scales, yout);
+}
+
+/* Same transform on fp32 input rows (used for the weight side, Sec. 3.4, and
+ * for round-trip checks). */
+int kqo_quantize_f32(const float* X, int64_t M, int64_t d, const float* A, const float* B, int a,
+                     int b, int64_t nfac, uint8_t* codes, uint8_t* scales, float* yout) {
+    return run(KIND_KRON_F32IN, X, M, d, A, B, a, b, nfac, NULL, codes, scales, yout);
+}
+
+/* SmoothQuant comparator: y_c = x_c * mult_c, then MXFP4 (Sec. 4.4 "Scale"). */
+int kqo_smoothquant(const uint16_t* X, int64_t M, int64_t d, const float* mult, uint8_t* codes,
+                    uint8_t* scales, float* yout) {
+    return run(KIND_SMOOTH, X, M, d, NULL, NULL, 0, 0, 1, mult, codes, scales, yout);
+}
+
+/* Hadamard-32 comparator: y = H32 x / sqrt(32), then MXFP4 (Sec. 1, Sec. 4.3). */
+int kqo_hadamard32(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, uint8_t* scales,
+                   float* yout) {
+    return run(KIND_HAD, X, M, d, NULL, NULL, 0, 0, 1, NULL, codes, scales, yout);
+}
+
+/* Plain MXFP4 of the bf16 input ("Q4", Sec. 4.4). */
+int kqo_mxfp4(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, uint8_t* scales) {
+    return run(KIND_PLAIN, X, M, d, NULL, NULL, 0, 0, 1, NULL, codes, scales, NULL);
+}
+
+/* Element encode alone: one unpacked code per value at E8M0 byte s. */
+int kqo_e2m1_codes(const float* v, int64_t n, int s, uint8_t* out) {
+    if (n < 0 || s < 0 || s > 254) return -1;
+    if (n > 0 && (!v || !out)) return -2;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) out[i] = (uint8_t)e2m1_code(v[i], s);
+    return 0;
+}
+
+/* Scale rule alone: E8M0 byte of each block maximum. */
+int kqo_e8m0_scales(const float* amax, int64_t n, uint8_t* out) {
+    if (n < 0) return -1;
+    if (n > 0 && (!amax || !out)) return -2;
+    for (int64_t i = 0; i < n; ++i) out[i] = (uint8_t)e8m0_scale(amax[i]);
+    return 0;
+}
+
+/* Number of OpenMP threads a parallel region would use (for reporting). */
+#ifdef _OPENMP
+#include <omp.h>
+int kqo_num_threads(void) { return omp_get_max_threads(); }
+void kqo_set_num_threads(int n) { omp_set_num_threads(n); }
+#else
+int kqo_num_threads(void) { return 1; }
+void kqo_set_num_threads(int n) { (void)n; }
+#endif

@@ -1,0 +1,319 @@
+"""Pins of the CPU oracle to facts fixed by the paper and by mathematics.
+
+Each test checks the oracle against something other than itself: hand-derived
+encodes (tests/golden/), closed forms (the Kronecker identity, the inverse of
+a Kronecker product, the Sylvester Hadamard), an independently derived
+threshold rule checked over every fp32 value in [0, 8], the bit-level scale
+rule, and invariants (sign symmetry, power-of-two equivariance, eq. (1)
+invariance, thread-count independence).  CPU only.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from conftest import load_golden, parse_values
+
+AB_SPLITS = [(4, 8), (2, 16), (8, 4), (1, 32)]
+
+
+def _row(vals):
+    return synth.to_bf16_bits(np.array([vals], dtype=np.float32))
+
+
+# ---------------------------------------------------------------- golden blocks
+@pytest.mark.parametrize("case", load_golden("mxfp4_blocks.txt"), ids=lambda c: c[0])
+def test_golden_mxfp4_block(case):
+    name, spec, s, hexcodes = case
+    vals = parse_values(spec)
+    X = _row(vals)
+    # the fixture values must be bf16-exact, so the encode sees exactly them
+    assert np.array_equal(oracle.bf16_to_f32(X)[0], np.array(vals, dtype=np.float32))
+    codes, scales = oracle.mxfp4(X)
+    assert int(scales[0, 0]) == int(s), name
+    assert codes[0].tobytes().hex() == hexcodes, name
+
+
+@pytest.mark.parametrize("case", load_golden("transform_blocks.txt"), ids=lambda c: c[0] + c[1])
+def test_golden_transform_block(case):
+    method, spec, s, hexcodes = case
+    X = _row(parse_values(spec))
+    if method == "hadamard32":
+        codes, scales, _ = oracle.hadamard32(X)
+    else:
+        from scipy.linalg import hadamard
+        A = (hadamard(4) / 2.0).astype(np.float32)
+        B = (hadamard(8) / np.sqrt(8.0)).astype(np.float32)
+        codes, scales, _ = oracle.quantize(X, A[None], B[None])
+    assert int(scales[0, 0]) == int(s)
+    assert codes[0].tobytes().hex() == hexcodes
+
+
+# ---------------------------------------------------------------- element encode
+def _threshold_magnitude(v):
+    """E2M1 magnitude index from the decision thresholds: the midpoints of
+    consecutive magnitudes {0,.5,1,1.5,2,3,4,6}; at a midpoint the even index
+    wins, so the comparison is '>' when the upper neighbour is odd and '>='
+    when it is even."""
+    return ((v > 0.25).astype(np.uint8) + (v >= 0.75) + (v > 1.25) + (v >= 1.75) + (v > 2.5)
+            + (v >= 3.5) + (v > 5.0)).astype(np.uint8)
+
+
+def test_e2m1_exhaustive_unit_scale():
+    """Every fp32 bit pattern in [0, 8] (and its negation) at scale 2^0."""
+    lo, hi = 0, np.float32(8.0).view(np.uint32) + 1
+    chunk = 1 << 24
+    for start in range(int(lo), int(hi), chunk):
+        bits = np.arange(start, min(start + chunk, int(hi)), dtype=np.uint32)
+        v = bits.view(np.float32)
+        got = oracle.e2m1_codes(v, 127)
+        assert np.array_equal(got, _threshold_magnitude(v)), hex(start)
+        gotn = oracle.e2m1_codes(-v, 127)
+        assert np.array_equal(gotn, _threshold_magnitude(v) | 8), hex(start)
+
+
+def test_e2m1_saturation_and_other_scales():
+    rng = np.random.default_rng(7)
+    big = np.float32(8.0) * (1 + rng.random(100000, dtype=np.float32) * 1e6)
+    assert np.all(oracle.e2m1_codes(big, 127) == 7)
+    for s in (0, 1, 2, 100, 127, 128, 200, 254):
+        # values whose scaled magnitude |y| / 2^(s-127) spans [0, 8)
+        v = np.minimum(rng.random(200000) * 8.0 * np.exp2(s - 127.0),
+                       np.finfo(np.float32).max).astype(np.float32)
+        scaled = np.abs(v.astype(np.float64)) * np.exp2(127.0 - s)
+        assert np.array_equal(oracle.e2m1_codes(v, s), _threshold_magnitude(scaled)), s
+
+
+# ---------------------------------------------------------------- E8M0 scale
+def test_e8m0_bit_rule():
+    """s = max(biased exponent field - 2, 0), from the fp32 bit pattern; this
+    is floor(log2 amax) - emax(E2M1) + 127 clamped at 0 for normal amax, and 0
+    for subnormal amax."""
+    rng = np.random.default_rng(3)
+    bits = rng.integers(0, 0x7F800000, size=2_000_000, dtype=np.uint32)
+    amax = bits.view(np.float32)
+    got = oracle.e8m0_scales(amax)
+    expfield = ((bits >> 23) & 0xFF).astype(np.int64)
+    want = np.maximum(expfield - 2, 0)
+    assert np.array_equal(got.astype(np.int64), want)
+    # for s > 0 the scaled maximum lands in [4, 8): largest magnitude 6 fits
+    pos = got > 0
+    r = amax[pos].astype(np.float64) / np.exp2(got[pos].astype(np.float64) - 127.0)
+    assert r.min() >= 4.0 and r.max() < 8.0
+    assert oracle.e8m0_scales(np.zeros(1))[0] == 0
+
+
+# ---------------------------------------------------------------- transform
+def _kron_bound(X, A, B):
+    """Per-element sum_j |K_kj| |x_j|, fp64."""
+    K = np.abs(oracle.kron_dense(A, B))
+    Xa = np.abs(oracle.bf16_to_f32(X).astype(np.float64))
+    M, d = Xa.shape
+    blocks = Xa.reshape(M, d // 32, 32)
+    if K.shape[0] == 1:
+        return (blocks @ K[0].T).reshape(M, d)
+    return np.einsum("fij,mfj->mfi", K, blocks).reshape(M, d)
+
+
+@pytest.mark.parametrize("ab", AB_SPLITS)
+@pytest.mark.parametrize("per_block", [False, True])
+def test_kron_identity(ab, per_block):
+    """(A (x) B) x via the canonical separable fp32 order equals the dense
+    numpy.kron product in fp64 to within fp32 accumulation error."""
+    a, b = ab
+    M, d = 37, 1152
+    X = synth.activations(M, d, "student_t3", seed=11, chan_frac=0.01, chan_factor=30)
+    A, B = synth.factors(a, b, d // 32 if per_block else 1, seed=5)
+    _, _, y = oracle.quantize(X, A, B, want_y=True)
+    ref = oracle.transform_f64(X, A, B)
+    bound = _kron_bound(X, A, B)
+    err = np.abs(y.astype(np.float64) - ref)
+    assert np.all(err <= (a + b + 2) * 2.0**-24 * bound + 1e-30)
+    # a transposed factor would break the identity by far more than rounding
+    At = np.swapaxes(A, -1, -2).copy()
+    _, _, y_bad = oracle.quantize(X, At, B, want_y=True)
+    if a > 1:
+        assert np.max(np.abs(y_bad - ref) / (bound + 1e-30)) > 1e-3
+
+
+def test_kronecker_bit_formula_and_lu():
+    """Sec. 3.5 (K2): K[r, c] = prod_k G_k[r_(5-k), c_(5-k)] equals
+    G1 (x) ... (x) G5 in numpy.kron order; LU factors have det -1; the
+    Hadamard init is LU(1/sqrt2, 1/sqrt2, 1)."""
+    rng = np.random.default_rng(1)
+    abc = rng.normal(size=(5, 3))
+    abc[:, 0] = np.where(np.abs(abc[:, 0]) < 0.2, 0.5, abc[:, 0])
+    Gs = [oracle.lu_factor(*abc[k]) for k in range(5)]
+    for G in Gs:
+        assert abs(np.linalg.det(G) + 1.0) < 1e-12
+    K = Gs[0]
+    for G in Gs[1:]:
+        K = np.kron(K, G)
+    Kbit = np.ones((32, 32))
+    for r in range(32):
+        for c in range(32):
+            for k in range(1, 6):
+                Kbit[r, c] *= Gs[k - 1][(r >> (5 - k)) & 1, (c >> (5 - k)) & 1]
+    assert np.allclose(K, Kbit, rtol=0, atol=1e-12 * np.abs(K).max())
+    h = 1 / np.sqrt(2)
+    H2 = np.array([[h, h], [h, -h]])
+    assert np.allclose(oracle.lu_factor(h, h, 1.0), H2, atol=1e-15)
+    # lu_to_factors: A (x) B = K^T for every split
+    for a, b in AB_SPLITS:
+        A, B = oracle.lu_to_factors(abc[None], a)
+        assert A.shape == (1, a, a) and B.shape == (1, b, b)
+        KT = np.kron(A[0].astype(np.float64), B[0].astype(np.float64))
+        assert np.allclose(KT, K.T, rtol=0, atol=1e-6 * np.abs(K).max())
+
+
+def test_sylvester_hadamard_split():
+    from scipy.linalg import hadamard
+    assert np.array_equal(np.kron(hadamard(4), hadamard(8)), hadamard(32))
+    H2 = hadamard(2)
+    H = H2
+    for _ in range(4):
+        H = np.kron(H, H2)
+    assert np.array_equal(H, hadamard(32))
+
+
+def test_identity_factors_reduce_to_plain_mxfp4():
+    X = synth.activations(64, 1152, "normal", seed=2)
+    X[X == 0x8000] = 0  # -0.0 would become +0.0 through the products (sign of zero)
+    for a, b in AB_SPLITS:
+        A = np.eye(a, dtype=np.float32)[None]
+        B = np.eye(b, dtype=np.float32)[None]
+        c1, s1, y = oracle.quantize(X, A, B, want_y=True)
+        c0, s0 = oracle.mxfp4(X)
+        assert np.array_equal(y, oracle.bf16_to_f32(X))
+        assert np.array_equal(s1, s0) and np.array_equal(c1, c0)
+
+
+def test_hadamard32_against_dense():
+    X = synth.activations(33, 2240, "laplace", seed=4, chan_frac=0.02, chan_factor=20)
+    _, _, y = oracle.hadamard32(X, want_y=True)
+    ref = oracle.hadamard32_f64(X)
+    bound = np.abs(oracle.bf16_to_f32(X).astype(np.float64)).reshape(33, -1, 32).sum(-1)
+    bound = np.repeat(bound, 32, axis=1) / np.sqrt(32.0)
+    assert np.all(np.abs(y - ref) <= 7 * 2.0**-24 * bound + 1e-30)
+
+
+def test_smoothquant_single_rounding():
+    """y_c = fp32(x_c * m_c): the product of two fp32 values is exact in
+    fp64, so one rounding to fp32 gives the expected value bit for bit."""
+    X = synth.activations(40, 2240, "laplace", seed=8, chan_frac=0.02, chan_factor=20)
+    m = synth.smoothquant_multipliers(X)
+    _, _, y = oracle.smoothquant(X, m, want_y=True)
+    ref = (oracle.bf16_to_f32(X).astype(np.float64) * m.astype(np.float64)).astype(np.float32)
+    assert np.array_equal(y.view(np.uint32), ref.view(np.uint32))
+    c1, s1, _ = oracle.smoothquant(X, np.ones(2240, np.float32))
+    c0, s0 = oracle.mxfp4(X)
+    assert np.array_equal(c1, c0) and np.array_equal(s1, s0)
+
+
+# ---------------------------------------------------------------- layout and error
+@pytest.mark.parametrize("method", ["kron", "kron_pb", "had", "smooth", "plain"])
+def test_dequantized_error_bound(method):
+    """Q_b(y) - y stays within half the local E2M1 spacing times the scale
+    (at most 1 * 2^(s-127)), or equals the clip when |y| > 6 * 2^(s-127).
+    A wrong row/block/nibble offset in the packing fails this."""
+    M, d = 29, 2240
+    X = synth.activations(M, d, "student_t3", seed=21, chan_frac=0.005, chan_factor=50)
+    if method in ("kron", "kron_pb"):
+        A, B = synth.factors(4, 8, d // 32 if method == "kron_pb" else 1, seed=9)
+        codes, scales, y = oracle.quantize(X, A, B, want_y=True)
+    elif method == "had":
+        codes, scales, y = oracle.hadamard32(X, want_y=True)
+    elif method == "smooth":
+        codes, scales, y = oracle.smoothquant(X, synth.smoothquant_multipliers(X), want_y=True)
+    else:
+        codes, scales = oracle.mxfp4(X)
+        y = oracle.bf16_to_f32(X)
+    deq = oracle.dequantize(codes, scales)
+    unit = np.exp2(np.repeat(scales.astype(np.float64), 32, axis=1) - 127.0)
+    yd = y.astype(np.float64)
+    clip = np.maximum(np.abs(yd) - 6.0 * unit, 0.0)
+    assert np.all(np.abs(deq - yd) <= np.maximum(1.0 * unit, clip) * (1 + 1e-12))
+    # and the block maximum never clips by more than 8/6
+    amax = np.abs(yd).reshape(M, -1, 32).max(-1)
+    assert np.all(amax < 8.0 * np.exp2(scales.astype(np.float64) - 127.0) + 1e-300)
+
+
+# ---------------------------------------------------------------- invariants
+def test_sign_symmetry():
+    X = synth.activations(50, 1152, "normal", seed=12)
+    A, B = synth.factors(4, 8, 1, seed=13)
+    c, s, _ = oracle.quantize(X, A, B)
+    cn, sn, _ = oracle.quantize(X ^ np.uint16(0x8000), A, B)
+    assert np.array_equal(s, sn)
+    u, un = oracle.unpack_codes(c), oracle.unpack_codes(cn)
+    nz = (u & 7) != 0
+    assert np.array_equal(u[nz] ^ 8, un[nz])
+    assert np.array_equal(u & 7, un & 7)
+
+
+def test_power_of_two_equivariance():
+    X = synth.activations(50, 1152, "normal", seed=14)
+    A, B = synth.factors(4, 8, 1, seed=15)
+    c, s, _ = oracle.quantize(X, A, B)
+    for k in (-5, 3):
+        Xk = synth.to_bf16_bits(oracle.bf16_to_f32(X) * np.float32(2.0**k))
+        ck, sk, _ = oracle.quantize(Xk, A, B)
+        assert np.array_equal(ck, c)
+        assert np.array_equal(sk.astype(int), s.astype(int) + k)
+
+
+def test_thread_count_independence():
+    X = synth.activations(96, 1152, "student_t3", seed=16)
+    A, B = synth.factors(4, 8, 36, seed=17)
+    n = oracle.num_threads()
+    try:
+        oracle.set_num_threads(1)
+        c1, s1, y1 = oracle.quantize(X, A, B, want_y=True)
+        oracle.set_num_threads(max(n, 4))
+        c2, s2, y2 = oracle.quantize(X, A, B, want_y=True)
+    finally:
+        oracle.set_num_threads(n)
+    assert np.array_equal(c1, c2) and np.array_equal(s1, s2)
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+
+
+# ---------------------------------------------------------------- weight side
+@pytest.mark.parametrize("ab", AB_SPLITS)
+def test_weight_side_invariance_and_round_trip(ab):
+    """Eq. (1): (x T) . (w T^-T) = x . w, with the per-block inverse built as
+    A^-1 (x) B^-1 (Sec. 3.2); and transforming by (A, B) then by (A^-1, B^-1)
+    returns the input."""
+    a, b = ab
+    d = 1152
+    X = synth.activations(16, d, "normal", seed=18)
+    W = synth.activations(12, d, "normal", seed=19, chan_frac=0.0)
+    A, B = synth.factors(a, b, d // 32, seed=20)
+    _, _, y = oracle.quantize(X, A, B, want_y=True)
+    wt, wc, ws = oracle.weight_transform(W, A, B)
+    lhs = y.astype(np.float64) @ wt.astype(np.float64).T
+    xf = oracle.bf16_to_f32(X).astype(np.float64)
+    wf = oracle.bf16_to_f32(W).astype(np.float64)
+    rhs = xf @ wf.T
+    scale = np.abs(xf) @ np.abs(wf).T
+    assert np.max(np.abs(lhs - rhs) / scale) < 2e-5
+    # inverse transpose really is (A (x) B)^-T per block
+    Ait, Bit = oracle.factors_inverse_transpose(A, B)
+    Kinv = np.linalg.inv(oracle.kron_dense(A, B))
+    assert np.allclose(oracle.kron_dense(Ait, Bit), np.swapaxes(Kinv, -1, -2), atol=1e-5)
+    # round trip through the inverse factors
+    Ai = np.linalg.inv(A.astype(np.float64)).astype(np.float32)
+    Bi = np.linalg.inv(B.astype(np.float64)).astype(np.float32)
+    _, _, back = oracle.quantize_f32(y, Ai, Bi, want_y=True)
+    assert np.max(np.abs(back - xf)) <= 1e-5 * np.abs(xf).max()
+    assert wc.shape == (12, d // 2) and ws.shape == (12, d // 32)
+
+
+def test_rejects_bad_arguments():
+    X = np.zeros((2, 64), np.uint16)
+    A, B = synth.factors(4, 8, 1, seed=0)
+    with pytest.raises(ValueError):
+        oracle.quantize(X, A, np.eye(16, dtype=np.float32)[None])  # a*b != 32
+    with pytest.raises(ValueError):
+        oracle.quantize(np.zeros((2, 48), np.uint16), A, B)      # d % 32 != 0
+    c, s, _ = oracle.quantize(np.zeros((0, 64), np.uint16), A, B)
+    assert c.shape == (0, 32) and s.shape == (0, 2)
