@@ -1,0 +1,169 @@
+/*
+ * kroquant.h -- C ABI of libkroquant.so, the MI355X (gfx950) online activation
+ * quantizer of "KroQuant: Kronecker-Structured Block Transforms for Efficient
+ * Post-Training Quantization of Diffusion Transformers".
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Matrices are row-major and contiguous (leading dimension = number of
+ *    columns).  bf16 values are passed as their 16-bit patterns (uint16_t).
+ *  - d (columns) must be a positive multiple of 32: the quantizer works on
+ *    row-wise blocks of 32 elements (Sec. 3.1) and T is block-diagonal with
+ *    one 32x32 block per 32-column group (Sec. 3.1 "Goal").  Any M >= 0 is
+ *    accepted; M = 0 returns KQ_SUCCESS without touching the GPU.
+ *  - MXFP4 output layout, for an input of M rows:
+ *      codes  [M, d/2]  uint8: E2M1 codes (bit 3 = sign, bits 0-2 = index of
+ *                       the magnitude 0, .5, 1, 1.5, 2, 3, 4, 6), element 2i
+ *                       of a row in the low nibble of byte i, 2i+1 in the high;
+ *      scales [M, d/32] uint8: E8M0 byte s of block j, scale 2^(s - 127),
+ *                       s = max(floor(log2 amax) - 2 + 127, 0), 0 for an all-zero block.
+ *    Element values round to the nearest E2M1 magnitude of |y| / 2^(s-127),
+ *    ties to even, saturating at 6; a negative value that rounds to 0 keeps
+ *    its sign (code 8).  (OCP Microscaling v1.0 MXFP4, the format of Sec. 3.1.)
+ *  - Device pointers are plain HIP device (or managed) addresses; the caller
+ *    owns every buffer.  The quantize calls never allocate, free or
+ *    synchronize; they enqueue one kernel on `stream` (a hipStream_t; NULL =
+ *    the null stream) and return.  A fault inside the kernel surfaces at the
+ *    caller's next synchronization, as for any HIP launch.
+ *  - Alignment: X, codes and y_out must be 16-byte aligned; scales and the
+ *    factor / multiplier arrays need only their natural alignment (4 B for
+ *    fp32).
+ *  - Inputs must be finite; NaN or Inf inputs give unspecified codes.
+ *  - Arguments are validated before any HIP call.  On failure the call
+ *    returns the status and kq_last_error_detail() describes the argument
+ *    (thread-local).  HIP launch/runtime errors return KQ_ERROR_HIP with the
+ *    HIP error string in the detail.  No C++ exception crosses this ABI.
+ */
+#ifndef KROQUANT_H
+#define KROQUANT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum kq_status {
+    KQ_SUCCESS = 0,
+    KQ_ERROR_INVALID_VALUE = 1, /* a size or count is out of range            */
+    KQ_ERROR_NULL_POINTER = 2,  /* a required pointer is NULL                 */
+    KQ_ERROR_MISALIGNED = 3,    /* a pointer breaks the alignment rule above  */
+    KQ_ERROR_UNSUPPORTED = 4,   /* (a, b) split or factor count not supported */
+    KQ_ERROR_SINGULAR = 5,      /* a factor is singular or ill-conditioned    */
+    KQ_ERROR_HIP = 6            /* the HIP runtime reported an error          */
+} kq_status;
+
+/*
+ * kq_quantize -- the KroQuant online quantizer (Sec. 3.2 transform, Sec. 3.5
+ * kernels, Sec. 3.1 quantizer).  For every row r and 32-column block j of X:
+ *     y = (A_f (x) B_f) x,   x = X[r, 32j : 32j+32] widened to fp32,
+ * evaluated on the block reshaped row-major to a x b (Xm[p][q] = x[p*b+q]) as
+ * Ym = A_f . Xm . B_f^T, which is (A (x) B) vec(Xm^T) = vec(B Xm^T A^T); then
+ * MXFP4 of y into codes[r, 16j:16j+16] and scales[r, j].
+ *
+ *   X       device, bf16 [M, d]
+ *   A       device, fp32 [nfac, a, a] row-major; B device, fp32 [nfac, b, b]
+ *   (a, b)  one of (4, 8), (2, 16), (8, 4), (1, 32)
+ *   nfac    1 (one pair for every block) or d/32 (pair f = j for block j:
+ *           T = diag(K^(1), ..., K^(d/32)), Sec. 3.1)
+ *   codes   device, uint8 [M, d/2];  scales device, uint8 [M, d/32]
+ *   y_out   device, fp32 [M, d] or NULL: the transformed values that were
+ *           quantized
+ *
+ * Arithmetic: fp32, in the order
+ *     Z[p][i] = B[i][0]*Xm[p][0],  Z[p][i] = fma(B[i][q], Xm[p][q], Z[p][i]) for q = 1..b-1,
+ *     Y[o][i] = A[o][0]*Z[0][i],   Y[o][i] = fma(A[o][p], Z[p][i], Y[o][i])  for p = 1..a-1.
+ * To apply the paper's right-multiplication A -> A T with K = G1 (x) ... (x) G5
+ * (eq. (1), Sec. 3.2), pass A (x) B = K^T; kq_lu_to_factors builds exactly that.
+ */
+kq_status kq_quantize(const uint16_t* X, int64_t M, int64_t d, const float* A, const float* B,
+                      int a, int b, int64_t nfac, uint8_t* codes, uint8_t* scales, float* y_out,
+                      void* stream);
+
+/*
+ * kq_smoothquant_quantize -- SmoothQuant comparator (per-channel scaling, the
+ * "Scale" kernel of Sec. 4.4; smoothing vector of Appendix D): y_c = x_c *
+ * mult_c, one fp32 multiply, then MXFP4 as above.  mult is device fp32 [d]
+ * holding the multipliers 1/s_c (the activation is divided by the smoothing
+ * factor s_c).
+ */
+kq_status kq_smoothquant_quantize(const uint16_t* X, int64_t M, int64_t d, const float* mult,
+                                  uint8_t* codes, uint8_t* scales, float* y_out, void* stream);
+
+/*
+ * kq_hadamard32_quantize -- fixed block Hadamard comparator (Sec. 1; the
+ * Hadamard initialization of Sec. 3.2 and the ablation of Sec. 4.3):
+ * y = H32 x / sqrt(32) per block, H32 the Sylvester matrix, computed in fp32
+ * by add/subtract butterflies with strides 1, 2, 4, 8, 16 and one final
+ * multiply by fp32(1/sqrt(32)); then MXFP4.
+ */
+kq_status kq_hadamard32_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes,
+                                 uint8_t* scales, float* y_out, void* stream);
+
+/*
+ * kq_mxfp4_quantize -- the bare MXFP4 quantizer ("Q4", the lower bound of
+ * Sec. 4.4): y = x, then MXFP4.
+ */
+kq_status kq_mxfp4_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes,
+                            uint8_t* scales, void* stream);
+
+/*
+ * kq_e2m1_encode -- the element-encode step alone, for checking the device
+ * conversion: codes[i] = code(v[2i]) | code(v[2i+1]) << 4 at E8M0 byte s
+ * (0..254), with the rounding rule above.  v device fp32 [n], n even;
+ * codes device uint8 [n/2] (4-byte aligned).
+ */
+kq_status kq_e2m1_encode(const float* v, int64_t n, int s, uint8_t* codes, void* stream);
+
+/*
+ * kq_weight_transform -- offline weight side (Sec. 3.4, eq. (1)):
+ * W~ = W T^-T, i.e. per block w' = (A_f (x) B_f)^-T w = (A_f^-T (x) B_f^-T) w,
+ * using (A (x) B)^-1 = A^-1 (x) B^-1 (Sec. 3.2).
+ *   W        device bf16 [o, d];  A_host / B_host: HOST fp32 forward factors
+ *            ([nfac, a, a], [nfac, b, b]) as for kq_quantize
+ *   W_out    device fp32 [o, d] (required)
+ *   codes, scales  device, optional (both NULL or both set): MXFP4 of W~
+ * The factors are inverted on the host in fp64 (Gauss-Jordan, partial
+ * pivoting), transposed and rounded to fp32; then the kq_quantize kernel
+ * applies them.  Returns KQ_ERROR_SINGULAR if a pivot is below 1e-12 times
+ * its row's infinity norm or a factor's infinity-norm condition number
+ * exceeds 1e6.  Allocates a small device buffer for the inverted factors and
+ * synchronizes `stream` before returning (offline call).
+ */
+kq_status kq_weight_transform(const uint16_t* W, int64_t o, int64_t d, const float* A_host,
+                              const float* B_host, int a, int b, int64_t nfac, float* W_out,
+                              uint8_t* codes, uint8_t* scales, void* stream);
+
+/*
+ * kq_factors_inverse_transpose -- host helper: A_it[f] = fp32(inv(A[f])^T),
+ * B_it[f] = fp32(inv(B[f])^T) with fp64 Gauss-Jordan and partial pivoting;
+ * all arrays are HOST memory.  Same singularity rule as kq_weight_transform.
+ */
+kq_status kq_factors_inverse_transpose(const float* A, const float* B, int a, int b,
+                                       int64_t nfac, float* A_it, float* B_it);
+
+/*
+ * kq_lu_to_factors -- host helper for the unit-determinant LU parametrization
+ * of Sec. 3.2: abc holds, per block, the 15 parameters (a_k, b_k, c_k) for
+ * k = 1..5 (HOST fp32 [nfac, 5, 3]); G_k = [[1,0],[c_k,1]] . [[a_k,b_k],[0,-1/a_k]]
+ * and K = G1 (x) G2 (x) G3 (x) G4 (x) G5.  Writes HOST fp32 A [nfac, a, a],
+ * B [nfac, 32/a, 32/a] with A (x) B = K^T, so that kq_quantize applies the
+ * paper's x -> x K to every row block.  a in {1, 2, 4, 8}; a_k = 0 gives
+ * KQ_ERROR_SINGULAR.  Computed in fp64, rounded once to fp32.
+ */
+kq_status kq_lu_to_factors(const float* abc, int a, int64_t nfac, float* A, float* B);
+
+/* Stable name of a status ("KQ_SUCCESS", ...). Never NULL. */
+const char* kq_status_string(kq_status s);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* kq_last_error_detail(void);
+
+/* Library version: major * 10000 + minor * 100 + patch. */
+int kq_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KROQUANT_H */

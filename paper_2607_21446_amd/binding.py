@@ -1,0 +1,212 @@
+"""Thin Python binding of libkroquant.so (include/kroquant.h).
+
+Argument marshalling only: every step of the quantizer runs in the HIP
+kernels of the library.  torch supplies device memory and the current HIP
+stream.  There is no fallback: if the library is missing the first call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from functools import lru_cache
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkroquant.so")
+
+STATUS = {
+    0: "KQ_SUCCESS", 1: "KQ_ERROR_INVALID_VALUE", 2: "KQ_ERROR_NULL_POINTER", 3: "KQ_ERROR_MISALIGNED",
+    4: "KQ_ERROR_UNSUPPORTED", 5: "KQ_ERROR_SINGULAR", 6: "KQ_ERROR_HIP",
+}
+
+EXPORTED = (
+    "kq_quantize", "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_mxfp4_quantize",
+    "kq_e2m1_encode", "kq_weight_transform", "kq_factors_inverse_transpose", "kq_lu_to_factors",
+    "kq_status_string", "kq_last_error_detail", "kq_version",
+)
+
+
+class KQError(RuntimeError):
+    def __init__(self, status: int, detail: str, call: str):
+        self.status = status
+        self.name = STATUS.get(status, f"status {status}")
+        self.detail = detail
+        super().__init__(f"{call}: {self.name}: {detail}")
+
+
+@lru_cache(maxsize=1)
+def lib() -> ctypes.CDLL:
+    """Load libkroquant.so (built in-tree by __graft_entry__.build())."""
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"libkroquant.so not found at {_LIB_PATH}; build it first "
+                          "(python -m paper_2607_21446_amd._build)")
+    L = ctypes.CDLL(_LIB_PATH)
+    P, I64, I, F = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
+    L.kq_quantize.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P]
+    L.kq_smoothquant_quantize.argtypes = [P, I64, I64, P, P, P, P, P]
+    L.kq_hadamard32_quantize.argtypes = [P, I64, I64, P, P, P, P]
+    L.kq_mxfp4_quantize.argtypes = [P, I64, I64, P, P, P]
+    L.kq_e2m1_encode.argtypes = [P, I64, I, P, P]
+    L.kq_weight_transform.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P]
+    L.kq_factors_inverse_transpose.argtypes = [P, P, I, I, I64, P, P]
+    L.kq_lu_to_factors.argtypes = [P, I, I64, P, P]
+    for name in EXPORTED[:8]:
+        getattr(L, name).restype = ctypes.c_int
+    L.kq_status_string.argtypes = [I]
+    L.kq_status_string.restype = ctypes.c_char_p
+    L.kq_last_error_detail.argtypes = []
+    L.kq_last_error_detail.restype = ctypes.c_char_p
+    L.kq_version.argtypes = []
+    L.kq_version.restype = ctypes.c_int
+    del F
+    return L
+
+
+def _check(status: int, call: str):
+    if status != 0:
+        raise KQError(status, lib().kq_last_error_detail().decode(), call)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _need(t, dtype, name, device=True):
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if device and not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _outputs(X, codes, scales, y, want_y):
+    M, d = X.shape
+    if codes is None:
+        codes = torch.empty((M, d // 2), dtype=torch.uint8, device=X.device)
+    if scales is None:
+        scales = torch.empty((M, d // 32), dtype=torch.uint8, device=X.device)
+    if y is None and want_y:
+        y = torch.empty((M, d), dtype=torch.float32, device=X.device)
+    _need(codes, torch.uint8, "codes")
+    _need(scales, torch.uint8, "scales")
+    if y is not None:
+        _need(y, torch.float32, "y")
+    return codes, scales, y
+
+
+def quantize(X, A, B, codes=None, scales=None, y=None, want_y=False, stream=None):
+    """KroQuant quantizer kq_quantize: X bf16 [M, d]; A [nfac, a, a] and
+    B [nfac, b, b] fp32 device tensors.  Returns (codes, scales, y or None)."""
+    _need(X, torch.bfloat16, "X")
+    _need(A, torch.float32, "A")
+    _need(B, torch.float32, "B")
+    a, b = A.shape[-1], B.shape[-1]
+    nfac = A.numel() // (a * a)
+    codes, scales, y = _outputs(X, codes, scales, y, want_y)
+    M, d = X.shape
+    _check(lib().kq_quantize(_ptr(X), M, d, _ptr(A), _ptr(B), a, b, nfac, _ptr(codes), _ptr(scales),
+                             _ptr(y), _stream(stream)), "kq_quantize")
+    return codes, scales, y
+
+
+def smoothquant(X, mult, codes=None, scales=None, y=None, want_y=False, stream=None):
+    """SmoothQuant comparator kq_smoothquant_quantize; mult fp32 [d] = 1/s."""
+    _need(X, torch.bfloat16, "X")
+    _need(mult, torch.float32, "mult")
+    codes, scales, y = _outputs(X, codes, scales, y, want_y)
+    M, d = X.shape
+    _check(lib().kq_smoothquant_quantize(_ptr(X), M, d, _ptr(mult), _ptr(codes), _ptr(scales), _ptr(y),
+                                         _stream(stream)), "kq_smoothquant_quantize")
+    return codes, scales, y
+
+
+def hadamard32(X, codes=None, scales=None, y=None, want_y=False, stream=None):
+    """Hadamard-32 comparator kq_hadamard32_quantize."""
+    _need(X, torch.bfloat16, "X")
+    codes, scales, y = _outputs(X, codes, scales, y, want_y)
+    M, d = X.shape
+    _check(lib().kq_hadamard32_quantize(_ptr(X), M, d, _ptr(codes), _ptr(scales), _ptr(y), _stream(stream)),
+           "kq_hadamard32_quantize")
+    return codes, scales, y
+
+
+def mxfp4(X, codes=None, scales=None, stream=None):
+    """Plain MXFP4 kq_mxfp4_quantize."""
+    _need(X, torch.bfloat16, "X")
+    codes, scales, _ = _outputs(X, codes, scales, None, False)
+    M, d = X.shape
+    _check(lib().kq_mxfp4_quantize(_ptr(X), M, d, _ptr(codes), _ptr(scales), _stream(stream)),
+           "kq_mxfp4_quantize")
+    return codes, scales
+
+
+def e2m1_encode(v, s, codes=None, stream=None):
+    """Element encode kq_e2m1_encode: v fp32 [n] -> codes uint8 [n/2]."""
+    _need(v, torch.float32, "v")
+    n = v.numel()
+    if codes is None:
+        codes = torch.empty(n // 2, dtype=torch.uint8, device=v.device)
+    _check(lib().kq_e2m1_encode(_ptr(v), n, int(s), _ptr(codes), _stream(stream)), "kq_e2m1_encode")
+    return codes
+
+
+def weight_transform(W, A_host, B_host, W_out=None, codes=None, scales=None, quantize=True, stream=None):
+    """Offline weight side kq_weight_transform: W bf16 [o, d] on the device;
+    A_host, B_host CPU fp32 tensors (forward factors).  Synchronizes."""
+    _need(W, torch.bfloat16, "W")
+    A_host = A_host.detach().to("cpu", torch.float32).contiguous()
+    B_host = B_host.detach().to("cpu", torch.float32).contiguous()
+    a, b = A_host.shape[-1], B_host.shape[-1]
+    nfac = A_host.numel() // (a * a)
+    o, d = W.shape
+    if W_out is None:
+        W_out = torch.empty((o, d), dtype=torch.float32, device=W.device)
+    if quantize:
+        codes, scales, _ = _outputs(W, codes, scales, None, False)
+    _check(lib().kq_weight_transform(_ptr(W), o, d, _ptr(A_host), _ptr(B_host), a, b, nfac, _ptr(W_out),
+                                     _ptr(codes), _ptr(scales), _stream(stream)), "kq_weight_transform")
+    return W_out, codes, scales
+
+
+def factors_inverse_transpose(A, B):
+    """Host helper kq_factors_inverse_transpose on CPU fp32 tensors."""
+    A = A.detach().to("cpu", torch.float32).contiguous()
+    B = B.detach().to("cpu", torch.float32).contiguous()
+    a, b = A.shape[-1], B.shape[-1]
+    nfac = A.numel() // (a * a)
+    Ait, Bit = torch.empty_like(A), torch.empty_like(B)
+    _check(lib().kq_factors_inverse_transpose(_ptr(A), _ptr(B), a, b, nfac, _ptr(Ait), _ptr(Bit)),
+           "kq_factors_inverse_transpose")
+    return Ait, Bit
+
+
+def lu_to_factors(abc, a):
+    """Host helper kq_lu_to_factors: abc CPU fp32 [nfac, 5, 3] -> (A, B)."""
+    abc = abc.detach().to("cpu", torch.float32).contiguous()
+    nfac = abc.numel() // 15
+    b = 32 // a
+    A = torch.empty((nfac, a, a), dtype=torch.float32)
+    B = torch.empty((nfac, b, b), dtype=torch.float32)
+    _check(lib().kq_lu_to_factors(_ptr(abc), int(a), nfac, _ptr(A), _ptr(B)), "kq_lu_to_factors")
+    return A, B
+
+
+def status_string(status: int) -> str:
+    return lib().kq_status_string(int(status)).decode()
+
+
+def version() -> int:
+    return int(lib().kq_version())

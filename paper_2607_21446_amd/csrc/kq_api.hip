@@ -1,0 +1,326 @@
+// C ABI of libkroquant.so: argument validation, dispatch to the kernels and
+// the host-side helpers of the offline weight path.  See include/kroquant.h
+// for the contract of every entry point.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "kq_kernels.h"
+#include "kroquant.h"
+
+namespace {
+
+thread_local std::string g_detail;
+
+kq_status fail(kq_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_detail = buf;
+    return st;
+}
+
+kq_status ok() {
+    g_detail.clear();
+    return KQ_SUCCESS;
+}
+
+kq_status from_hip(hipError_t e, const char* what) {
+    if (e == hipSuccess) return ok();
+    return fail(KQ_ERROR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+
+bool supported_split(int a, int b) {
+    return (a == 4 && b == 8) || (a == 2 && b == 16) || (a == 8 && b == 4) || (a == 1 && b == 32);
+}
+
+// Shape and output checks common to every quantize entry point.
+kq_status check_common(const void* X, int64_t M, int64_t d, const void* codes, const void* scales,
+                       const void* y, bool codes_required) {
+    if (M < 0) return fail(KQ_ERROR_INVALID_VALUE, "M = %lld must be >= 0", (long long)M);
+    if (d <= 0 || d % 32 != 0)
+        return fail(KQ_ERROR_INVALID_VALUE, "d = %lld must be a positive multiple of 32", (long long)d);
+    if (M > 0 && d > INT64_MAX / 4 / M)
+        return fail(KQ_ERROR_INVALID_VALUE, "M * d = %lld * %lld is too large", (long long)M, (long long)d);
+    if (!X) return fail(KQ_ERROR_NULL_POINTER, "X is NULL");
+    if (codes_required && (!codes || !scales))
+        return fail(KQ_ERROR_NULL_POINTER, "codes and scales must not be NULL");
+    if (!codes_required && ((codes == nullptr) != (scales == nullptr)))
+        return fail(KQ_ERROR_NULL_POINTER, "codes and scales must be both NULL or both set");
+    if (!aligned(X, 16)) return fail(KQ_ERROR_MISALIGNED, "X must be 16-byte aligned");
+    if (codes && !aligned(codes, 16)) return fail(KQ_ERROR_MISALIGNED, "codes must be 16-byte aligned");
+    if (y && !aligned(y, 16)) return fail(KQ_ERROR_MISALIGNED, "y_out must be 16-byte aligned");
+    return ok();
+}
+
+kq::Params make_params(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, uint8_t* scales, float* y) {
+    kq::Params p{};
+    p.X = X;
+    p.M = M;
+    p.d = d;
+    p.nb = d / 32;
+    p.nblocks = M * (d / 32);
+    p.nfac = 1;
+    p.codes = codes;
+    p.scales = scales;
+    p.y = y;
+    return p;
+}
+
+kq::LaunchConfig default_config() {
+    kq::LaunchConfig c;
+    c.blocks_per_lane = 1;
+    c.max_blocks = 1 << 20;
+    return c;
+}
+
+// fp64 Gauss-Jordan inverse with partial pivoting of an n x n fp32 matrix.
+// Returns false if a pivot is below 1e-12 times the infinity norm of its row
+// or if the infinity-norm condition number exceeds 1e6.
+bool invert(const float* A, int n, double* inv, std::string& why) {
+    std::vector<double> m(n * 2 * n, 0.0);
+    double norm_a = 0.0;
+    for (int i = 0; i < n; ++i) {
+        double row = 0.0;
+        for (int j = 0; j < n; ++j) {
+            m[i * 2 * n + j] = A[i * n + j];
+            row += std::fabs((double)A[i * n + j]);
+        }
+        norm_a = std::max(norm_a, row);
+        m[i * 2 * n + n + i] = 1.0;
+    }
+    for (int c = 0; c < n; ++c) {
+        int piv = c;
+        for (int r = c + 1; r < n; ++r)
+            if (std::fabs(m[r * 2 * n + c]) > std::fabs(m[piv * 2 * n + c])) piv = r;
+        double rownorm = 0.0;
+        for (int j = 0; j < n; ++j) rownorm = std::max(rownorm, std::fabs(m[piv * 2 * n + j]));
+        const double pv = m[piv * 2 * n + c];
+        if (!(std::fabs(pv) > 1e-12 * rownorm)) {
+            why = "zero or tiny pivot";
+            return false;
+        }
+        if (piv != c)
+            for (int j = 0; j < 2 * n; ++j) std::swap(m[c * 2 * n + j], m[piv * 2 * n + j]);
+        for (int j = 0; j < 2 * n; ++j) m[c * 2 * n + j] /= pv;
+        for (int r = 0; r < n; ++r) {
+            if (r == c) continue;
+            const double f = m[r * 2 * n + c];
+            if (f == 0.0) continue;
+            for (int j = 0; j < 2 * n; ++j) m[r * 2 * n + j] -= f * m[c * 2 * n + j];
+        }
+    }
+    double norm_i = 0.0;
+    for (int i = 0; i < n; ++i) {
+        double row = 0.0;
+        for (int j = 0; j < n; ++j) {
+            inv[i * n + j] = m[i * 2 * n + n + j];
+            row += std::fabs(inv[i * n + j]);
+        }
+        norm_i = std::max(norm_i, row);
+    }
+    if (!(norm_a * norm_i <= 1e6)) {
+        why = "condition number above 1e6";
+        return false;
+    }
+    return true;
+}
+
+kq_status inverse_transpose(const float* F, int n, int64_t nfac, float* out, const char* name) {
+    std::vector<double> inv(n * n);
+    std::string why;
+    for (int64_t f = 0; f < nfac; ++f) {
+        if (!invert(F + f * n * n, n, inv.data(), why))
+            return fail(KQ_ERROR_SINGULAR, "%s[%lld]: %s", name, (long long)f, why.c_str());
+        for (int i = 0; i < n; ++i)
+            for (int j = 0; j < n; ++j) out[f * n * n + i * n + j] = (float)inv[j * n + i];
+    }
+    return ok();
+}
+
+kq_status check_factors(int a, int b, int64_t nfac, int64_t d) {
+    if (!supported_split(a, b))
+        return fail(KQ_ERROR_UNSUPPORTED, "(a, b) = (%d, %d) is not one of (4,8), (2,16), (8,4), (1,32)", a, b);
+    if (nfac != 1 && nfac != d / 32)
+        return fail(KQ_ERROR_UNSUPPORTED, "nfac = %lld must be 1 or d/32 = %lld", (long long)nfac,
+                    (long long)(d / 32));
+    return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+kq_status kq_quantize(const uint16_t* X, int64_t M, int64_t d, const float* A, const float* B, int a,
+                      int b, int64_t nfac, uint8_t* codes, uint8_t* scales, float* y_out, void* stream) {
+    kq_status st = check_common(X, M, d, codes, scales, y_out, true);
+    if (st != KQ_SUCCESS) return st;
+    if ((st = check_factors(a, b, nfac, d)) != KQ_SUCCESS) return st;
+    if (!A || !B) return fail(KQ_ERROR_NULL_POINTER, "A and B must not be NULL");
+    if (!aligned(A, 4) || !aligned(B, 4)) return fail(KQ_ERROR_MISALIGNED, "A and B must be 4-byte aligned");
+    if (M == 0) return ok();
+    kq::Params p = make_params(X, M, d, codes, scales, y_out);
+    p.A = A;
+    p.B = B;
+    p.nfac = nfac;
+    const kq::Mapping map = (nfac == 1) ? kq::Mapping::Flat : kq::Mapping::Column;
+    return from_hip(kq::launch(kq::Kind::Kron, a, p, map, (hipStream_t)stream, default_config()), "kq_quantize");
+}
+
+kq_status kq_smoothquant_quantize(const uint16_t* X, int64_t M, int64_t d, const float* mult, uint8_t* codes,
+                                  uint8_t* scales, float* y_out, void* stream) {
+    kq_status st = check_common(X, M, d, codes, scales, y_out, true);
+    if (st != KQ_SUCCESS) return st;
+    if (!mult) return fail(KQ_ERROR_NULL_POINTER, "mult must not be NULL");
+    if (!aligned(mult, 16)) return fail(KQ_ERROR_MISALIGNED, "mult must be 16-byte aligned");
+    if (M == 0) return ok();
+    kq::Params p = make_params(X, M, d, codes, scales, y_out);
+    p.mult = mult;
+    return from_hip(kq::launch(kq::Kind::Smooth, 0, p, kq::Mapping::Flat, (hipStream_t)stream, default_config()),
+                    "kq_smoothquant_quantize");
+}
+
+kq_status kq_hadamard32_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, uint8_t* scales,
+                                 float* y_out, void* stream) {
+    kq_status st = check_common(X, M, d, codes, scales, y_out, true);
+    if (st != KQ_SUCCESS) return st;
+    if (M == 0) return ok();
+    kq::Params p = make_params(X, M, d, codes, scales, y_out);
+    return from_hip(kq::launch(kq::Kind::Hadamard, 0, p, kq::Mapping::Flat, (hipStream_t)stream, default_config()),
+                    "kq_hadamard32_quantize");
+}
+
+kq_status kq_mxfp4_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, uint8_t* scales,
+                            void* stream) {
+    kq_status st = check_common(X, M, d, codes, scales, nullptr, true);
+    if (st != KQ_SUCCESS) return st;
+    if (M == 0) return ok();
+    kq::Params p = make_params(X, M, d, codes, scales, nullptr);
+    return from_hip(kq::launch(kq::Kind::Plain, 0, p, kq::Mapping::Flat, (hipStream_t)stream, default_config()),
+                    "kq_mxfp4_quantize");
+}
+
+kq_status kq_e2m1_encode(const float* v, int64_t n, int s, uint8_t* codes, void* stream) {
+    if (n < 0 || n % 2 != 0) return fail(KQ_ERROR_INVALID_VALUE, "n = %lld must be even and >= 0", (long long)n);
+    if (s < 0 || s > 254) return fail(KQ_ERROR_INVALID_VALUE, "s = %d must be in [0, 254]", s);
+    if (n == 0) return ok();
+    if (!v || !codes) return fail(KQ_ERROR_NULL_POINTER, "v and codes must not be NULL");
+    if (!aligned(v, 8)) return fail(KQ_ERROR_MISALIGNED, "v must be 8-byte aligned");
+    return from_hip(kq::launch_e2m1(v, n / 2, (uint32_t)s, codes, (hipStream_t)stream), "kq_e2m1_encode");
+}
+
+kq_status kq_factors_inverse_transpose(const float* A, const float* B, int a, int b, int64_t nfac, float* A_it,
+                                       float* B_it) {
+    if (!supported_split(a, b))
+        return fail(KQ_ERROR_UNSUPPORTED, "(a, b) = (%d, %d) is not one of (4,8), (2,16), (8,4), (1,32)", a, b);
+    if (nfac < 1) return fail(KQ_ERROR_INVALID_VALUE, "nfac = %lld must be >= 1", (long long)nfac);
+    if (!A || !B || !A_it || !B_it) return fail(KQ_ERROR_NULL_POINTER, "factor pointers must not be NULL");
+    kq_status st = inverse_transpose(A, a, nfac, A_it, "A");
+    if (st != KQ_SUCCESS) return st;
+    return inverse_transpose(B, b, nfac, B_it, "B");
+}
+
+kq_status kq_weight_transform(const uint16_t* W, int64_t o, int64_t d, const float* A_host, const float* B_host,
+                              int a, int b, int64_t nfac, float* W_out, uint8_t* codes, uint8_t* scales,
+                              void* stream) {
+    kq_status st = check_common(W, o, d, codes, scales, W_out, false);
+    if (st != KQ_SUCCESS) return st;
+    if ((st = check_factors(a, b, nfac, d)) != KQ_SUCCESS) return st;
+    if (!W_out) return fail(KQ_ERROR_NULL_POINTER, "W_out must not be NULL");
+    if (!A_host || !B_host) return fail(KQ_ERROR_NULL_POINTER, "A_host and B_host must not be NULL");
+    std::vector<float> Ait(nfac * a * a), Bit(nfac * b * b);
+    if ((st = inverse_transpose(A_host, a, nfac, Ait.data(), "A")) != KQ_SUCCESS) return st;
+    if ((st = inverse_transpose(B_host, b, nfac, Bit.data(), "B")) != KQ_SUCCESS) return st;
+    if (o == 0) return ok();
+    hipStream_t s = (hipStream_t)stream;
+    const size_t bytesA = Ait.size() * sizeof(float), bytesB = Bit.size() * sizeof(float);
+    float* dev = nullptr;
+    hipError_t e = hipMalloc(&dev, bytesA + bytesB);
+    if (e != hipSuccess) return from_hip(e, "kq_weight_transform: hipMalloc");
+    e = hipMemcpyAsync(dev, Ait.data(), bytesA, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(dev + Ait.size(), Bit.data(), bytesB, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) {
+        kq::Params p = make_params(W, o, d, codes, scales, W_out);
+        p.A = dev;
+        p.B = dev + Ait.size();
+        p.nfac = nfac;
+        const kq::Mapping map = (nfac == 1) ? kq::Mapping::Flat : kq::Mapping::Column;
+        e = kq::launch(kq::Kind::Kron, a, p, map, s, default_config());
+    }
+    // the host vectors and the device buffer must outlive the queued work
+    const hipError_t es = hipStreamSynchronize(s);
+    if (e == hipSuccess) e = es;
+    const hipError_t ef = hipFree(dev);
+    if (e == hipSuccess) e = ef;
+    return from_hip(e, "kq_weight_transform");
+}
+
+kq_status kq_lu_to_factors(const float* abc, int a, int64_t nfac, float* A, float* B) {
+    if (a != 1 && a != 2 && a != 4 && a != 8) return fail(KQ_ERROR_UNSUPPORTED, "a = %d must be 1, 2, 4 or 8", a);
+    if (nfac < 1) return fail(KQ_ERROR_INVALID_VALUE, "nfac = %lld must be >= 1", (long long)nfac);
+    if (!abc || !A || !B) return fail(KQ_ERROR_NULL_POINTER, "abc, A and B must not be NULL");
+    const int b = 32 / a;
+    const int na = (a == 1) ? 0 : (a == 2) ? 1 : (a == 4) ? 2 : 3;
+    for (int64_t f = 0; f < nfac; ++f) {
+        double G[5][2][2];
+        for (int k = 0; k < 5; ++k) {
+            const double ak = abc[f * 15 + 3 * k], bk = abc[f * 15 + 3 * k + 1], ck = abc[f * 15 + 3 * k + 2];
+            if (ak == 0.0) return fail(KQ_ERROR_SINGULAR, "block %lld: a_%d = 0", (long long)f, k + 1);
+            // L = [[1,0],[c,1]], U = [[a,b],[0,-1/a]]:  G = L U
+            G[k][0][0] = ak;
+            G[k][0][1] = bk;
+            G[k][1][0] = ck * ak;
+            G[k][1][1] = ck * bk - 1.0 / ak;
+        }
+        // Kronecker entries: (G_1 (x) .. (x) G_n)[r][c] = prod_k G_k[bit_(n-k)(r)][bit_(n-k)(c)];
+        // the library factors are the transposes (A (x) B = K^T).
+        for (int r = 0; r < a; ++r)
+            for (int c = 0; c < a; ++c) {
+                double v = 1.0;
+                for (int k = 0; k < na; ++k) {
+                    const int sh = na - 1 - k;
+                    v *= G[k][(r >> sh) & 1][(c >> sh) & 1];
+                }
+                A[f * a * a + c * a + r] = (float)v;
+            }
+        const int nbits = 5 - na;
+        for (int r = 0; r < b; ++r)
+            for (int c = 0; c < b; ++c) {
+                double v = 1.0;
+                for (int k = 0; k < nbits; ++k) {
+                    const int sh = nbits - 1 - k;
+                    v *= G[na + k][(r >> sh) & 1][(c >> sh) & 1];
+                }
+                B[f * b * b + c * b + r] = (float)v;
+            }
+    }
+    return ok();
+}
+
+const char* kq_status_string(kq_status s) {
+    switch (s) {
+        case KQ_SUCCESS: return "KQ_SUCCESS";
+        case KQ_ERROR_INVALID_VALUE: return "KQ_ERROR_INVALID_VALUE";
+        case KQ_ERROR_NULL_POINTER: return "KQ_ERROR_NULL_POINTER";
+        case KQ_ERROR_MISALIGNED: return "KQ_ERROR_MISALIGNED";
+        case KQ_ERROR_UNSUPPORTED: return "KQ_ERROR_UNSUPPORTED";
+        case KQ_ERROR_SINGULAR: return "KQ_ERROR_SINGULAR";
+        case KQ_ERROR_HIP: return "KQ_ERROR_HIP";
+    }
+    return "KQ_ERROR_UNKNOWN";
+}
+
+const char* kq_last_error_detail(void) { return g_detail.c_str(); }
+
+int kq_version(void) { return 100; }
+
+}  // extern "C"

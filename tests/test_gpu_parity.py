@@ -1,0 +1,296 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle on the
+same seeded inputs.
+
+Bar (stricter than the tolerance the method needs, because the kernels keep
+the oracle's fp32 evaluation order): E8M0 scales, packed E2M1 codes and the
+fp32 transformed values are bit-identical.  `assert_mx_close` holds the looser
+bar for paths whose arithmetic order differs (the offline weight side, where
+the fp64 factor inverse comes from a different routine): scales bit-exact,
+codes bit-exact except adjacent-magnitude flips at rounding ties (at most 1e-4
+of the codes), fp32 values within 1e-5 relative error measured against
+max(|y_ref|, amax_block / 32).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+torch = pytest.importorskip("torch")
+kq = pytest.importorskip("paper_2607_21446_amd")
+
+pytestmark = pytest.mark.gpu
+
+AB_SPLITS = [(4, 8), (2, 16), (8, 4), (1, 32)]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    kq.lib()
+    yield
+
+
+def dev_bf16(X):
+    return torch.from_numpy(np.ascontiguousarray(X).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def dev_f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def assert_exact(got, want, what=""):
+    cg, sg, yg = got
+    cr, sr, yr = want
+    assert np.array_equal(sg, sr), f"{what}: scales differ at {np.argwhere(sg != sr)[:5].tolist()}"
+    assert np.array_equal(cg, cr), f"{what}: codes differ at {np.argwhere(cg != cr)[:5].tolist()}"
+    if yr is not None:
+        assert np.array_equal(yg.view(np.uint32), yr.view(np.uint32)), f"{what}: y differs"
+
+
+def assert_mx_close(got, want, what=""):
+    cg, sg, yg = got
+    cr, sr, yr = want
+    assert np.array_equal(sg, sr), f"{what}: scale mismatch"
+    ug, ur = oracle.unpack_codes(cg), oracle.unpack_codes(cr)
+    bad = ug != ur
+    if bad.any():
+        dmag = np.abs((ug[bad] & 7).astype(int) - (ur[bad] & 7).astype(int))
+        sign_only = ((ug[bad] & 7) == 0) & ((ur[bad] & 7) == 0)
+        assert np.all((dmag == 1) | sign_only), f"{what}: non-adjacent code flip"
+        assert bad.mean() <= 1e-4, f"{what}: {bad.mean():.2e} of codes flipped"
+    if yr is not None:
+        amax = np.abs(yr).reshape(yr.shape[0], -1, 32).max(-1)
+        den = np.maximum(np.abs(yr), np.repeat(amax, 32, axis=1) / 32.0)
+        den = np.where(den > 0, den, 1.0)
+        assert np.max(np.abs(yg.astype(np.float64) - yr) / den) <= 1e-5, f"{what}: y error"
+
+
+def gpu_quantize(X, A, B, want_y=True):
+    codes, scales, y = kq.quantize(dev_bf16(X), dev_f32(A), dev_f32(B), want_y=want_y)
+    return host(codes), host(scales), (host(y) if want_y else None)
+
+
+# ------------------------------------------------------------------ element encode
+def test_e2m1_convert_exhaustive():
+    """Every fp32 bit pattern with |v| <= 8 through the device convert at
+    scale 2^0, against the oracle's nearest-magnitude rule."""
+    hi = int(np.float32(8.0).view(np.uint32)) + 1
+    chunk = 1 << 26
+    for sign in (0, 1):
+        for start in range(0, hi, chunk):
+            n = min(chunk, hi - start)
+            n += n % 2
+            bits = torch.arange(start, start + n, dtype=torch.int64, device="cuda")
+            bits = torch.clamp(bits, max=hi - 1).to(torch.int32)
+            if sign:
+                bits = bits | torch.tensor(-(1 << 31), dtype=torch.int32, device="cuda")
+            v = bits.view(torch.float32)
+            got = oracle.unpack_codes(host(kq.e2m1_encode(v, 127)))
+            want = oracle.e2m1_codes(host(v), 127)
+            assert np.array_equal(got, want), f"sign {sign} chunk {start:#x}"
+
+
+@pytest.mark.parametrize("s", [0, 1, 2, 3, 100, 126, 128, 200, 252, 254])
+def test_e2m1_convert_other_scales(s):
+    rng = np.random.default_rng(s)
+    mags = rng.random(1 << 20) * 8.0 * np.exp2(s - 127.0)
+    v = (mags * np.where(rng.random(1 << 20) < 0.5, -1, 1))
+    v = np.clip(v, -np.finfo(np.float32).max, np.finfo(np.float32).max).astype(np.float32)
+    got = oracle.unpack_codes(host(kq.e2m1_encode(dev_f32(v), s)))
+    assert np.array_equal(got, oracle.e2m1_codes(v, s))
+
+
+# ------------------------------------------------------------------ small shapes, every variant
+@pytest.mark.parametrize("ab", AB_SPLITS)
+@pytest.mark.parametrize("per_block", [False, True])
+@pytest.mark.parametrize("M,d", [(1, 32), (3, 64), (257, 1152), (64, 2240), (130, 3072)])
+def test_kroquant_parity(ab, per_block, M, d):
+    a, b = ab
+    X = synth.activations(M, d, "student_t3", seed=M * 7 + d, chan_frac=0.005, chan_factor=50)
+    A, B = synth.factors(a, b, d // 32 if per_block else 1, seed=d + a)
+    got = gpu_quantize(X, A, B)
+    want = oracle.quantize(X, A, B, want_y=True)
+    assert_exact(got, want, f"kron {ab} pb={per_block} {M}x{d}")
+
+
+@pytest.mark.parametrize("M,d", [(1, 32), (3, 64), (257, 1152), (64, 2240), (130, 5600)])
+def test_comparators_parity(M, d):
+    X = synth.activations(M, d, "laplace", seed=M + d, chan_frac=0.02, chan_factor=20)
+    Xd = dev_bf16(X)
+    mult = synth.smoothquant_multipliers(X)
+    c, s, y = kq.smoothquant(Xd, dev_f32(mult), want_y=True)
+    assert_exact((host(c), host(s), host(y)), oracle.smoothquant(X, mult, want_y=True), "smooth")
+    c, s, y = kq.hadamard32(Xd, want_y=True)
+    assert_exact((host(c), host(s), host(y)), oracle.hadamard32(X, want_y=True), "hadamard")
+    c, s = kq.mxfp4(Xd)
+    cr, sr = oracle.mxfp4(X)
+    assert_exact((host(c), host(s), None), (cr, sr, None), "mxfp4")
+
+
+def test_tiny_config_all_paths():
+    w = synth.workload("tiny_256x1152")
+    assert_exact(gpu_quantize(w.X, w.A, w.B), oracle.quantize(w.X, w.A, w.B, want_y=True), "tiny")
+
+
+# ------------------------------------------------------------------ edge blocks
+def _edge_matrix():
+    rows = []
+    f = np.float32
+    rows.append(np.zeros(64, f))                                            # all zero
+    rows.append(np.concatenate([np.full(32, -0.0, f), np.zeros(32, f)]))     # -0.0 inputs
+    sub = (np.arange(64, dtype=np.uint32) % 127 + 1).astype(np.uint32)      # bf16 subnormals
+    rows.append((sub << 16).view(np.float32) * np.where(np.arange(64) % 3, 1, -1).astype(f))
+    ties = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0, 6.0] * 8, f)     # exact ties at s = 127
+    ties[0] = 6.0
+    rows.append(ties * np.where(np.arange(64) % 2, -1, 1).astype(f))
+    sat = np.full(64, 7.0, f)                                               # saturation
+    sat[0] = 7.5
+    rows.append(sat)
+    big = np.zeros(64, f)
+    big[5] = np.float32((np.uint32(0x7F7F) << 16).view(np.float32))         # largest finite bf16
+    big[40] = -big[5]
+    rows.append(big)
+    tiny = np.zeros(64, f)
+    tiny[3] = (np.uint32(1) << 16).view(np.float32)                        # smallest bf16 subnormal
+    rows.append(tiny)
+    return synth.to_bf16_bits(np.stack(rows))
+
+
+def test_edge_blocks_plain_smooth_hadamard():
+    X = _edge_matrix()
+    Xd = dev_bf16(X)
+    c, s = kq.mxfp4(Xd)
+    cr, sr = oracle.mxfp4(X)
+    assert_exact((host(c), host(s), None), (cr, sr, None), "mxfp4 edges")
+    one = np.ones(64, np.float32)
+    c, s, y = kq.smoothquant(Xd, dev_f32(one), want_y=True)
+    assert_exact((host(c), host(s), host(y)), oracle.smoothquant(X, one, want_y=True), "smooth edges")
+    # Hadamard keeps a lone largest-bf16 value finite (/sqrt(32)); skip no row
+    c, s, y = kq.hadamard32(Xd, want_y=True)
+    assert_exact((host(c), host(s), host(y)), oracle.hadamard32(X, want_y=True), "hadamard edges")
+
+
+@pytest.mark.parametrize("ab", AB_SPLITS)
+def test_edge_blocks_kron(ab):
+    a, b = ab
+    X = _edge_matrix()
+    X = X[np.arange(X.shape[0]) != 5]  # an amplifying transform overflows the largest bf16
+    A, B = synth.factors(a, b, 2, seed=3)
+    assert_exact(gpu_quantize(X, A, B), oracle.quantize(X, A, B, want_y=True), f"kron edges {ab}")
+    # identity factors: plain MXFP4 (the -0.0 row excepted, products give +0.0)
+    Ai = np.eye(a, dtype=np.float32)[None]
+    Bi = np.eye(b, dtype=np.float32)[None]
+    keep = np.arange(X.shape[0]) != 1
+    c, s, _ = gpu_quantize(X[keep], Ai, Bi)
+    cr, sr = oracle.mxfp4(X[keep])
+    assert np.array_equal(c, cr) and np.array_equal(s, sr)
+
+
+# ------------------------------------------------------------------ layout, guards, determinism
+def test_guard_bands_and_full_coverage():
+    M, d = 77, 2240
+    X = synth.activations(M, d, "normal", seed=1)
+    A, B = synth.factors(4, 8, 1, seed=2)
+    want = oracle.quantize(X, A, B, want_y=True)
+    G = 4096
+    for canary in (0xA5, 0x5A):
+        cbuf = torch.full((M * d // 2 + 2 * G,), canary, dtype=torch.uint8, device="cuda")
+        sbuf = torch.full((M * d // 32 + 2 * G,), canary, dtype=torch.uint8, device="cuda")
+        ybuf = torch.full((M * d + 2 * G,), float("nan"), dtype=torch.float32, device="cuda")
+        codes = cbuf[G:G + M * d // 2].view(M, d // 2)
+        scales = sbuf[G:G + M * d // 32].view(M, d // 32)
+        y = ybuf[G:G + M * d].view(M, d)
+        kq.quantize(dev_bf16(X), dev_f32(A), dev_f32(B), codes=codes, scales=scales, y=y)
+        cb, sb, yb = host(cbuf), host(sbuf), host(ybuf)
+        assert np.all(cb[:G] == canary) and np.all(cb[-G:] == canary)
+        assert np.all(sb[:G] == canary) and np.all(sb[-G:] == canary)
+        assert np.all(np.isnan(yb[:G])) and np.all(np.isnan(yb[-G:]))
+        assert_exact((cb[G:-G].reshape(M, -1), sb[G:-G].reshape(M, -1), yb[G:-G].reshape(M, d)), want)
+
+
+def test_flat_and_column_mappings_agree():
+    """nfac = 1 runs the flat mapping, nfac = d/32 the column mapping: with
+    every per-block pair equal to the shared one they must agree bit for bit."""
+    M, d = 300, 3072
+    X = synth.activations(M, d, "student_t3", seed=4, chan_frac=0.005, chan_factor=50)
+    A, B = synth.factors(4, 8, 1, seed=6)
+    g1 = gpu_quantize(X, A, B)
+    g2 = gpu_quantize(X, np.repeat(A, d // 32, 0), np.repeat(B, d // 32, 0))
+    assert_exact(g1, g2)
+    g3 = gpu_quantize(X, A, B)
+    assert_exact(g1, g3)
+
+
+def test_non_default_stream():
+    M, d = 512, 3072
+    X = synth.activations(M, d, "normal", seed=9)
+    A, B = synth.factors(4, 8, 1, seed=10)
+    s = torch.cuda.Stream()
+    Xd, Ad, Bd = dev_bf16(X), dev_f32(A), dev_f32(B)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        c, sc, y = kq.quantize(Xd, Ad, Bd, want_y=True)
+    s.synchronize()
+    assert_exact((c.cpu().numpy(), sc.cpu().numpy(), y.cpu().numpy()), oracle.quantize(X, A, B, want_y=True))
+
+
+# ------------------------------------------------------------------ weight side
+@pytest.mark.parametrize("ab", AB_SPLITS)
+@pytest.mark.parametrize("per_block", [False, True])
+def test_weight_transform(ab, per_block):
+    a, b = ab
+    o, d = 96, 1152
+    W = synth.activations(o, d, "normal", seed=a * 3 + b, chan_frac=0.0)
+    A, B = synth.factors(a, b, d // 32 if per_block else 1, seed=a + 11)
+    Wt, c, s = kq.weight_transform(dev_bf16(W), torch.from_numpy(A), torch.from_numpy(B))
+    got = (host(c), host(s), host(Wt))
+    yr, cr, sr = oracle.weight_transform(W, A, B)
+    assert_mx_close(got, (cr, sr, yr), f"weight {ab}")
+    # eq. (1): <x T, w T^-T> = <x, w>
+    X = synth.activations(8, d, "normal", seed=5)
+    _, _, y = gpu_quantize(X, A, B)
+    lhs = y.astype(np.float64) @ got[2].astype(np.float64).T
+    xf, wf = oracle.bf16_to_f32(X).astype(np.float64), oracle.bf16_to_f32(W).astype(np.float64)
+    assert np.max(np.abs(lhs - xf @ wf.T) / (np.abs(xf) @ np.abs(wf).T)) < 2e-5
+
+
+# ------------------------------------------------------------------ full-size workloads
+FULL = ["pixart_8192x1152", "pixart_8192x4608", "sana_4096x2240", "sana_4096x5600", "flux_4608x3072",
+        "flux_4608x12288"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_workloads(name):
+    """Every output of the DiT-shaped workloads, KroQuant and the comparators."""
+    w = synth.workload(name)
+    Xd = dev_bf16(w.X)
+    c, s, _ = kq.quantize(Xd, dev_f32(w.A), dev_f32(w.B))
+    cr, sr, _ = oracle.quantize(w.X, w.A, w.B)
+    assert_exact((host(c), host(s), None), (cr, sr, None), name)
+    c, s, _ = kq.smoothquant(Xd, dev_f32(w.mult))
+    cr, sr, _ = oracle.smoothquant(w.X, w.mult)
+    assert_exact((host(c), host(s), None), (cr, sr, None), name + " smooth")
+    c, s, _ = kq.hadamard32(Xd)
+    cr, sr, _ = oracle.hadamard32(w.X)
+    assert_exact((host(c), host(s), None), (cr, sr, None), name + " hadamard")
+
+
+@pytest.mark.parametrize("name", ["large_18432x12288", "large_18432x12288_2x16"])
+def test_large_per_block_sampled_rows(name):
+    """Large per-block-factor workload at full size; the oracle recomputes a
+    sample of rows (first, last, and random ones) one by one."""
+    w = synth.workload(name)
+    c, s, _ = kq.quantize(dev_bf16(w.X), dev_f32(w.A), dev_f32(w.B))
+    c, s = host(c), host(s)
+    M = w.X.shape[0]
+    rows = np.unique(np.concatenate([[0, 1, 63, 64, M - 1],
+                                     np.random.default_rng(0).choice(M, 120, replace=False)]))
+    cr, sr, _ = oracle.quantize(np.ascontiguousarray(w.X[rows]), w.A, w.B)
+    assert_exact((c[rows], s[rows], None), (cr, sr, None), name)

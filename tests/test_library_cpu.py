@@ -1,0 +1,156 @@
+"""Boundary tests that need no GPU: the C-ABI library loads, exports every
+symbol include/kroquant.h declares, rejects every invalid argument with its
+exact status before any HIP call, and its host helpers match the oracle."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from conftest import ROOT
+
+kq = pytest.importorskip("paper_2607_21446_amd")
+
+SUCCESS, INVALID, NULLP, MISALIGNED, UNSUPPORTED, SINGULAR, HIP = range(7)
+FAKE = 1 << 20  # 16-byte aligned fake device address: validation fails before any use
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "kroquant.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(kq_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    L = kq.lib()
+    declared = _declared()
+    assert set(declared) == set(kq.EXPORTED)
+    for name in declared:
+        assert hasattr(L, name), name
+    assert kq.version() >= 100
+
+
+def test_status_strings_are_stable():
+    names = ["KQ_SUCCESS", "KQ_ERROR_INVALID_VALUE", "KQ_ERROR_NULL_POINTER", "KQ_ERROR_MISALIGNED",
+             "KQ_ERROR_UNSUPPORTED", "KQ_ERROR_SINGULAR", "KQ_ERROR_HIP"]
+    for i, n in enumerate(names):
+        assert kq.status_string(i) == n
+    assert kq.status_string(99) == "KQ_ERROR_UNKNOWN"
+
+
+def _q(**kw):
+    args = dict(X=FAKE, M=4, d=64, A=FAKE, B=FAKE, a=4, b=8, nfac=1, codes=FAKE, scales=FAKE, y=None)
+    args.update(kw)
+    L = kq.lib()
+    return L.kq_quantize(args["X"], args["M"], args["d"], args["A"], args["B"], args["a"], args["b"],
+                         args["nfac"], args["codes"], args["scales"], args["y"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(d=48), INVALID), (dict(d=0), INVALID), (dict(d=-32), INVALID), (dict(M=-1), INVALID),
+    (dict(a=4, b=4), UNSUPPORTED), (dict(a=16, b=2), UNSUPPORTED), (dict(a=3, b=8), UNSUPPORTED),
+    (dict(nfac=3), UNSUPPORTED), (dict(nfac=0), UNSUPPORTED),
+    (dict(X=None), NULLP), (dict(A=None), NULLP), (dict(B=None), NULLP), (dict(codes=None), NULLP),
+    (dict(scales=None), NULLP), (dict(X=FAKE + 8), MISALIGNED), (dict(codes=FAKE + 4), MISALIGNED),
+    (dict(y=FAKE + 4), MISALIGNED), (dict(A=FAKE + 2), MISALIGNED),
+    (dict(M=1 << 40, d=1 << 30), INVALID),
+])
+def test_quantize_rejects(kw, status):
+    assert _q(**kw) == status
+    assert kq.lib().kq_last_error_detail() != b""
+
+
+def test_zero_rows_is_a_no_op():
+    assert _q(M=0) == SUCCESS
+    assert _q(M=0, nfac=2) == SUCCESS
+    L = kq.lib()
+    assert L.kq_mxfp4_quantize(FAKE, 0, 64, FAKE, FAKE, None) == SUCCESS
+    assert L.kq_hadamard32_quantize(FAKE, 0, 64, FAKE, FAKE, None, None) == SUCCESS
+    assert L.kq_smoothquant_quantize(FAKE, 0, 64, FAKE, FAKE, FAKE, None, None) == SUCCESS
+    assert L.kq_e2m1_encode(FAKE, 0, 127, FAKE, None) == SUCCESS
+
+
+def test_comparators_reject():
+    L = kq.lib()
+    assert L.kq_smoothquant_quantize(FAKE, 4, 64, None, FAKE, FAKE, None, None) == NULLP
+    assert L.kq_smoothquant_quantize(FAKE, 4, 64, FAKE + 4, FAKE, FAKE, None, None) == MISALIGNED
+    assert L.kq_smoothquant_quantize(FAKE, 4, 40, FAKE, FAKE, FAKE, None, None) == INVALID
+    assert L.kq_hadamard32_quantize(FAKE, 4, 64, None, FAKE, None, None) == NULLP
+    assert L.kq_mxfp4_quantize(FAKE + 2, 4, 64, FAKE, FAKE, None) == MISALIGNED
+    assert L.kq_e2m1_encode(FAKE, 3, 127, FAKE, None) == INVALID
+    assert L.kq_e2m1_encode(FAKE, 4, 255, FAKE, None) == INVALID
+    assert L.kq_e2m1_encode(FAKE, 4, -1, FAKE, None) == INVALID
+
+
+def test_weight_transform_rejects_before_any_hip_call():
+    L = kq.lib()
+    A = np.eye(4, dtype=np.float32)[None].copy()
+    B = np.zeros((1, 8, 8), np.float32)  # singular
+    pa, pb = A.ctypes.data, B.ctypes.data
+    st = L.kq_weight_transform(FAKE, 4, 64, pa, pb, 4, 8, 1, FAKE, None, None, None)
+    assert st == SINGULAR
+    Bn = np.eye(8, dtype=np.float32)[None].copy()
+    st = L.kq_weight_transform(FAKE, 4, 64, pa, Bn.ctypes.data, 4, 8, 1, None, None, None, None)
+    assert st == NULLP
+    st = L.kq_weight_transform(FAKE, 4, 64, pa, Bn.ctypes.data, 4, 8, 1, FAKE, FAKE, None, None)
+    assert st == NULLP  # codes without scales
+    st = L.kq_weight_transform(FAKE, 0, 64, pa, Bn.ctypes.data, 4, 8, 1, FAKE, None, None, None)
+    assert st == SUCCESS
+    Bill = np.diag([1.0] * 7 + [1e-7]).astype(np.float32)[None].copy()  # cond 1e7
+    st = L.kq_weight_transform(FAKE, 4, 64, pa, Bill.ctypes.data, 4, 8, 1, FAKE, None, None, None)
+    assert st == SINGULAR
+
+
+@pytest.mark.parametrize("ab", [(4, 8), (2, 16), (8, 4), (1, 32)])
+def test_inverse_transpose_matches_oracle(ab):
+    a, b = ab
+    A, B = synth.factors(a, b, 7, seed=31)
+    Ait, Bit = kq.factors_inverse_transpose(torch.from_numpy(A), torch.from_numpy(B))
+    Ro, Bo = oracle.factors_inverse_transpose(A, B)
+    # both round an fp64 inverse to fp32: at most one fp32 ulp apart
+    assert np.allclose(Ait.numpy(), Ro, rtol=2.0**-23, atol=1e-30)
+    assert np.allclose(Bit.numpy(), Bo, rtol=2.0**-23, atol=1e-30)
+
+
+@pytest.mark.parametrize("a", [1, 2, 4, 8])
+def test_lu_to_factors_matches_oracle(a):
+    rng = np.random.default_rng(5)
+    abc = rng.normal(size=(6, 5, 3)).astype(np.float32)
+    abc[..., 0] = np.where(np.abs(abc[..., 0]) < 0.3, 0.7, abc[..., 0])
+    A, B = kq.lu_to_factors(torch.from_numpy(abc), a)
+    Ao, Bo = oracle.lu_to_factors(abc.astype(np.float64), a)
+    assert A.shape == Ao.shape and B.shape == Bo.shape
+    assert np.allclose(A.numpy(), Ao, rtol=2.0**-22, atol=1e-30)
+    assert np.allclose(B.numpy(), Bo, rtol=2.0**-22, atol=1e-30)
+    # the Hadamard initialization LU(1/sqrt2, 1/sqrt2, 1) gives H32^T / sqrt(32) = H32 / sqrt(32)
+    h = 1 / np.sqrt(2.0)
+    Ah, Bh = kq.lu_to_factors(torch.tensor([[h, h, 1.0]] * 5, dtype=torch.float32)[None], a)
+    from scipy.linalg import hadamard
+    K = np.kron(Ah[0].numpy().astype(np.float64), Bh[0].numpy().astype(np.float64))
+    assert np.allclose(K, hadamard(32) / np.sqrt(32.0), atol=1e-6)
+
+
+def test_lu_rejects():
+    L = kq.lib()
+    abc = np.zeros((1, 5, 3), np.float32)
+    A = np.zeros((1, 4, 4), np.float32)
+    B = np.zeros((1, 8, 8), np.float32)
+    assert L.kq_lu_to_factors(abc.ctypes.data, 4, 1, A.ctypes.data, B.ctypes.data) == SINGULAR
+    assert L.kq_lu_to_factors(abc.ctypes.data, 3, 1, A.ctypes.data, B.ctypes.data) == UNSUPPORTED
+    assert L.kq_lu_to_factors(None, 4, 1, A.ctypes.data, B.ctypes.data) == NULLP
+
+
+def test_product_path_has_no_oracle_dependency():
+    """The binding and the HIP sources never reference the oracle."""
+    pkg = os.path.join(ROOT, "paper_2607_21446_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".h", ".cpp")):
+                with open(os.path.join(dirpath, fn)) as f:
+                    text = f.read()
+                assert "oracle" not in text.lower(), fn
+                assert "kqo_" not in text, fn
