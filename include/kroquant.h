@@ -25,9 +25,11 @@
  *    synchronize; they enqueue one kernel on `stream` (a hipStream_t; NULL =
  *    the null stream) and return.  A fault inside the kernel surfaces at the
  *    caller's next synchronization, as for any HIP launch.
- *  - Alignment: X, codes and y_out must be 16-byte aligned; scales and the
- *    factor / multiplier arrays need only their natural alignment (4 B for
- *    fp32).
+ *  - Alignment: X, codes and y_out must be 16-byte aligned; scales need no
+ *    alignment; the factors need 4 B and the SmoothQuant multipliers 16 B.
+ *  - Environment: KQ_MAX_WAVES (cap on workgroups) and KQ_UNITS_PER_WAVE
+ *    (1 or 2) set the launch shape of the matrix-core kernel; read once,
+ *    tuning knobs that never change results.
  *  - Inputs must be finite; NaN or Inf inputs give unspecified codes.
  *  - Arguments are validated before any HIP call.  On failure the call
  *    returns the status and kq_last_error_detail() describes the argument
@@ -57,9 +59,9 @@ typedef enum kq_status {
  * kq_quantize -- the KroQuant online quantizer (Sec. 3.2 transform, Sec. 3.5
  * kernels, Sec. 3.1 quantizer).  For every row r and 32-column block j of X:
  *     y = (A_f (x) B_f) x,   x = X[r, 32j : 32j+32] widened to fp32,
- * evaluated on the block reshaped row-major to a x b (Xm[p][q] = x[p*b+q]) as
- * Ym = A_f . Xm . B_f^T, which is (A (x) B) vec(Xm^T) = vec(B Xm^T A^T); then
- * MXFP4 of y into codes[r, 16j:16j+16] and scales[r, j].
+ * i.e. with the block reshaped row-major to a x b (Xm[p][q] = x[p*b+q]),
+ * Ym = A_f . Xm . B_f^T = (A (x) B) vec(Xm^T) = vec(B Xm^T A^T); then MXFP4
+ * of y into codes[r, 16j:16j+16] and scales[r, j].
  *
  *   X       device, bf16 [M, d]
  *   A       device, fp32 [nfac, a, a] row-major; B device, fp32 [nfac, b, b]
@@ -70,15 +72,60 @@ typedef enum kq_status {
  *   y_out   device, fp32 [M, d] or NULL: the transformed values that were
  *           quantized
  *
- * Arithmetic: fp32, in the order
- *     Z[p][i] = B[i][0]*Xm[p][0],  Z[p][i] = fma(B[i][q], Xm[p][q], Z[p][i]) for q = 1..b-1,
- *     Y[o][i] = A[o][0]*Z[0][i],   Y[o][i] = fma(A[o][p], Z[p][i], Y[o][i])  for p = 1..a-1.
+ * Arithmetic: the 32x32 block K = A (x) B is materialised in fp32 and applied
+ * on the matrix cores as a three-term bf16 split with fp32 accumulation
+ * (the single 32x32 GEMM per block of Sec. 3.5).  Results agree with the
+ * fixed-order evaluation of kq_quantize_exact as follows: E8M0 scales are
+ * identical (blocks whose amax lies within the rounding margin of a power of
+ * two are re-evaluated in that order); codes differ only by one magnitude
+ * step where a value sits on a rounding tie; y_out differs by at most
+ * 116 * 2^-24 * sum_k |K_nk| |x_k| per element.
  * To apply the paper's right-multiplication A -> A T with K = G1 (x) ... (x) G5
  * (eq. (1), Sec. 3.2), pass A (x) B = K^T; kq_lu_to_factors builds exactly that.
  */
 kq_status kq_quantize(const uint16_t* X, int64_t M, int64_t d, const float* A, const float* B,
                       int a, int b, int64_t nfac, uint8_t* codes, uint8_t* scales, float* y_out,
                       void* stream);
+
+/* Bytes of packed K per factor pair (see kq_pack_factors). */
+#define KQ_PACK_BYTES_PER_FACTOR 6160
+
+/*
+ * kq_pack_factors -- offline, once per layer: materialise every 32x32 block
+ * K_f = A_f (x) B_f in fp32, split it into the three bf16 terms the matrix
+ * cores multiply, and store them with ||K_f||_inf in `kpack` (device,
+ * nfac * KQ_PACK_BYTES_PER_FACTOR bytes, 16-byte aligned).  This is the
+ * "precomputed dense" kernel variant K1 of Sec. 3.5, which keeps the dense
+ * blocks in HBM; kq_quantize instead rebuilds K from the factors on the fly
+ * in every wave (variant K2).  A, B device fp32 as for kq_quantize.  Enqueued
+ * on `stream`; no allocation, no synchronization.
+ */
+kq_status kq_pack_factors(const float* A, const float* B, int a, int b, int64_t nfac, void* kpack,
+                          void* stream);
+
+/*
+ * kq_quantize_packed -- kq_quantize reading K from `kpack` (filled by
+ * kq_pack_factors from the same A, B, a, b, nfac) instead of rebuilding it.
+ * A and B are still required: blocks on a binade edge are re-evaluated in
+ * the fixed order of kq_quantize_exact.  Outputs are bit-identical to
+ * kq_quantize's.
+ */
+kq_status kq_quantize_packed(const uint16_t* X, int64_t M, int64_t d, const float* A,
+                             const float* B, int a, int b, int64_t nfac, const void* kpack,
+                             uint8_t* codes, uint8_t* scales, float* y_out, void* stream);
+
+/*
+ * kq_quantize_exact -- kq_quantize with the transform evaluated on the vector
+ * ALUs in one fixed fp32 order, so that every output is a deterministic
+ * function of that order:
+ *     Z[p][i] = B[i][0]*Xm[p][0],  Z[p][i] = fma(B[i][q], Xm[p][q], Z[p][i]) for q = 1..b-1,
+ *     Y[o][i] = A[o][0]*Z[0][i],   Y[o][i] = fma(A[o][p], Z[p][i], Y[o][i])  for p = 1..a-1.
+ * Same arguments, layout and errors as kq_quantize; slower (12 FMAs per
+ * element for (4, 8)).
+ */
+kq_status kq_quantize_exact(const uint16_t* X, int64_t M, int64_t d, const float* A,
+                            const float* B, int a, int b, int64_t nfac, uint8_t* codes,
+                            uint8_t* scales, float* y_out, void* stream);
 
 /*
  * kq_smoothquant_quantize -- SmoothQuant comparator (per-channel scaling, the
@@ -124,8 +171,8 @@ kq_status kq_e2m1_encode(const float* v, int64_t n, int s, uint8_t* codes, void*
  *   W_out    device fp32 [o, d] (required)
  *   codes, scales  device, optional (both NULL or both set): MXFP4 of W~
  * The factors are inverted on the host in fp64 (Gauss-Jordan, partial
- * pivoting), transposed and rounded to fp32; then the kq_quantize kernel
- * applies them.  Returns KQ_ERROR_SINGULAR if a pivot is below 1e-12 times
+ * pivoting), transposed and rounded to fp32; then the kq_quantize_exact
+ * kernel applies them.  Returns KQ_ERROR_SINGULAR if a pivot is below 1e-12 times
  * its row's infinity norm or a factor's infinity-norm condition number
  * exceeds 1e6.  Allocates a small device buffer for the inverted factors and
  * synchronizes `stream` before returning (offline call).

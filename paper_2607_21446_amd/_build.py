@@ -16,6 +16,8 @@ SOURCES = ["kq_kernels.hip", "kq_api.hip"]
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-ffp-contract=off",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-core results in architectural VGPRs (no accumulator-register reads)
+    "-mllvm", "-amdgpu-mfma-vgpr-form=true",
     "-Wall", "-Wno-unused-command-line-argument",
 ]
 

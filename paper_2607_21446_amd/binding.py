@@ -20,7 +20,7 @@ STATUS = {
 }
 
 EXPORTED = (
-    "kq_quantize", "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_mxfp4_quantize",
+    "kq_quantize", "kq_quantize_exact", "kq_quantize_packed", "kq_pack_factors", "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_mxfp4_quantize",
     "kq_e2m1_encode", "kq_weight_transform", "kq_factors_inverse_transpose", "kq_lu_to_factors",
     "kq_status_string", "kq_last_error_detail", "kq_version",
 )
@@ -43,6 +43,9 @@ def lib() -> ctypes.CDLL:
     L = ctypes.CDLL(_LIB_PATH)
     P, I64, I, F = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
     L.kq_quantize.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P]
+    L.kq_quantize_exact.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P]
+    L.kq_quantize_packed.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P, P]
+    L.kq_pack_factors.argtypes = [P, P, I, I, I64, P, P]
     L.kq_smoothquant_quantize.argtypes = [P, I64, I64, P, P, P, P, P]
     L.kq_hadamard32_quantize.argtypes = [P, I64, I64, P, P, P, P]
     L.kq_mxfp4_quantize.argtypes = [P, I64, I64, P, P, P]
@@ -50,7 +53,7 @@ def lib() -> ctypes.CDLL:
     L.kq_weight_transform.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P]
     L.kq_factors_inverse_transpose.argtypes = [P, P, I, I, I64, P, P]
     L.kq_lu_to_factors.argtypes = [P, I, I64, P, P]
-    for name in EXPORTED[:8]:
+    for name in EXPORTED[:11]:
         getattr(L, name).restype = ctypes.c_int
     L.kq_status_string.argtypes = [I]
     L.kq_status_string.restype = ctypes.c_char_p
@@ -107,9 +110,7 @@ def _outputs(X, codes, scales, y, want_y):
     return codes, scales, y
 
 
-def quantize(X, A, B, codes=None, scales=None, y=None, want_y=False, stream=None):
-    """KroQuant quantizer kq_quantize: X bf16 [M, d]; A [nfac, a, a] and
-    B [nfac, b, b] fp32 device tensors.  Returns (codes, scales, y or None)."""
+def _kron(fn, name, X, A, B, codes, scales, y, want_y, stream):
     _need(X, torch.bfloat16, "X")
     _need(A, torch.float32, "A")
     _need(B, torch.float32, "B")
@@ -117,8 +118,53 @@ def quantize(X, A, B, codes=None, scales=None, y=None, want_y=False, stream=None
     nfac = A.numel() // (a * a)
     codes, scales, y = _outputs(X, codes, scales, y, want_y)
     M, d = X.shape
-    _check(lib().kq_quantize(_ptr(X), M, d, _ptr(A), _ptr(B), a, b, nfac, _ptr(codes), _ptr(scales),
-                             _ptr(y), _stream(stream)), "kq_quantize")
+    _check(fn(_ptr(X), M, d, _ptr(A), _ptr(B), a, b, nfac, _ptr(codes), _ptr(scales), _ptr(y),
+              _stream(stream)), name)
+    return codes, scales, y
+
+
+def quantize(X, A, B, codes=None, scales=None, y=None, want_y=False, stream=None):
+    """KroQuant quantizer kq_quantize (matrix-core path): X bf16 [M, d];
+    A [nfac, a, a] and B [nfac, b, b] fp32 device tensors.
+    Returns (codes, scales, y or None)."""
+    return _kron(lib().kq_quantize, "kq_quantize", X, A, B, codes, scales, y, want_y, stream)
+
+
+def quantize_exact(X, A, B, codes=None, scales=None, y=None, want_y=False, stream=None):
+    """kq_quantize_exact: the same quantizer with the fixed-order fp32
+    evaluation on the vector ALUs."""
+    return _kron(lib().kq_quantize_exact, "kq_quantize_exact", X, A, B, codes, scales, y, want_y, stream)
+
+
+PACK_BYTES_PER_FACTOR = 6160
+
+
+def pack_factors(A, B, kpack=None, stream=None):
+    """kq_pack_factors: materialised K = A (x) B terms for the matrix cores
+    (offline, once per layer).  Returns a uint8 device tensor."""
+    _need(A, torch.float32, "A")
+    _need(B, torch.float32, "B")
+    a, b = A.shape[-1], B.shape[-1]
+    nfac = A.numel() // (a * a)
+    if kpack is None:
+        kpack = torch.empty(nfac * PACK_BYTES_PER_FACTOR, dtype=torch.uint8, device=A.device)
+    _need(kpack, torch.uint8, "kpack")
+    _check(lib().kq_pack_factors(_ptr(A), _ptr(B), a, b, nfac, _ptr(kpack), _stream(stream)), "kq_pack_factors")
+    return kpack
+
+
+def quantize_packed(X, A, B, kpack, codes=None, scales=None, y=None, want_y=False, stream=None):
+    """kq_quantize_packed: kq_quantize with K read from kpack."""
+    _need(X, torch.bfloat16, "X")
+    _need(A, torch.float32, "A")
+    _need(B, torch.float32, "B")
+    _need(kpack, torch.uint8, "kpack")
+    a, b = A.shape[-1], B.shape[-1]
+    nfac = A.numel() // (a * a)
+    codes, scales, y = _outputs(X, codes, scales, y, want_y)
+    M, d = X.shape
+    _check(lib().kq_quantize_packed(_ptr(X), M, d, _ptr(A), _ptr(B), a, b, nfac, _ptr(kpack), _ptr(codes),
+                                    _ptr(scales), _ptr(y), _stream(stream)), "kq_quantize_packed")
     return codes, scales, y
 
 

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdint>
+#include <cstdlib>
 #include <string>
 #include <vector>
 
@@ -76,11 +77,23 @@ kq::Params make_params(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, 
     return p;
 }
 
+// KQ_MAX_WAVES and KQ_UNITS_PER_WAVE (optional, read once): launch shape of
+// the matrix-core kernel.  Tuning knobs only; outputs do not depend on them.
 kq::LaunchConfig default_config() {
-    kq::LaunchConfig c;
-    c.blocks_per_lane = 1;
-    c.max_blocks = 1 << 20;
-    return c;
+    static const kq::LaunchConfig cfg = [] {
+        kq::LaunchConfig c;
+        if (const char* e = std::getenv("KQ_MAX_WAVES")) {
+            const long long v = std::atoll(e);
+            if (v >= 1 && v <= (1 << 30)) c.max_waves = v;
+        }
+        if (const char* e = std::getenv("KQ_PACKED_PERSISTENT")) c.packed_one_unit = std::atoi(e) == 0;
+        if (const char* e = std::getenv("KQ_UNITS_PER_WAVE")) {
+            const int v = std::atoi(e);
+            if (v == 1 || v == 2) c.units_per_wave = v;
+        }
+        return c;
+    }();
+    return cfg;
 }
 
 // fp64 Gauss-Jordan inverse with partial pivoting of an n x n fp32 matrix.
@@ -160,20 +173,54 @@ kq_status check_factors(int a, int b, int64_t nfac, int64_t d) {
 
 extern "C" {
 
-kq_status kq_quantize(const uint16_t* X, int64_t M, int64_t d, const float* A, const float* B, int a,
-                      int b, int64_t nfac, uint8_t* codes, uint8_t* scales, float* y_out, void* stream) {
+static kq_status quantize_kron(kq::Kind kind, const char* name, const uint16_t* X, int64_t M, int64_t d,
+                               const float* A, const float* B, int a, int b, int64_t nfac, const void* kpack,
+                               uint8_t* codes, uint8_t* scales, float* y_out, void* stream) {
     kq_status st = check_common(X, M, d, codes, scales, y_out, true);
     if (st != KQ_SUCCESS) return st;
     if ((st = check_factors(a, b, nfac, d)) != KQ_SUCCESS) return st;
     if (!A || !B) return fail(KQ_ERROR_NULL_POINTER, "A and B must not be NULL");
     if (!aligned(A, 4) || !aligned(B, 4)) return fail(KQ_ERROR_MISALIGNED, "A and B must be 4-byte aligned");
+    if (kpack && !aligned(kpack, 16)) return fail(KQ_ERROR_MISALIGNED, "kpack must be 16-byte aligned");
     if (M == 0) return ok();
     kq::Params p = make_params(X, M, d, codes, scales, y_out);
     p.A = A;
     p.B = B;
     p.nfac = nfac;
+    p.kpack = static_cast<const uint8_t*>(kpack);
     const kq::Mapping map = (nfac == 1) ? kq::Mapping::Flat : kq::Mapping::Column;
-    return from_hip(kq::launch(kq::Kind::Kron, a, p, map, (hipStream_t)stream, default_config()), "kq_quantize");
+    return from_hip(kq::launch(kind, a, p, map, (hipStream_t)stream, default_config()), name);
+}
+
+kq_status kq_quantize(const uint16_t* X, int64_t M, int64_t d, const float* A, const float* B, int a,
+                      int b, int64_t nfac, uint8_t* codes, uint8_t* scales, float* y_out, void* stream) {
+    return quantize_kron(kq::Kind::KronMfma, "kq_quantize", X, M, d, A, B, a, b, nfac, nullptr, codes, scales,
+                         y_out, stream);
+}
+
+kq_status kq_quantize_packed(const uint16_t* X, int64_t M, int64_t d, const float* A, const float* B, int a,
+                             int b, int64_t nfac, const void* kpack, uint8_t* codes, uint8_t* scales, float* y_out,
+                             void* stream) {
+    if (!kpack) return fail(KQ_ERROR_NULL_POINTER, "kpack must not be NULL");
+    return quantize_kron(kq::Kind::KronMfma, "kq_quantize_packed", X, M, d, A, B, a, b, nfac, kpack, codes,
+                         scales, y_out, stream);
+}
+
+kq_status kq_pack_factors(const float* A, const float* B, int a, int b, int64_t nfac, void* kpack, void* stream) {
+    if (!supported_split(a, b))
+        return fail(KQ_ERROR_UNSUPPORTED, "(a, b) = (%d, %d) is not one of (4,8), (2,16), (8,4), (1,32)", a, b);
+    if (nfac < 1) return fail(KQ_ERROR_INVALID_VALUE, "nfac = %lld must be >= 1", (long long)nfac);
+    if (!A || !B || !kpack) return fail(KQ_ERROR_NULL_POINTER, "A, B and kpack must not be NULL");
+    if (!aligned(A, 4) || !aligned(B, 4)) return fail(KQ_ERROR_MISALIGNED, "A and B must be 4-byte aligned");
+    if (!aligned(kpack, 16)) return fail(KQ_ERROR_MISALIGNED, "kpack must be 16-byte aligned");
+    return from_hip(kq::launch_pack(a, A, B, nfac, static_cast<uint8_t*>(kpack), (hipStream_t)stream),
+                    "kq_pack_factors");
+}
+
+kq_status kq_quantize_exact(const uint16_t* X, int64_t M, int64_t d, const float* A, const float* B, int a,
+                            int b, int64_t nfac, uint8_t* codes, uint8_t* scales, float* y_out, void* stream) {
+    return quantize_kron(kq::Kind::Kron, "kq_quantize_exact", X, M, d, A, B, a, b, nfac, nullptr, codes, scales,
+                         y_out, stream);
 }
 
 kq_status kq_smoothquant_quantize(const uint16_t* X, int64_t M, int64_t d, const float* mult, uint8_t* codes,

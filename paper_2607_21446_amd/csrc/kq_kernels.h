@@ -5,9 +5,10 @@
 
 namespace kq {
 
-constexpr int kThreads = 256;  // 4 wave64 per workgroup
+constexpr int kThreads = 256;  // workgroup size of the element-encode kernel
+constexpr int64_t kPackBytes = 6 * 64 * 16 + 16;  // packed K per factor pair
 
-enum class Kind { Plain, Smooth, Hadamard, Kron };
+enum class Kind { Plain, Smooth, Hadamard, Kron, KronMfma };
 enum class Mapping { Flat, Column };
 
 // Everything a launch needs; sizes already validated by the caller.
@@ -24,15 +25,19 @@ struct Params {
     uint8_t* codes;      // [M, d/2] or null (then scales is null too)
     uint8_t* scales;     // [M, nb]
     float* y;            // [M, d] or null
+    const uint8_t* kpack;  // [nfac, kPackBytes] materialised K terms, or null
     int64_t units;       // wave units, filled in by the launcher
 };
 
 struct LaunchConfig {
-    int blocks_per_lane = 1;   // U: 32-element blocks a lane holds per wave unit
-    int max_blocks = 1 << 20;  // cap on the workgroup count (grid-stride beyond it)
+    int64_t max_blocks = int64_t(1) << 30;  // cap on the workgroup count (grid-stride beyond it)
+    int64_t max_waves = int64_t(1) << 30;   // cap on the matrix-core kernel's workgroups (one wave each)
+    int units_per_wave = 2;                 // 64-block units a matrix-core wave loads per step (1 or 2)
+    bool packed_one_unit = true;            // packed K: one unit per wave, no loop
 };
 
 hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg);
+hipError_t launch_pack(int a, const float* A, const float* B, int64_t nfac, uint8_t* kpack, hipStream_t st);
 hipError_t launch_e2m1(const float* v, int64_t npairs, uint32_t s, uint8_t* codes, hipStream_t st);
 
 }  // namespace kq

@@ -1,18 +1,36 @@
 // KroQuant online activation quantizer: HIP kernels for gfx950 (MI355X).
 //
-// One lane owns one whole 32-element block (Sec. 3.1: row-wise blocks of 32
-// sharing one E8M0 scale).  The block's 64 input bytes, its 32 transformed
-// fp32 values, its amax, scale and 16 code bytes all stay in that lane's
-// registers, so the transform, the amax and the encode need no cross-lane
-// traffic.  Factors are wave-uniform and are read with scalar loads.
+// Two implementations of the Kronecker block transform y = (A (x) B) x
+// (Sec. 3.2) feed the same MXFP4 encoder (Sec. 3.1: row-wise blocks of 32
+// sharing one E8M0 scale):
 //
-// Two lane -> block mappings:
+//  * exact (VALU, quant_kernel): one lane owns one whole 32-element block.
+//    The block's input, its 32 transformed fp32 values, its amax, scale and
+//    16 code bytes stay in that lane's registers, and the separable product
+//    is evaluated with fp32 FMAs in the fixed order below, so every output
+//    is bit-identical to that order.  Factors are wave-uniform scalar loads.
+//    12 FMAs per element make it bound by VALU issue, not by HBM.
+//  * matrix-core (MFMA, kron_mfma_kernel): the materialised 32x32 block
+//    K = A (x) B, rounded to fp32 and split into three bf16 terms
+//    (hi + mid + lo), multiplies 32 blocks at a time with
+//    v_mfma_f32_32x32x16_bf16 (the bf16 input is the B operand as loaded),
+//    accumulating in fp32 -- the "single 32x32 tensor-core GEMM per block"
+//    of Sec. 3.5 done in enough precision for fp32 parity.  Its rounding
+//    differs from the exact order by at most 116 u sum_k |K_nk||x_k|
+//    (u = 2^-24), which can move a code only next to a rounding tie.  The
+//    E8M0 scale depends on amax only through its binade; whenever a block's
+//    amax lies within 2^-16 ||K||_inf max|x| of a power of two (256 u, over
+//    twice that bound) that block is recomputed on the exact path, so scales
+//    are always those of the exact order and each block's outputs depend on
+//    that block alone.
+//
+// Two unit -> block mappings (a unit is the 64 blocks of one wave):
 //   FLAT    the blocks of the matrix are one flat array (rows are contiguous);
-//           lane l of sub-tile k of wave unit u owns block (u*U + k)*64 + l.
-//           Stores of one sub-tile are 1 KiB of codes and 64 B of scales,
-//           both contiguous.  Used when every block has the same factors.
-//   COLUMN  wave unit u owns column block j = u % nb over 64*U consecutive
-//           rows (lane = row), so per-block factors K^(j) (T = diag(K^(1..d/32)),
+//           unit u owns blocks 64u .. 64u+63.  Its stores are 1 KiB of codes
+//           and 64 B of scales, both contiguous.  Used when every block has
+//           the same factors.
+//   COLUMN  unit u owns column block j = u % nb over 64 consecutive rows
+//           (lane = row), so per-block factors K^(j) (T = diag(K^(1..d/32)),
 //           Sec. 3.1) are uniform across the wave.
 //
 // Arithmetic contract (kept bit-identical to the reference evaluation order):
@@ -181,16 +199,34 @@ struct KronOp {
 };
 
 // ------------------------------------------------------------------ kernels
-template <int U>
-struct Tile {
-    uint4 raw[U][4];
-};
+// One wave per workgroup; a wave unit is 64 blocks (4 KiB of bf16 input).
+// The unit's 256 16-byte chunks are read with four fully coalesced,
+// nontemporal 1 KiB loads (instruction k, lane l -> chunk 64k + l), parked in
+// LDS and read back so that lane l holds the 4 chunks of block l.  LDS slot of
+// chunk m of block b: 4b + (m ^ ((b >> 2) & 3)); the XOR keeps both the
+// chunk-order writes and the block-order reads free of bank conflicts.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// per-block body shared by both mappings
+__device__ __forceinline__ uint4 load_nt(const uint4* p) {
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ int lds_slot(int b, int m) { return 4 * b + (m ^ ((b >> 2) & 3)); }
+
+// make this wave's LDS writes visible to its own later reads (same wave,
+// different lanes)
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// per-block body: transform, encode, store.  codes16 / scale / y32 point at
+// this lane's block in the outputs.
 template <class Op>
 __device__ __forceinline__ void process_block(const Op& op, const uint4 (&raw)[4], const Params& p,
-                                              int64_t blk, int64_t col) {
-    const int64_t codes_off = blk * 16, scale_off = blk, y_off = blk * 32;
+                                              uint8_t* codes16, uint8_t* scale, float* y32, int64_t col) {
     float x[32], y[32];
 #pragma unroll
     for (int m = 0; m < 4; ++m) unpack8(raw[m], x + 8 * m);
@@ -198,63 +234,533 @@ __device__ __forceinline__ void process_block(const Op& op, const uint4 (&raw)[4
     uint32_t w[4];
     const uint32_t s = encode32(y, w);
     if (p.codes) {
-        *reinterpret_cast<uint4*>(p.codes + codes_off) = make_uint4(w[0], w[1], w[2], w[3]);
-        p.scales[scale_off] = (uint8_t)s;
+        *reinterpret_cast<uint4*>(codes16) = make_uint4(w[0], w[1], w[2], w[3]);
+        *scale = (uint8_t)s;
     }
     if (p.y) {
-        float4* dst = reinterpret_cast<float4*>(p.y + y_off);
+        float4* dst = reinterpret_cast<float4*>(y32);
 #pragma unroll
         for (int m = 0; m < 8; ++m)
             dst[m] = make_float4(y[4 * m], y[4 * m + 1], y[4 * m + 2], y[4 * m + 3]);
     }
 }
 
-template <int U, class Op>
-__global__ __launch_bounds__(kThreads) void flat_kernel(const Params p) {
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t stride = (int64_t)gridDim.x * (kThreads / 64);
-    Op op;
-    op.setup(p, 0);
-    for (int64_t u = (int64_t)blockIdx.x * (kThreads / 64) + wave; u < p.units; u += stride) {
-        Tile<U> t;
+// FLAT: unit u = blocks 64u .. 64u+63 of the flat block array.
+// COLUMN: unit u = column block j = u % nb of rows 64*(u / nb) .. +63.
+// Addresses: a wave-uniform unit base plus a 32-bit lane offset (a unit spans
+// 64 rows at most, so lane offsets stay below 2^31 for any d < 2^24).
+template <Mapping MAP, class Op>
+__global__ __launch_bounds__(64) void quant_kernel(const Params p) {
+    __shared__ uint4 lds[256];
+    const int lane = threadIdx.x;
+    for (int64_t u = blockIdx.x; u < p.units; u += gridDim.x) {
+        int64_t j = 0, row0 = 0, first;  // first: flat index of the unit's block 0
+        int nvalid;                       // blocks of the unit inside the matrix
+        uint32_t bstride;                 // flat-block distance between the unit's blocks
+        if (MAP == Mapping::Flat) {
+            first = u * 64;
+            nvalid = (int)min<int64_t>(64, p.nblocks - first);
+            bstride = 1;
+        } else {
+            j = u % p.nb;
+            row0 = (u / p.nb) * 64;
+            first = row0 * p.nb + j;
+            nvalid = (int)min<int64_t>(64, p.M - row0);
+            bstride = (uint32_t)p.nb;
+        }
+        const uint4* src = reinterpret_cast<const uint4*>(p.X) + first * 4;
+        uint4 v[4];
+        if (nvalid == 64) {
 #pragma unroll
-        for (int k = 0; k < U; ++k) {
-            const int64_t blk = (u * U + k) * 64 + lane;
-            if (blk < p.nblocks) load_block(p.X, blk, t.raw[k]);
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t ci = 64 * k + lane;
+                v[k] = load_nt(src + ((ci >> 2) * bstride * 4 + (ci & 3)));
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t ci = 64 * k + lane;
+                v[k] = make_uint4(0u, 0u, 0u, 0u);
+                if ((int)(ci >> 2) < nvalid) v[k] = load_nt(src + ((ci >> 2) * bstride * 4 + (ci & 3)));
+            }
         }
 #pragma unroll
-        for (int k = 0; k < U; ++k) {
-            const int64_t blk = (u * U + k) * 64 + lane;
-            if (blk < p.nblocks) process_block(op, t.raw[k], p, blk, blk % p.nb);
+        for (int k = 0; k < 4; ++k) {
+            const int ci = 64 * k + lane;
+            lds[lds_slot(ci >> 2, ci & 3)] = v[k];
+        }
+        wave_lds_sync();
+        uint4 raw[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) raw[m] = lds[lds_slot(lane, m)];
+        wave_lds_sync();  // the next unit's writes come after these reads
+        if (lane < nvalid) {
+            Op op;
+            op.setup(p, j);
+            const uint32_t lo = (uint32_t)lane * bstride;  // this lane's block, relative to `first`
+            const int64_t col = (MAP == Mapping::Flat) ? (first + lane) % p.nb : j;
+            process_block(op, raw, p, p.codes + first * 16 + (uint64_t)lo * 16, p.scales + first + lo,
+                          p.y + first * 32 + (uint64_t)lo * 32, col);
         }
     }
 }
 
-template <int U, class Op>
-__global__ __launch_bounds__(kThreads) void column_kernel(const Params p) {
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t stride = (int64_t)gridDim.x * (kThreads / 64);
-    for (int64_t u = (int64_t)blockIdx.x * (kThreads / 64) + wave; u < p.units; u += stride) {
-        const int64_t j = u % p.nb;
-        const int64_t row0 = (u / p.nb) * (64 * U);
-        Op op;
-        op.setup(p, j);
-        Tile<U> t;
+// ------------------------------------------------------------------ matrix-core path
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// The value `v` of lane l ^ 32 (the other half of the wave).
+__device__ __forceinline__ uint32_t other_half(uint32_t v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return (threadIdx.x & 32) ? r[0] : r[1];
+}
+__device__ __forceinline__ float other_half(float v) { return __uint_as_float(other_half(__float_as_uint(v))); }
+
+// This lane's slice of K = A (x) B as the A operand of v_mfma_f32_32x32x16_bf16:
+// lane l holds K[n][k] for n = l % 32 and k = 16 s + 8 (l / 32) + c (c = 0..7)
+// in k-step s = 0, 1; K[n][k] = fp32(A[n / b][k / b] * B[n % b][k % b])
+// (numpy.kron index order), split as hi + mid + lo with each term the bf16
+// nearest to what the previous terms leave.
+struct KSlices {
+    bf16x8 hi[2], mid[2], lo[2];
+};
+
+// The factor entries behind this lane's slice: kv(s, c) = fa[s][c] * fb[s][c].
+template <int NA, int NB>
+struct KFactors {
+    float fa[2][8], fb[2][8];
+};
+
+template <int NA, int NB>
+__device__ __forceinline__ void load_k_factors(const float* A, const float* B, int lane, KFactors<NA, NB>& kf) {
+    const int n = lane & 31, h = lane >> 5;
+    const int ia = n / NB, ib = n % NB;
 #pragma unroll
-        for (int k = 0; k < U; ++k) {
-            const int64_t r = row0 + k * 64 + lane;
-            if (r < p.M) load_block(p.X, r * p.nb + j, t.raw[k]);
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            const int k = 16 * s + 8 * h + c;
+            kf.fa[s][c] = A[ia * NA + k / NB];
+            kf.fb[s][c] = B[ib * NB + k % NB];
         }
+}
+
+// Split the slice into bf16 terms; returns ||K||_inf.
+template <int NA, int NB>
+__device__ __forceinline__ float build_k(const KFactors<NA, NB>& kf, KSlices& ks) {
+    float rowsum = 0.0f;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            const float kv = kf.fa[s][c] * kf.fb[s][c];
+            rowsum += fabsf(kv);
+            const __bf16 t1 = (__bf16)kv;
+            const float r1 = kv - (float)t1;  // exact
+            const __bf16 t2 = (__bf16)r1;
+            const float r2 = r1 - (float)t2;  // exact
+            ks.hi[s][c] = t1;
+            ks.mid[s][c] = t2;
+            ks.lo[s][c] = (__bf16)r2;
+        }
+    }
+    // row n is split over lanes n and n + 32; then the max over the 32 rows
+    // (sums are >= 0, so their fp32 bit patterns order like the values)
+    uint32_t r = __float_as_uint(rowsum + other_half(rowsum));
+#pragma unroll
+    for (int off = 16; off >= 1; off >>= 1) r = max(r, (uint32_t)__shfl_xor((int)r, off));
+    return __uint_as_float(r);
+}
+
+// max |x| of the 16 bf16 values in two chunks, as fp32
+__device__ __forceinline__ float max_abs_bf16(const uint4 (&r)[2]) {
+    u16x2 m = {0, 0};
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        const uint32_t w[4] = {r[s].x, r[s].y, r[s].z, r[s].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            m = __builtin_elementwise_max(m, __builtin_bit_cast(u16x2, w[i] & 0x7FFF7FFFu));
+    }
+    const uint32_t top = m[0] > m[1] ? m[0] : m[1];
+    return __uint_as_float(top << 16);
+}
+
+// Exact fixed-order evaluation of one block by 32 cooperating lanes: lane n
+// (n = lane % 32; both half-waves compute the same) evaluates output
+// y[n] = Y[o][i], n = o*b + i, with the FMA chains of KronOp:
+//   Z[p][i] = B[i][0]*x[p*b] then fma(B[i][q], x[p*b+q], .), q = 1..b-1,
+//   Y[o][i] = A[o][0]*Z[0][i] then fma(A[o][p], Z[p][i], .), p = 1..a-1.
+// Called with all 64 lanes active; `blk` lies in this wave's LDS unit.
+template <int NA, int NB>
+__device__ __forceinline__ void exact_block_coop(const uint4* unit_lds, int blk, const float* Af, const float* Bf,
+                                              const Params& p, int64_t out_blk) {
+    const int n = threadIdx.x & 31;
+    const int o = n / NB, i = n % NB;
+    float x[32];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) unpack8(unit_lds[lds_slot(blk, m)], x + 8 * m);
+    float acc = 0.0f;
+#pragma unroll
+    for (int pr = 0; pr < NA; ++pr) {
+        float z = Bf[i * NB] * x[pr * NB];
+#pragma unroll
+        for (int q = 1; q < NB; ++q) z = __builtin_fmaf(Bf[i * NB + q], x[pr * NB + q], z);
+        acc = (pr == 0) ? Af[o * NA] * z : __builtin_fmaf(Af[o * NA + pr], z, acc);
+    }
+    float am = fabsf(acc);
+#pragma unroll
+    for (int off = 16; off >= 1; off >>= 1) am = fmaxf(am, __shfl_xor(am, off));
+    const uint32_t sb = e8m0_byte(am);
+    const float next = __shfl_down(acc, 1);  // y[n + 1]
+    const uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, acc, next, __uint_as_float(sb << 23), 0);
+    if (threadIdx.x < 32) {
+        if (p.codes) {
+            if ((n & 1) == 0) p.codes[out_blk * 16 + (n >> 1)] = (uint8_t)(c & 0xFFu);
+            if (n == 0) p.scales[out_blk] = (uint8_t)sb;
+        }
+        if (p.y) p.y[out_blk * 32 + n] = acc;
+    }
+}
+
+// Matrix-core KroQuant.  A wave handles U consecutive units per step (all
+// their loads issued before any compute).  FLAT: workgroup g handles steps
+// g, g + G, ...;  COLUMN: workgroup g handles column block j = g % nb for
+// steps g / nb, g / nb + G / nb, ... (G a multiple of nb), so one K per wave.
+template <Mapping MAP, int NA, int NB, int U, bool PACKED>
+__global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
+    __shared__ uint4 lds[U][256];
+    const int lane = threadIdx.x;
+    const int h = lane >> 5, jl = lane & 31;
+    int64_t jcol = 0, s0 = blockIdx.x, sstep = gridDim.x;
+    if (MAP == Mapping::Column) {
+        jcol = blockIdx.x % p.nb;
+        s0 = blockIdx.x / p.nb;
+        sstep = gridDim.x / p.nb;
+    }
+    const int64_t f = (p.nfac == 1) ? 0 : jcol;
+    const float* Af = p.A + f * (NA * NA);
+    const float* Bf = p.B + f * (NB * NB);
+    // K operand: from the pack (materialised offline) or built here from the factors
+    KFactors<NA, NB> kf;
+    KSlices ks;
+    float kbound = 0.0f;
+    if (PACKED) {
+        const uint4* pk = reinterpret_cast<const uint4*>(p.kpack + f * kPackBytes);
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+            ks.hi[s] = __builtin_bit_cast(bf16x8, pk[(0 * 2 + s) * 64 + lane]);
+            ks.mid[s] = __builtin_bit_cast(bf16x8, pk[(1 * 2 + s) * 64 + lane]);
+            ks.lo[s] = __builtin_bit_cast(bf16x8, pk[(2 * 2 + s) * 64 + lane]);
+        }
+        kbound = ld_uniform(reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16), 0) * 0x1p-16f;
+    } else {
+        load_k_factors<NA, NB>(Af, Bf, lane, kf);  // first, so their latency overlaps the input loads
+    }
+    const int64_t nunits = (MAP == Mapping::Flat) ? (p.nblocks + 63) / 64 : (p.M + 63) / 64;
+    const int64_t nsteps = (nunits + U - 1) / U;
+    const uint32_t bstride = (MAP == Mapping::Flat) ? 1u : (uint32_t)p.nb;
+    // geometry of unit u: flat index of its block 0 and its number of blocks
+    auto unit_first = [&](int64_t u) -> int64_t {
+        return (MAP == Mapping::Flat) ? u * 64 : u * 64 * p.nb + jcol;
+    };
+    auto unit_valid = [&](int64_t u) -> int {
+        const int64_t left = (MAP == Mapping::Flat) ? p.nblocks - u * 64 : p.M - u * 64;
+        return (int)max<int64_t>(0, min<int64_t>(64, left));
+    };
+    // issue the (nontemporal, coalesced) loads of step st into v
+    uint4 v[U][4];
+    auto issue = [&](int64_t st) {
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-            const int64_t r = row0 + k * 64 + lane;
-            if (r < p.M) {
-                const int64_t blk = r * p.nb + j;
-                process_block(op, t.raw[k], p, blk, j);
+            const int64_t u = st * U + k;
+            const int nv = unit_valid(u);
+            const uint4* src = reinterpret_cast<const uint4*>(p.X) + unit_first(u) * 4;
+            if (nv == 64) {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const uint32_t ci = 64 * c + lane;
+                    v[k][c] = load_nt(src + ((ci >> 2) * bstride * 4 + (ci & 3)));
+                }
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const uint32_t ci = 64 * c + lane;
+                    v[k][c] = make_uint4(0u, 0u, 0u, 0u);
+                    if ((int)(ci >> 2) < nv) v[k][c] = load_nt(src + ((ci >> 2) * bstride * 4 + (ci & 3)));
+                }
             }
         }
+    };
+    if (s0 < nsteps) issue(s0);
+    if (!PACKED) kbound = build_k<NA, NB>(kf, ks) * 0x1p-16f;
+    for (int64_t st = s0; st < nsteps; st += sstep) {
+        int64_t first[U];
+        int nvalid[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            first[k] = unit_first(st * U + k);
+            nvalid[k] = unit_valid(st * U + k);
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int ci = 64 * c + lane;
+                lds[k][lds_slot(ci >> 2, ci & 3)] = v[k][c];
+            }
+        // the next step's loads are in flight while this step computes
+        if (st + sstep < nsteps) issue(st + sstep);
+        wave_lds_sync();
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            if (nvalid[k] == 0) continue;
+            // both 32-block tiles of the unit: their MFMA chains interleave
+            uint4 raw[2][2];
+            f32x16 acc[2];
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                raw[t][0] = lds[k][lds_slot(32 * t + jl, h)];
+                raw[t][1] = lds[k][lds_slot(32 * t + jl, 2 + h)];
+                acc[t] = f32x16{};
+            }
+            // smallest terms first; acc[n][block] += K[n][k-step] . x[block][k-step]
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.lo[s], __builtin_bit_cast(bf16x8, raw[t][s]), acc[t], 0, 0, 0);
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.mid[s], __builtin_bit_cast(bf16x8, raw[t][s]), acc[t], 0, 0, 0);
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.hi[s], __builtin_bit_cast(bf16x8, raw[t][s]), acc[t], 0, 0, 0);
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                if (32 * t >= nvalid[k]) break;
+                const int bt = 32 * t + jl;  // this lane's block within the unit
+                const bool valid = bt < nvalid[k];
+                // lane holds y[8q + 4h + r] of block bt in acc[t][4q + r]; all values >= 0 below
+                // compare as their fp32 bit patterns
+                float am = 0.0f;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) am = fmaxf(am, fabsf(acc[t][i]));
+                uint32_t amb = __float_as_uint(am);
+                amb = max(amb, other_half(amb));
+                am = __uint_as_float(amb);
+                uint32_t mxb = __float_as_uint(max_abs_bf16(raw[t]));
+                mxb = max(mxb, other_half(mxb));
+                const float bnd = kbound * __uint_as_float(mxb);
+                const uint32_t e = amb >> 23;
+                const float lo_p2 = __uint_as_float(e << 23), hi_p2 = __uint_as_float((e + 1u) << 23);
+                const bool near = valid && (e <= 3u || am - lo_p2 <= bnd || hi_p2 - am <= bnd);
+                const uint64_t ob = (uint64_t)first[k] + (uint64_t)((uint32_t)bt * bstride);  // output block
+                const uint32_t sb = e > 2u ? e - 2u : 0u;
+                const float sc = __uint_as_float(sb << 23);
+                uint32_t w[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, acc[t][4 * q], acc[t][4 * q + 1], sc, 0);
+                    w[q] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, acc[t][4 * q + 2], acc[t][4 * q + 3], sc, 1);
+                }
+                // code dword q of the block = [lower half: lane h=0's w[q]] [upper half: lane h=1's w[q]];
+                // lane h=0 stores dwords 0-1, lane h=1 dwords 2-3
+                const uint32_t send = h ? (w[0] | (w[1] << 16)) : (w[2] | (w[3] << 16));
+                const uint32_t recv = other_half(send);
+                uint2 out;
+                if (h == 0) {
+                    out.x = w[0] | (recv << 16);
+                    out.y = w[1] | (recv & 0xFFFF0000u);
+                } else {
+                    out.x = (recv & 0xFFFFu) | (w[2] << 16);
+                    out.y = (recv >> 16) | (w[3] << 16);
+                }
+                if (valid && !near) {
+                    if (p.codes) {
+                        *reinterpret_cast<uint2*>(p.codes + ob * 16 + 8 * h) = out;
+                        if (h == 0) p.scales[ob] = (uint8_t)sb;
+                    }
+                    if (p.y) {
+                        float* yb = p.y + ob * 32 + 4 * h;
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            *reinterpret_cast<float4*>(yb + 8 * q) =
+                                make_float4(acc[t][4 * q], acc[t][4 * q + 1], acc[t][4 * q + 2], acc[t][4 * q + 3]);
+                    }
+                }
+                // blocks whose amax is on a binade edge: the fixed evaluation order decides
+                uint64_t edge = __builtin_amdgcn_ballot_w64(near) & 0xFFFFFFFFull;
+                while (edge) {
+                    const int b = __builtin_ctzll(edge);
+                    edge &= edge - 1;
+                    const int64_t blk_out = first[k] + (int64_t)(32 * t + b) * bstride;
+                    exact_block_coop<NA, NB>(lds[k], 32 * t + b, Af, Bf, p, blk_out);
+                }
+            }
+        }
+        wave_lds_sync();  // the next step's writes come after this step's reads
+    }
+}
+
+// Matrix-core KroQuant with K read from the pack, one 64-block unit per wave
+// (no loop): few live registers, so every wave of a large grid is resident
+// at once and all input loads are in flight from the start.  FLAT: unit =
+// blockIdx.x;  COLUMN: column block j = blockIdx.x % nb, rows 64 * (blockIdx.x / nb).
+template <Mapping MAP, int NA, int NB>
+__global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
+    __shared__ uint4 lds[256];
+    const int lane = threadIdx.x;
+    const int h = lane >> 5, jl = lane & 31;
+    int64_t jcol = 0, u = blockIdx.x, first;
+    int nvalid;
+    uint32_t bstride;
+    if (MAP == Mapping::Flat) {
+        first = u * 64;
+        nvalid = (int)min<int64_t>(64, p.nblocks - first);
+        bstride = 1;
+    } else {
+        jcol = u % p.nb;
+        const int64_t row0 = (u / p.nb) * 64;
+        first = row0 * p.nb + jcol;
+        nvalid = (int)min<int64_t>(64, p.M - row0);
+        bstride = (uint32_t)p.nb;
+    }
+    const uint4* src = reinterpret_cast<const uint4*>(p.X) + first * 4;
+    {
+        uint4 v[4];
+        if (nvalid == 64) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t ci = 64 * c + lane;
+                v[c] = load_nt(src + ((ci >> 2) * bstride * 4 + (ci & 3)));
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t ci = 64 * c + lane;
+                v[c] = make_uint4(0u, 0u, 0u, 0u);
+                if ((int)(ci >> 2) < nvalid) v[c] = load_nt(src + ((ci >> 2) * bstride * 4 + (ci & 3)));
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int ci = 64 * c + lane;
+            lds[lds_slot(ci >> 2, ci & 3)] = v[c];
+        }
+    }
+    const int64_t f = (p.nfac == 1) ? 0 : jcol;
+    const uint4* pk = reinterpret_cast<const uint4*>(p.kpack + f * kPackBytes);
+    KSlices ks;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        ks.hi[s] = __builtin_bit_cast(bf16x8, pk[(0 * 2 + s) * 64 + lane]);
+        ks.mid[s] = __builtin_bit_cast(bf16x8, pk[(1 * 2 + s) * 64 + lane]);
+        ks.lo[s] = __builtin_bit_cast(bf16x8, pk[(2 * 2 + s) * 64 + lane]);
+    }
+    const float kbound = ld_uniform(reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16), 0) * 0x1p-16f;
+    wave_lds_sync();
+    uint64_t edges = 0;  // blocks of the unit on a binade edge (bit = block index)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        if (32 * t >= nvalid) break;
+        const int bt = 32 * t + jl;
+        const bool valid = bt < nvalid;
+        uint4 raw[2];
+        raw[0] = lds[lds_slot(bt, h)];
+        raw[1] = lds[lds_slot(bt, 2 + h)];
+        f32x16 acc = {};
+#pragma unroll
+        for (int s = 0; s < 2; ++s)
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.lo[s], __builtin_bit_cast(bf16x8, raw[s]), acc, 0, 0, 0);
+#pragma unroll
+        for (int s = 0; s < 2; ++s)
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.mid[s], __builtin_bit_cast(bf16x8, raw[s]), acc, 0, 0, 0);
+#pragma unroll
+        for (int s = 0; s < 2; ++s)
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.hi[s], __builtin_bit_cast(bf16x8, raw[s]), acc, 0, 0, 0);
+        float am = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) am = fmaxf(am, fabsf(acc[i]));
+        uint32_t amb = __float_as_uint(am);
+        amb = max(amb, other_half(amb));
+        am = __uint_as_float(amb);
+        uint32_t mxb = __float_as_uint(max_abs_bf16(raw));
+        mxb = max(mxb, other_half(mxb));
+        const float bnd = kbound * __uint_as_float(mxb);
+        const uint32_t e = amb >> 23;
+        const float lo_p2 = __uint_as_float(e << 23), hi_p2 = __uint_as_float((e + 1u) << 23);
+        const bool near = valid && (e <= 3u || am - lo_p2 <= bnd || hi_p2 - am <= bnd);
+        const uint64_t ob = (uint64_t)first + (uint64_t)((uint32_t)bt * bstride);
+        const uint32_t sb = e > 2u ? e - 2u : 0u;
+        const float sc = __uint_as_float(sb << 23);
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, acc[4 * q], acc[4 * q + 1], sc, 0);
+            w[q] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, acc[4 * q + 2], acc[4 * q + 3], sc, 1);
+        }
+        const uint32_t send = h ? (w[0] | (w[1] << 16)) : (w[2] | (w[3] << 16));
+        const uint32_t recv = other_half(send);
+        uint2 out;
+        if (h == 0) {
+            out.x = w[0] | (recv << 16);
+            out.y = w[1] | (recv & 0xFFFF0000u);
+        } else {
+            out.x = (recv & 0xFFFFu) | (w[2] << 16);
+            out.y = (recv >> 16) | (w[3] << 16);
+        }
+        if (valid && !near) {
+            if (p.codes) {
+                *reinterpret_cast<uint2*>(p.codes + ob * 16 + 8 * h) = out;
+                if (h == 0) p.scales[ob] = (uint8_t)sb;
+            }
+            if (p.y) {
+                float* yb = p.y + ob * 32 + 4 * h;
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    *reinterpret_cast<float4*>(yb + 8 * q) =
+                        make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
+            }
+        }
+        edges |= (__builtin_amdgcn_ballot_w64(near) & 0xFFFFFFFFull) << (32 * t);
+    }
+    // blocks whose amax is on a binade edge: the fixed evaluation order decides
+    const float* Af = p.A + f * (NA * NA);
+    const float* Bf = p.B + f * (NB * NB);
+    while (edges) {
+        const int b = __builtin_ctzll(edges);
+        edges &= edges - 1;
+        exact_block_coop<NA, NB>(lds, b, Af, Bf, p, first + (int64_t)b * bstride);
+    }
+}
+
+// Materialise and split K = A (x) B for every factor pair, in the lane layout
+// of the matrix-core A operand (offline step; the K1 variant of Sec. 3.5
+// keeps the dense 32x32 blocks in HBM).  Layout per pair (kPackBytes):
+// uint4 [3 terms: hi, mid, lo][2 k-steps][64 lanes], then fp32 ||K||_inf.
+template <int NA, int NB>
+__global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ A, const float* __restrict__ B,
+                                                  int64_t nfac, uint8_t* __restrict__ kpack) {
+    const int lane = threadIdx.x;
+    for (int64_t f = blockIdx.x; f < nfac; f += gridDim.x) {
+        KFactors<NA, NB> kf;
+        load_k_factors<NA, NB>(A + f * (NA * NA), B + f * (NB * NB), lane, kf);
+        KSlices ks;
+        const float kinf = build_k<NA, NB>(kf, ks);
+        uint4* pk = reinterpret_cast<uint4*>(kpack + f * kPackBytes);
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+            pk[(0 * 2 + s) * 64 + lane] = __builtin_bit_cast(uint4, ks.hi[s]);
+            pk[(1 * 2 + s) * 64 + lane] = __builtin_bit_cast(uint4, ks.mid[s]);
+            pk[(2 * 2 + s) * 64 + lane] = __builtin_bit_cast(uint4, ks.lo[s]);
+        }
+        if (lane == 0) *reinterpret_cast<uint4*>(kpack + f * kPackBytes + 6 * 64 * 16) = make_uint4(__float_as_uint(kinf), 0u, 0u, 0u);
     }
 }
 
@@ -270,48 +776,89 @@ __global__ __launch_bounds__(kThreads) void e2m1_kernel(const float* __restrict_
 }
 
 // ------------------------------------------------------------------ launchers
-namespace {
-int grid_for(int64_t units, int max_blocks) {
-    const int64_t waves_per_block = kThreads / 64;
-    int64_t g = (units + waves_per_block - 1) / waves_per_block;
-    if (g > max_blocks) g = max_blocks;
+template <Mapping MAP, class Op>
+static hipError_t launch_map(Params p, hipStream_t st, const LaunchConfig& cfg) {
+    if (MAP == Mapping::Flat)
+        p.units = (p.nblocks + 63) / 64;
+    else
+        p.units = ((p.M + 63) / 64) * p.nb;
+    int64_t g = p.units < cfg.max_blocks ? p.units : cfg.max_blocks;
     if (g < 1) g = 1;
-    return (int)g;
-}
-}  // namespace
-
-template <int U, class Op>
-static hipError_t launch_flat(Params p, hipStream_t st, int max_blocks) {
-    p.units = (p.nblocks + 64 * U - 1) / (64 * U);
-    hipLaunchKernelGGL((flat_kernel<U, Op>), dim3(grid_for(p.units, max_blocks)), dim3(kThreads), 0, st, p);
-    return hipGetLastError();
-}
-
-template <int U, class Op>
-static hipError_t launch_column(Params p, hipStream_t st, int max_blocks) {
-    const int64_t row_tiles = (p.M + 64 * U - 1) / (64 * U);
-    p.units = row_tiles * p.nb;
-    hipLaunchKernelGGL((column_kernel<U, Op>), dim3(grid_for(p.units, max_blocks)), dim3(kThreads), 0, st, p);
+    hipLaunchKernelGGL((quant_kernel<MAP, Op>), dim3((unsigned)g), dim3(64), 0, st, p);
     return hipGetLastError();
 }
 
 template <class Op>
 static hipError_t launch_op(const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
+    if (map == Mapping::Flat) return launch_map<Mapping::Flat, Op>(p, st, cfg);
+    return launch_map<Mapping::Column, Op>(p, st, cfg);
+}
+
+template <int NA, int NB, int U, bool PACKED>
+static hipError_t launch_mfma_u(Params p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
+    int64_t g;
     if (map == Mapping::Flat) {
-        if (cfg.blocks_per_lane == 2) return launch_flat<2, Op>(p, st, cfg.max_blocks);
-        return launch_flat<1, Op>(p, st, cfg.max_blocks);
+        const int64_t steps = ((p.nblocks + 63) / 64 + U - 1) / U;
+        g = steps < cfg.max_waves ? steps : cfg.max_waves;
+        if (g < 1) g = 1;
+        hipLaunchKernelGGL((kron_mfma_kernel<Mapping::Flat, NA, NB, U, PACKED>), dim3((unsigned)g), dim3(64), 0, st, p);
+    } else {
+        const int64_t steps = ((p.M + 63) / 64 + U - 1) / U;  // per column block
+        int64_t per_col = (cfg.max_waves + p.nb - 1) / p.nb;   // workgroups per column block
+        if (per_col > steps) per_col = steps;
+        if (per_col < 1) per_col = 1;
+        g = per_col * p.nb;
+        hipLaunchKernelGGL((kron_mfma_kernel<Mapping::Column, NA, NB, U, PACKED>), dim3((unsigned)g), dim3(64), 0, st, p);
     }
-    if (cfg.blocks_per_lane == 2) return launch_column<2, Op>(p, st, cfg.max_blocks);
-    return launch_column<1, Op>(p, st, cfg.max_blocks);
+    return hipGetLastError();
+}
+
+template <int NA, int NB>
+static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
+    if (p.kpack) {
+        if (cfg.packed_one_unit) {
+            const int64_t units =
+                (map == Mapping::Flat) ? (p.nblocks + 63) / 64 : ((p.M + 63) / 64) * p.nb;
+            if (map == Mapping::Flat)
+                hipLaunchKernelGGL((kron_mfma_unit_kernel<Mapping::Flat, NA, NB>), dim3((unsigned)units), dim3(64), 0, st, p);
+            else
+                hipLaunchKernelGGL((kron_mfma_unit_kernel<Mapping::Column, NA, NB>), dim3((unsigned)units), dim3(64), 0, st, p);
+            return hipGetLastError();
+        }
+        if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, true>(p, map, st, cfg);
+        return launch_mfma_u<NA, NB, 1, true>(p, map, st, cfg);
+    }
+    if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, false>(p, map, st, cfg);
+    return launch_mfma_u<NA, NB, 1, false>(p, map, st, cfg);
+}
+
+hipError_t launch_pack(int a, const float* A, const float* B, int64_t nfac, uint8_t* kpack, hipStream_t st) {
+    const unsigned g = (unsigned)(nfac < 65536 ? nfac : 65536);
+    switch (a) {
+        case 4: hipLaunchKernelGGL((pack_kernel<4, 8>), dim3(g), dim3(64), 0, st, A, B, nfac, kpack); break;
+        case 2: hipLaunchKernelGGL((pack_kernel<2, 16>), dim3(g), dim3(64), 0, st, A, B, nfac, kpack); break;
+        case 8: hipLaunchKernelGGL((pack_kernel<8, 4>), dim3(g), dim3(64), 0, st, A, B, nfac, kpack); break;
+        case 1: hipLaunchKernelGGL((pack_kernel<1, 32>), dim3(g), dim3(64), 0, st, A, B, nfac, kpack); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
     switch (kind) {
         case Kind::Plain: return launch_op<PlainOp>(p, map, st, cfg);
         case Kind::Smooth:
-            if (map == Mapping::Flat) return launch_op<SmoothLaneOp>(p, map, st, cfg);
-            return launch_op<SmoothUniformOp>(p, map, st, cfg);
+            if (map == Mapping::Flat) return launch_map<Mapping::Flat, SmoothLaneOp>(p, st, cfg);
+            return launch_map<Mapping::Column, SmoothUniformOp>(p, st, cfg);
         case Kind::Hadamard: return launch_op<HadamardOp>(p, map, st, cfg);
+        case Kind::KronMfma:
+            switch (a) {
+                case 4: return launch_mfma<4, 8>(p, map, st, cfg);
+                case 2: return launch_mfma<2, 16>(p, map, st, cfg);
+                case 8: return launch_mfma<8, 4>(p, map, st, cfg);
+                case 1: return launch_mfma<1, 32>(p, map, st, cfg);
+                default: return hipErrorInvalidValue;
+            }
         case Kind::Kron:
             switch (a) {
                 case 4: return launch_op<KronOp<4, 8>>(p, map, st, cfg);

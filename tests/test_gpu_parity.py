@@ -72,8 +72,16 @@ def assert_mx_close(got, want, what=""):
         assert np.max(np.abs(yg.astype(np.float64) - yr) / den) <= 1e-5, f"{what}: y error"
 
 
-def gpu_quantize(X, A, B, want_y=True):
-    codes, scales, y = kq.quantize(dev_bf16(X), dev_f32(A), dev_f32(B), want_y=want_y)
+def gpu_quantize(X, A, B, want_y=True, exact=True):
+    fn = kq.quantize_exact if exact else kq.quantize
+    codes, scales, y = fn(dev_bf16(X), dev_f32(A), dev_f32(B), want_y=want_y)
+    return host(codes), host(scales), (host(y) if want_y else None)
+
+
+def gpu_quantize_packed(X, A, B, want_y=True):
+    Ad, Bd = dev_f32(A), dev_f32(B)
+    kpack = kq.pack_factors(Ad, Bd)
+    codes, scales, y = kq.quantize_packed(dev_bf16(X), Ad, Bd, kpack, want_y=want_y)
     return host(codes), host(scales), (host(y) if want_y else None)
 
 
@@ -115,9 +123,12 @@ def test_kroquant_parity(ab, per_block, M, d):
     a, b = ab
     X = synth.activations(M, d, "student_t3", seed=M * 7 + d, chan_frac=0.005, chan_factor=50)
     A, B = synth.factors(a, b, d // 32 if per_block else 1, seed=d + a)
-    got = gpu_quantize(X, A, B)
     want = oracle.quantize(X, A, B, want_y=True)
-    assert_exact(got, want, f"kron {ab} pb={per_block} {M}x{d}")
+    assert_exact(gpu_quantize(X, A, B, exact=True), want, f"exact {ab} pb={per_block} {M}x{d}")
+    hot = gpu_quantize(X, A, B, exact=False)
+    assert_mx_close(hot, want, f"mfma {ab} pb={per_block} {M}x{d}")
+    # the packed-K variant multiplies the same split terms: identical outputs
+    assert_exact(gpu_quantize_packed(X, A, B), hot, f"packed {ab} pb={per_block} {M}x{d}")
 
 
 @pytest.mark.parametrize("M,d", [(1, 32), (3, 64), (257, 1152), (64, 2240), (130, 5600)])
@@ -136,7 +147,9 @@ def test_comparators_parity(M, d):
 
 def test_tiny_config_all_paths():
     w = synth.workload("tiny_256x1152")
-    assert_exact(gpu_quantize(w.X, w.A, w.B), oracle.quantize(w.X, w.A, w.B, want_y=True), "tiny")
+    want = oracle.quantize(w.X, w.A, w.B, want_y=True)
+    assert_exact(gpu_quantize(w.X, w.A, w.B), want, "tiny exact")
+    assert_mx_close(gpu_quantize(w.X, w.A, w.B, exact=False), want, "tiny mfma")
 
 
 # ------------------------------------------------------------------ edge blocks
@@ -183,14 +196,19 @@ def test_edge_blocks_kron(ab):
     X = _edge_matrix()
     X = X[np.arange(X.shape[0]) != 5]  # an amplifying transform overflows the largest bf16
     A, B = synth.factors(a, b, 2, seed=3)
-    assert_exact(gpu_quantize(X, A, B), oracle.quantize(X, A, B, want_y=True), f"kron edges {ab}")
-    # identity factors: plain MXFP4 (the -0.0 row excepted, products give +0.0)
+    want = oracle.quantize(X, A, B, want_y=True)
+    assert_exact(gpu_quantize(X, A, B), want, f"kron edges {ab}")
+    assert_mx_close(gpu_quantize(X, A, B, exact=False), want, f"mfma edges {ab}")
+    # identity factors: plain MXFP4 (the -0.0 row excepted, products give +0.0);
+    # on the matrix-core path every block max here is a power of two or on a
+    # binade edge, so this also drives the exact re-evaluation of tiles
     Ai = np.eye(a, dtype=np.float32)[None]
     Bi = np.eye(b, dtype=np.float32)[None]
     keep = np.arange(X.shape[0]) != 1
-    c, s, _ = gpu_quantize(X[keep], Ai, Bi)
     cr, sr = oracle.mxfp4(X[keep])
-    assert np.array_equal(c, cr) and np.array_equal(s, sr)
+    for exact in (True, False):
+        c, s, _ = gpu_quantize(X[keep], Ai, Bi, exact=exact)
+        assert np.array_equal(c, cr) and np.array_equal(s, sr), exact
 
 
 # ------------------------------------------------------------------ layout, guards, determinism
@@ -207,12 +225,21 @@ def test_guard_bands_and_full_coverage():
         codes = cbuf[G:G + M * d // 2].view(M, d // 2)
         scales = sbuf[G:G + M * d // 32].view(M, d // 32)
         y = ybuf[G:G + M * d].view(M, d)
-        kq.quantize(dev_bf16(X), dev_f32(A), dev_f32(B), codes=codes, scales=scales, y=y)
+        kq.quantize_exact(dev_bf16(X), dev_f32(A), dev_f32(B), codes=codes, scales=scales, y=y)
         cb, sb, yb = host(cbuf), host(sbuf), host(ybuf)
         assert np.all(cb[:G] == canary) and np.all(cb[-G:] == canary)
         assert np.all(sb[:G] == canary) and np.all(sb[-G:] == canary)
         assert np.all(np.isnan(yb[:G])) and np.all(np.isnan(yb[-G:]))
         assert_exact((cb[G:-G].reshape(M, -1), sb[G:-G].reshape(M, -1), yb[G:-G].reshape(M, d)), want)
+        cbuf.fill_(canary)
+        sbuf.fill_(canary)
+        ybuf.fill_(float("nan"))
+        kq.quantize(dev_bf16(X), dev_f32(A), dev_f32(B), codes=codes, scales=scales, y=y)
+        cb, sb, yb = host(cbuf), host(sbuf), host(ybuf)
+        assert np.all(cb[:G] == canary) and np.all(cb[-G:] == canary)
+        assert np.all(sb[:G] == canary) and np.all(sb[-G:] == canary)
+        assert np.all(np.isnan(yb[:G])) and np.all(np.isnan(yb[-G:]))
+        assert_mx_close((cb[G:-G].reshape(M, -1), sb[G:-G].reshape(M, -1), yb[G:-G].reshape(M, d)), want)
 
 
 def test_flat_and_column_mappings_agree():
@@ -221,11 +248,12 @@ def test_flat_and_column_mappings_agree():
     M, d = 300, 3072
     X = synth.activations(M, d, "student_t3", seed=4, chan_frac=0.005, chan_factor=50)
     A, B = synth.factors(4, 8, 1, seed=6)
-    g1 = gpu_quantize(X, A, B)
-    g2 = gpu_quantize(X, np.repeat(A, d // 32, 0), np.repeat(B, d // 32, 0))
-    assert_exact(g1, g2)
-    g3 = gpu_quantize(X, A, B)
-    assert_exact(g1, g3)
+    for exact in (True, False):
+        g1 = gpu_quantize(X, A, B, exact=exact)
+        g2 = gpu_quantize(X, np.repeat(A, d // 32, 0), np.repeat(B, d // 32, 0), exact=exact)
+        assert_exact(g1, g2)
+        g3 = gpu_quantize(X, A, B, exact=exact)
+        assert_exact(g1, g3)
 
 
 def test_non_default_stream():
@@ -236,9 +264,12 @@ def test_non_default_stream():
     Xd, Ad, Bd = dev_bf16(X), dev_f32(A), dev_f32(B)
     torch.cuda.synchronize()
     with torch.cuda.stream(s):
-        c, sc, y = kq.quantize(Xd, Ad, Bd, want_y=True)
+        c, sc, y = kq.quantize_exact(Xd, Ad, Bd, want_y=True)
+        c2, sc2, y2 = kq.quantize(Xd, Ad, Bd, want_y=True)
     s.synchronize()
-    assert_exact((c.cpu().numpy(), sc.cpu().numpy(), y.cpu().numpy()), oracle.quantize(X, A, B, want_y=True))
+    want = oracle.quantize(X, A, B, want_y=True)
+    assert_exact((c.cpu().numpy(), sc.cpu().numpy(), y.cpu().numpy()), want)
+    assert_mx_close((c2.cpu().numpy(), sc2.cpu().numpy(), y2.cpu().numpy()), want)
 
 
 # ------------------------------------------------------------------ weight side
@@ -255,7 +286,7 @@ def test_weight_transform(ab, per_block):
     assert_mx_close(got, (cr, sr, yr), f"weight {ab}")
     # eq. (1): <x T, w T^-T> = <x, w>
     X = synth.activations(8, d, "normal", seed=5)
-    _, _, y = gpu_quantize(X, A, B)
+    _, _, y = gpu_quantize(X, A, B, exact=False)
     lhs = y.astype(np.float64) @ got[2].astype(np.float64).T
     xf, wf = oracle.bf16_to_f32(X).astype(np.float64), oracle.bf16_to_f32(W).astype(np.float64)
     assert np.max(np.abs(lhs - xf @ wf.T) / (np.abs(xf) @ np.abs(wf).T)) < 2e-5
@@ -271,9 +302,15 @@ def test_full_size_workloads(name):
     """Every output of the DiT-shaped workloads, KroQuant and the comparators."""
     w = synth.workload(name)
     Xd = dev_bf16(w.X)
-    c, s, _ = kq.quantize(Xd, dev_f32(w.A), dev_f32(w.B))
-    cr, sr, _ = oracle.quantize(w.X, w.A, w.B)
+    cr, sr, yr = oracle.quantize(w.X, w.A, w.B, want_y=True)
+    c, s, _ = kq.quantize_exact(Xd, dev_f32(w.A), dev_f32(w.B))
     assert_exact((host(c), host(s), None), (cr, sr, None), name)
+    c, s, y = kq.quantize(Xd, dev_f32(w.A), dev_f32(w.B), want_y=True)
+    hot = (host(c), host(s), host(y))
+    assert_mx_close(hot, (cr, sr, yr), name + " mfma")
+    kp = kq.pack_factors(dev_f32(w.A), dev_f32(w.B))
+    c, s, y = kq.quantize_packed(Xd, dev_f32(w.A), dev_f32(w.B), kp, want_y=True)
+    assert_exact((host(c), host(s), host(y)), hot, name + " packed")
     c, s, _ = kq.smoothquant(Xd, dev_f32(w.mult))
     cr, sr, _ = oracle.smoothquant(w.X, w.mult)
     assert_exact((host(c), host(s), None), (cr, sr, None), name + " smooth")
@@ -287,10 +324,15 @@ def test_large_per_block_sampled_rows(name):
     """Large per-block-factor workload at full size; the oracle recomputes a
     sample of rows (first, last, and random ones) one by one."""
     w = synth.workload(name)
-    c, s, _ = kq.quantize(dev_bf16(w.X), dev_f32(w.A), dev_f32(w.B))
-    c, s = host(c), host(s)
     M = w.X.shape[0]
     rows = np.unique(np.concatenate([[0, 1, 63, 64, M - 1],
                                      np.random.default_rng(0).choice(M, 120, replace=False)]))
     cr, sr, _ = oracle.quantize(np.ascontiguousarray(w.X[rows]), w.A, w.B)
-    assert_exact((c[rows], s[rows], None), (cr, sr, None), name)
+    Xd, Ad, Bd = dev_bf16(w.X), dev_f32(w.A), dev_f32(w.B)
+    c, s, _ = kq.quantize_exact(Xd, Ad, Bd)
+    assert_exact((host(c)[rows], host(s)[rows], None), (cr, sr, None), name)
+    c, s, _ = kq.quantize(Xd, Ad, Bd)
+    assert_mx_close((host(c)[rows], host(s)[rows], None), (cr, sr, None), name + " mfma")
+    kp = kq.pack_factors(Ad, Bd)
+    c2, s2, _ = kq.quantize_packed(Xd, Ad, Bd, kp)
+    assert np.array_equal(host(c2), host(c)) and np.array_equal(host(s2), host(s))

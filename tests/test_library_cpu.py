@@ -74,6 +74,19 @@ def test_zero_rows_is_a_no_op():
     assert L.kq_e2m1_encode(FAKE, 0, 127, FAKE, None) == SUCCESS
 
 
+def test_pack_and_packed_reject():
+    L = kq.lib()
+    assert L.kq_pack_factors(FAKE, FAKE, 4, 4, 1, FAKE, None) == UNSUPPORTED
+    assert L.kq_pack_factors(FAKE, FAKE, 4, 8, 0, FAKE, None) == INVALID
+    assert L.kq_pack_factors(FAKE, None, 4, 8, 1, FAKE, None) == NULLP
+    assert L.kq_pack_factors(FAKE, FAKE, 4, 8, 1, FAKE + 4, None) == MISALIGNED
+    assert L.kq_quantize_packed(FAKE, 4, 64, FAKE, FAKE, 4, 8, 1, None, FAKE, FAKE, None, None) == NULLP
+    assert L.kq_quantize_packed(FAKE, 4, 64, FAKE, FAKE, 4, 8, 1, FAKE + 8, FAKE, FAKE, None, None) == MISALIGNED
+    assert L.kq_quantize_packed(FAKE, 4, 48, FAKE, FAKE, 4, 8, 1, FAKE, FAKE, FAKE, None, None) == INVALID
+    assert L.kq_quantize_packed(FAKE, 0, 64, FAKE, FAKE, 4, 8, 1, FAKE, FAKE, FAKE, None, None) == SUCCESS
+    assert kq.PACK_BYTES_PER_FACTOR == 6 * 64 * 16 + 16
+
+
 def test_comparators_reject():
     L = kq.lib()
     assert L.kq_smoothquant_quantize(FAKE, 4, 64, None, FAKE, FAKE, None, None) == NULLP
