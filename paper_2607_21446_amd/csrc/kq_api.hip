@@ -87,6 +87,14 @@ kq::LaunchConfig default_config() {
             if (v >= 1 && v <= (1 << 30)) c.max_waves = v;
         }
         if (const char* e = std::getenv("KQ_PACKED_PERSISTENT")) c.packed_one_unit = std::atoi(e) == 0;
+        if (const char* e = std::getenv("KQ_SMOOTH_PATH")) {
+            const int v = std::atoi(e);
+            if (v >= 0 && v <= 3) c.smooth_path = v;
+        }
+        if (const char* e = std::getenv("KQ_SMOOTH_WAVES")) {
+            const long long v = std::atoll(e);
+            if (v >= 1 && v <= (1 << 24)) c.smooth_waves = v;
+        }
         if (const char* e = std::getenv("KQ_UNITS_PER_WAVE")) {
             const int v = std::atoi(e);
             if (v == 1 || v == 2) c.units_per_wave = v;

@@ -317,6 +317,14 @@ __device__ __forceinline__ uint32_t other_half(uint32_t v) {
 }
 __device__ __forceinline__ float other_half(float v) { return __uint_as_float(other_half(__float_as_uint(v))); }
 
+// max(v, v of lane l ^ 32) for v >= 0 as fp32 bit patterns: after the swap one
+// of the pair holds this lane's value and the other its partner's, in either
+// half, so their max needs no lane select.
+__device__ __forceinline__ uint32_t max_with_other_half(uint32_t v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return max((uint32_t)r[0], (uint32_t)r[1]);
+}
+
 // This lane's slice of K = A (x) B as the A operand of v_mfma_f32_32x32x16_bf16:
 // lane l holds K[n][k] for n = l % 32 and k = 16 s + 8 (l / 32) + c (c = 0..7)
 // in k-step s = 0, 1; K[n][k] = fp32(A[n / b][k / b] * B[n % b][k % b])
@@ -387,20 +395,163 @@ __device__ __forceinline__ float max_abs_bf16(const uint4 (&r)[2]) {
     return __uint_as_float(top << 16);
 }
 
-// Exact fixed-order evaluation of one block by 32 cooperating lanes: lane n
-// (n = lane % 32; both half-waves compute the same) evaluates output
-// y[n] = Y[o][i], n = o*b + i, with the FMA chains of KronOp:
+// SmoothQuant with the per-channel multiply applied to each 16-byte input
+// chunk while the chunks are still in the coalesced order (its 8 multipliers
+// are then 32 contiguous bytes, also coalesced across the wave), then parked
+// in LDS as fp32 and read back one block per lane.  LDS slot (16 B) of half
+// e of chunk m of block b: 8b + ((2m + e) ^ (b & 7)).
+__device__ __forceinline__ int lds_slot8(int b, int m8) { return 8 * b + (m8 ^ (b & 7)); }
+
+__global__ __launch_bounds__(64) void smooth_chunk_kernel(const Params p) {
+    __shared__ float4 lds[512];
+    const int lane = threadIdx.x;
+    const uint32_t nchunk_row = (uint32_t)(p.nb * 4);  // multiplier chunks per row (d < 2^29)
+    for (int64_t u = blockIdx.x; u < p.units; u += gridDim.x) {
+        const int64_t first = u * 64;
+        const int nvalid = (int)min<int64_t>(64, p.nblocks - first);
+        const uint4* src = reinterpret_cast<const uint4*>(p.X) + first * 4;
+        const uint32_t cbase = (uint32_t)((first * 4) % nchunk_row);  // wave-uniform
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int ci = 64 * c + lane;
+            const int b = ci >> 2, m = ci & 3;
+            float x[8];
+            float4 lo4 = make_float4(0.f, 0.f, 0.f, 0.f), hi4 = lo4;
+            if (b < nvalid) {
+                unpack8(load_nt(src + ci), x);
+                // multiplier chunk of this input chunk: (first*4 + ci) mod (4 nb)
+                uint32_t mc = cbase + (uint32_t)ci;
+                if (nchunk_row >= 256u) {
+                    if (mc >= nchunk_row) mc -= nchunk_row;
+                } else {
+                    mc %= nchunk_row;
+                }
+                const float4* mv = reinterpret_cast<const float4*>(p.mult) + 2 * mc;
+                const float4 m0 = mv[0], m1 = mv[1];
+                lo4 = make_float4(x[0] * m0.x, x[1] * m0.y, x[2] * m0.z, x[3] * m0.w);
+                hi4 = make_float4(x[4] * m1.x, x[5] * m1.y, x[6] * m1.z, x[7] * m1.w);
+            }
+            lds[lds_slot8(b, 2 * m)] = lo4;
+            lds[lds_slot8(b, 2 * m + 1)] = hi4;
+        }
+        wave_lds_sync();
+        float y[32];
+#pragma unroll
+        for (int m8 = 0; m8 < 8; ++m8) {
+            const float4 v = lds[lds_slot8(lane, m8)];
+            y[4 * m8] = v.x;
+            y[4 * m8 + 1] = v.y;
+            y[4 * m8 + 2] = v.z;
+            y[4 * m8 + 3] = v.w;
+        }
+        wave_lds_sync();
+        if (lane < nvalid) {
+            const int64_t blk = first + lane;
+            uint32_t w[4];
+            const uint32_t sb = encode32(y, w);
+            if (p.codes) {
+                *reinterpret_cast<uint4*>(p.codes + blk * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+                p.scales[blk] = (uint8_t)sb;
+            }
+            if (p.y) {
+                float4* dst = reinterpret_cast<float4*>(p.y + blk * 32);
+#pragma unroll
+                for (int m = 0; m < 8; ++m)
+                    dst[m] = make_float4(y[4 * m], y[4 * m + 1], y[4 * m + 2], y[4 * m + 3]);
+            }
+        }
+    }
+}
+
+// SmoothQuant, column-stationary: the grid stride G (in 64-block units) is a
+// multiple of nb / gcd(nb, 64), so 64 G is a multiple of nb and lane l of a
+// workgroup keeps the same column block (64 u + l) mod nb in every unit it
+// handles.  Its 32 multipliers are loaded once; the next unit's input loads
+// are issued before the current unit is encoded.
+__global__ __launch_bounds__(64) void smooth_stationary_kernel(const Params p) {
+    __shared__ uint4 lds[256];
+    const int lane = threadIdx.x;
+    const int64_t u0 = blockIdx.x, ustep = gridDim.x;
+    if (u0 >= p.units) return;
+    const int64_t col = (u0 * 64 + lane) % p.nb;
+    float mul[32];
+    {
+        const float4* mv = reinterpret_cast<const float4*>(p.mult + col * 32);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const float4 f = mv[k];
+            mul[4 * k] = f.x;
+            mul[4 * k + 1] = f.y;
+            mul[4 * k + 2] = f.z;
+            mul[4 * k + 3] = f.w;
+        }
+    }
+    uint4 v[4];
+    auto issue = [&](int64_t u) {
+        const int64_t first = u * 64;
+        const int nvalid = (int)min<int64_t>(64, p.nblocks - first);
+        const uint4* src = reinterpret_cast<const uint4*>(p.X) + first * 4;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int ci = 64 * c + lane;
+            v[c] = make_uint4(0u, 0u, 0u, 0u);
+            if ((ci >> 2) < nvalid) v[c] = load_nt(src + ci);
+        }
+    };
+    issue(u0);
+    for (int64_t u = u0; u < p.units; u += ustep) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int ci = 64 * c + lane;
+            lds[lds_slot(ci >> 2, ci & 3)] = v[c];
+        }
+        if (u + ustep < p.units) issue(u + ustep);
+        wave_lds_sync();
+        uint4 raw[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) raw[m] = lds[lds_slot(lane, m)];
+        wave_lds_sync();
+        const int64_t blk = u * 64 + lane;
+        if (blk < p.nblocks) {
+            float x[32], y[32];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) unpack8(raw[m], x + 8 * m);
+#pragma unroll
+            for (int k = 0; k < 32; ++k) y[k] = x[k] * mul[k];
+            uint32_t w[4];
+            const uint32_t sb = encode32(y, w);
+            if (p.codes) {
+                *reinterpret_cast<uint4*>(p.codes + blk * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+                p.scales[blk] = (uint8_t)sb;
+            }
+            if (p.y) {
+                float4* dst = reinterpret_cast<float4*>(p.y + blk * 32);
+#pragma unroll
+                for (int m = 0; m < 8; ++m)
+                    dst[m] = make_float4(y[4 * m], y[4 * m + 1], y[4 * m + 2], y[4 * m + 3]);
+            }
+        }
+    }
+}
+
+// Exact fixed-order evaluation of up to two blocks by 32 cooperating lanes
+// each: half-wave h takes block blk[h] (skipped if negative); lane n
+// (n = lane % 32) evaluates output y[n] = Y[o][i], n = o*b + i, with the FMA
+// chains of KronOp:
 //   Z[p][i] = B[i][0]*x[p*b] then fma(B[i][q], x[p*b+q], .), q = 1..b-1,
 //   Y[o][i] = A[o][0]*Z[0][i] then fma(A[o][p], Z[p][i], .), p = 1..a-1.
-// Called with all 64 lanes active; `blk` lies in this wave's LDS unit.
+// Called with all 64 lanes active; the blocks lie in this wave's LDS unit.
 template <int NA, int NB>
-__device__ __forceinline__ void exact_block_coop(const uint4* unit_lds, int blk, const float* Af, const float* Bf,
-                                              const Params& p, int64_t out_blk) {
+__device__ __forceinline__ void exact_blocks_coop(const uint4* unit_lds, int blk0, int blk1, const float* Af,
+                                                  const float* Bf, const Params& p, int64_t out0, int64_t out1) {
+    const int h = threadIdx.x >> 5;
     const int n = threadIdx.x & 31;
     const int o = n / NB, i = n % NB;
+    const int blk = h ? blk1 : blk0;
+    const int64_t out_blk = h ? out1 : out0;
     float x[32];
 #pragma unroll
-    for (int m = 0; m < 4; ++m) unpack8(unit_lds[lds_slot(blk, m)], x + 8 * m);
+    for (int m = 0; m < 4; ++m) unpack8(unit_lds[lds_slot(blk < 0 ? 0 : blk, m)], x + 8 * m);
     float acc = 0.0f;
 #pragma unroll
     for (int pr = 0; pr < NA; ++pr) {
@@ -411,16 +562,33 @@ __device__ __forceinline__ void exact_block_coop(const uint4* unit_lds, int blk,
     }
     float am = fabsf(acc);
 #pragma unroll
-    for (int off = 16; off >= 1; off >>= 1) am = fmaxf(am, __shfl_xor(am, off));
+    for (int off = 16; off >= 1; off >>= 1) am = fmaxf(am, __shfl_xor(am, off));  // within the half-wave
     const uint32_t sb = e8m0_byte(am);
-    const float next = __shfl_down(acc, 1);  // y[n + 1]
+    const float next = __shfl_down(acc, 1);  // y[n + 1] (n even: same half-wave)
     const uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, acc, next, __uint_as_float(sb << 23), 0);
-    if (threadIdx.x < 32) {
+    if (blk >= 0) {
         if (p.codes) {
             if ((n & 1) == 0) p.codes[out_blk * 16 + (n >> 1)] = (uint8_t)(c & 0xFFu);
             if (n == 0) p.scales[out_blk] = (uint8_t)sb;
         }
         if (p.y) p.y[out_blk * 32 + n] = acc;
+    }
+}
+
+// all blocks flagged in `edges` (bit b = block b of the unit), two at a time
+template <int NA, int NB>
+__device__ __forceinline__ void exact_flagged(uint64_t edges, const uint4* unit_lds, int64_t first, uint32_t bstride,
+                                              const float* Af, const float* Bf, const Params& p) {
+    while (edges) {
+        const int b0 = __builtin_ctzll(edges);
+        edges &= edges - 1;
+        int b1 = -1;
+        if (edges) {
+            b1 = __builtin_ctzll(edges);
+            edges &= edges - 1;
+        }
+        exact_blocks_coop<NA, NB>(unit_lds, b0, b1, Af, Bf, p, first + (int64_t)b0 * bstride,
+                                  first + (int64_t)(b1 < 0 ? 0 : b1) * bstride);
     }
 }
 
@@ -495,6 +663,25 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
     };
     if (s0 < nsteps) issue(s0);
     if (!PACKED) kbound = build_k<NA, NB>(kf, ks) * 0x1p-16f;
+    // no row of A and no row of B with every sign bit set: then an all-(+0)
+    // input block gives +0 for every output in the fixed order
+    bool zero_ok;
+    if (PACKED) {
+        zero_ok = __float_as_uint(ld_uniform(reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16), 2)) != 0u;
+    } else {
+        bool neg_row = false;
+        if (lane < NA) {
+            bool all = true;
+            for (int j = 0; j < NA; ++j) all = all && (__float_as_uint(Af[lane * NA + j]) >> 31);
+            neg_row = all;
+        }
+        if (lane < NB) {
+            bool all = true;
+            for (int j = 0; j < NB; ++j) all = all && (__float_as_uint(Bf[lane * NB + j]) >> 31);
+            neg_row = neg_row || all;
+        }
+        zero_ok = __builtin_amdgcn_ballot_w64(neg_row) == 0;
+    }
     for (int64_t st = s0; st < nsteps; st += sstep) {
         int64_t first[U];
         int nvalid[U];
@@ -559,7 +746,13 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
                 const float bnd = kbound * __uint_as_float(mxb);
                 const uint32_t e = amb >> 23;
                 const float lo_p2 = __uint_as_float(e << 23), hi_p2 = __uint_as_float((e + 1u) << 23);
-                const bool near = valid && (e <= 3u || am - lo_p2 <= bnd || hi_p2 - am <= bnd);
+                bool near = valid && (e <= 3u || am - lo_p2 <= bnd || hi_p2 - am <= bnd);
+                if (amb == 0u && zero_ok && mxb == 0u) {
+                    // all outputs +-0: exact when the inputs are all +0 (bit patterns 0)
+                    const uint32_t any = raw[t][0].x | raw[t][0].y | raw[t][0].z | raw[t][0].w | raw[t][1].x |
+                                         raw[t][1].y | raw[t][1].z | raw[t][1].w;
+                    if ((any | other_half(any)) == 0u) near = false;
+                }
                 const uint64_t ob = (uint64_t)first[k] + (uint64_t)((uint32_t)bt * bstride);  // output block
                 const uint32_t sb = e > 2u ? e - 2u : 0u;
                 const float sc = __uint_as_float(sb << 23);
@@ -595,13 +788,8 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
                     }
                 }
                 // blocks whose amax is on a binade edge: the fixed evaluation order decides
-                uint64_t edge = __builtin_amdgcn_ballot_w64(near) & 0xFFFFFFFFull;
-                while (edge) {
-                    const int b = __builtin_ctzll(edge);
-                    edge &= edge - 1;
-                    const int64_t blk_out = first[k] + (int64_t)(32 * t + b) * bstride;
-                    exact_block_coop<NA, NB>(lds[k], 32 * t + b, Af, Bf, p, blk_out);
-                }
+                exact_flagged<NA, NB>((__builtin_amdgcn_ballot_w64(near) & 0xFFFFFFFFull) << (32 * t), lds[k],
+                                      first[k], bstride, Af, Bf, p);
             }
         }
         wave_lds_sync();  // the next step's writes come after this step's reads
@@ -612,6 +800,14 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
 // (no loop): few live registers, so every wave of a large grid is resident
 // at once and all input loads are in flight from the start.  FLAT: unit =
 // blockIdx.x;  COLUMN: column block j = blockIdx.x % nb, rows 64 * (blockIdx.x / nb).
+//
+// Binade-edge test.  With e the error of this path and of the fixed order
+// (|e| <= 116 u sum_k |K_nk||x_k| <= 116 u ||K||_inf max|x|, u = 2^-24) and
+// max|x| <= ||K^-1||_inf max|Kx| <= ||K^-1||_inf (amax + |e|), the two amax
+// differ by at most 116 u cond (1 - 104 u cond)^-1 amax <= 2^-16 cond amax =
+// rho amax whenever cond = cond_inf(K) <= 2^16 (rho is +inf above).  A block
+// whose amax lies within rho amax of a power of two is re-evaluated in the
+// fixed order, so its E8M0 scale equals the fixed-order one.
 template <Mapping MAP, int NA, int NB>
 __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
     __shared__ uint4 lds[256];
@@ -663,7 +859,14 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
         ks.mid[s] = __builtin_bit_cast(bf16x8, pk[(1 * 2 + s) * 64 + lane]);
         ks.lo[s] = __builtin_bit_cast(bf16x8, pk[(2 * 2 + s) * 64 + lane]);
     }
-    const float kbound = ld_uniform(reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16), 0) * 0x1p-16f;
+    const float rho = ld_uniform(reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16), 1);
+    // nonzero when no row of A and no row of B has every sign bit set: then an
+    // all-(+0) input block gives +0 for every output in the fixed order
+    const bool zero_ok = __float_as_uint(ld_uniform(reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16), 2)) != 0u;
+    // output bases of the unit (wave-uniform) and this lane's block offsets
+    uint8_t* const codes_u = p.codes + first * 16;
+    uint8_t* const scales_u = p.scales + first;
+    float* const y_u = p.y + first * 32;
     wave_lds_sync();
     uint64_t edges = 0;  // blocks of the unit on a binade edge (bit = block index)
 #pragma unroll
@@ -684,19 +887,21 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
 #pragma unroll
         for (int s = 0; s < 2; ++s)
             acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.hi[s], __builtin_bit_cast(bf16x8, raw[s]), acc, 0, 0, 0);
+        // lane holds y[8q + 4h + r] of block bt in acc[4q + r]
         float am = 0.0f;
 #pragma unroll
         for (int i = 0; i < 16; ++i) am = fmaxf(am, fabsf(acc[i]));
-        uint32_t amb = __float_as_uint(am);
-        amb = max(amb, other_half(amb));
+        const uint32_t amb = max_with_other_half(__float_as_uint(am));
         am = __uint_as_float(amb);
-        uint32_t mxb = __float_as_uint(max_abs_bf16(raw));
-        mxb = max(mxb, other_half(mxb));
-        const float bnd = kbound * __uint_as_float(mxb);
         const uint32_t e = amb >> 23;
-        const float lo_p2 = __uint_as_float(e << 23), hi_p2 = __uint_as_float((e + 1u) << 23);
-        const bool near = valid && (e <= 3u || am - lo_p2 <= bnd || hi_p2 - am <= bnd);
-        const uint64_t ob = (uint64_t)first + (uint64_t)((uint32_t)bt * bstride);
+        const float win = rho * am;
+        bool near = valid && (e <= 3u || am - __uint_as_float(e << 23) <= win ||
+                              __uint_as_float((e + 1u) << 23) - am <= win);
+        if (amb == 0u && zero_ok) {
+            // all outputs +-0: exact when the inputs are all +0 (bit patterns 0)
+            const uint32_t any = raw[0].x | raw[0].y | raw[0].z | raw[0].w | raw[1].x | raw[1].y | raw[1].z | raw[1].w;
+            if ((any | other_half(any)) == 0u) near = false;
+        }
         const uint32_t sb = e > 2u ? e - 2u : 0u;
         const float sc = __uint_as_float(sb << 23);
         uint32_t w[4];
@@ -705,6 +910,8 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
             uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, acc[4 * q], acc[4 * q + 1], sc, 0);
             w[q] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, acc[4 * q + 2], acc[4 * q + 3], sc, 1);
         }
+        // code dword q of the block = [lower half: lane h=0's w[q]] [upper half: lane h=1's w[q]];
+        // lane h=0 stores dwords 0-1, lane h=1 dwords 2-3
         const uint32_t send = h ? (w[0] | (w[1] << 16)) : (w[2] | (w[3] << 16));
         const uint32_t recv = other_half(send);
         uint2 out;
@@ -715,13 +922,14 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
             out.x = (recv & 0xFFFFu) | (w[2] << 16);
             out.y = (recv >> 16) | (w[3] << 16);
         }
+        const uint32_t ob = (uint32_t)bt * bstride;  // this lane's block, relative to `first`
         if (valid && !near) {
             if (p.codes) {
-                *reinterpret_cast<uint2*>(p.codes + ob * 16 + 8 * h) = out;
-                if (h == 0) p.scales[ob] = (uint8_t)sb;
+                *reinterpret_cast<uint2*>(codes_u + ob * 16u + 8u * h) = out;
+                if (h == 0) scales_u[ob] = (uint8_t)sb;
             }
             if (p.y) {
-                float* yb = p.y + ob * 32 + 4 * h;
+                float* yb = y_u + ob * 32u + 4u * h;
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
                     *reinterpret_cast<float4*>(yb + 8 * q) =
@@ -731,28 +939,94 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
         edges |= (__builtin_amdgcn_ballot_w64(near) & 0xFFFFFFFFull) << (32 * t);
     }
     // blocks whose amax is on a binade edge: the fixed evaluation order decides
-    const float* Af = p.A + f * (NA * NA);
-    const float* Bf = p.B + f * (NB * NB);
-    while (edges) {
-        const int b = __builtin_ctzll(edges);
-        edges &= edges - 1;
-        exact_block_coop<NA, NB>(lds, b, Af, Bf, p, first + (int64_t)b * bstride);
-    }
+    exact_flagged<NA, NB>(edges, lds, first, bstride, p.A + f * (NA * NA), p.B + f * (NB * NB), p);
 }
 
 // Materialise and split K = A (x) B for every factor pair, in the lane layout
 // of the matrix-core A operand (offline step; the K1 variant of Sec. 3.5
 // keeps the dense 32x32 blocks in HBM).  Layout per pair (kPackBytes):
-// uint4 [3 terms: hi, mid, lo][2 k-steps][64 lanes], then fp32 ||K||_inf.
+// uint4 [3 terms: hi, mid, lo][2 k-steps][64 lanes], then fp32 ||K||_inf,
+// the relative binade-edge window rho (see kron_mfma_unit_kernel) and the
+// all-(+0)-input flag.
+// true when no row of F has every entry's sign bit set
+__device__ bool no_negative_row(const float* F, int n) {
+    for (int i = 0; i < n; ++i) {
+        bool all = true;
+        for (int j = 0; j < n; ++j) all = all && (__float_as_uint(F[i * n + j]) >> 31);
+        if (all) return false;
+    }
+    return true;
+}
+
+__device__ double norm_inf_f64(const float* F, int n) {
+    double best = 0.0;
+    for (int i = 0; i < n; ++i) {
+        double r = 0.0;
+        for (int j = 0; j < n; ++j) r += fabs((double)F[i * n + j]);
+        best = fmax(best, r);
+    }
+    return best;
+}
+
+// ||F^-1||_inf by fp64 Gauss-Jordan with partial pivoting in `work`
+// (n x 2n doubles); +inf if a pivot vanishes.
+__device__ double inverse_norm_inf_f64(const float* F, int n, double* work) {
+    const int w = 2 * n;
+    for (int i = 0; i < n; ++i)
+        for (int j = 0; j < w; ++j) work[i * w + j] = j < n ? (double)F[i * n + j] : (j - n == i ? 1.0 : 0.0);
+    for (int c = 0; c < n; ++c) {
+        int piv = c;
+        for (int r = c + 1; r < n; ++r)
+            if (fabs(work[r * w + c]) > fabs(work[piv * w + c])) piv = r;
+        const double pv = work[piv * w + c];
+        if (pv == 0.0) return __builtin_inf();
+        if (piv != c)
+            for (int j = 0; j < w; ++j) {
+                const double t = work[c * w + j];
+                work[c * w + j] = work[piv * w + j];
+                work[piv * w + j] = t;
+            }
+        for (int j = 0; j < w; ++j) work[c * w + j] /= pv;
+        for (int r = 0; r < n; ++r) {
+            if (r == c) continue;
+            const double fct = work[r * w + c];
+            if (fct != 0.0)
+                for (int j = 0; j < w; ++j) work[r * w + j] -= fct * work[c * w + j];
+        }
+    }
+    double best = 0.0;
+    for (int i = 0; i < n; ++i) {
+        double r = 0.0;
+        for (int j = n; j < w; ++j) r += fabs(work[i * w + j]);
+        best = fmax(best, r);
+    }
+    return best;
+}
+
 template <int NA, int NB>
 __global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ A, const float* __restrict__ B,
                                                   int64_t nfac, uint8_t* __restrict__ kpack) {
+    __shared__ double pack_lds[32 * 64];  // Gauss-Jordan workspace of lane 0
     const int lane = threadIdx.x;
     for (int64_t f = blockIdx.x; f < nfac; f += gridDim.x) {
         KFactors<NA, NB> kf;
         load_k_factors<NA, NB>(A + f * (NA * NA), B + f * (NB * NB), lane, kf);
         KSlices ks;
         const float kinf = build_k<NA, NB>(kf, ks);
+        // relative binade-edge window rho = 2^-16 cond_inf(K), cond_inf(K) =
+        // ||A||_inf ||B||_inf ||A^-1||_inf ||B^-1||_inf (Kronecker norms multiply)
+        float rho = __builtin_inff();
+        if (lane == 0) {
+            double* work = reinterpret_cast<double*>(pack_lds);
+            const double na = norm_inf_f64(A + f * (NA * NA), NA), nb_ = norm_inf_f64(B + f * (NB * NB), NB);
+            const double nai = inverse_norm_inf_f64(A + f * (NA * NA), NA, work);
+            const double nbi = inverse_norm_inf_f64(B + f * (NB * NB), NB, work);
+            const double cond = 1.01 * na * nb_ * nai * nbi;
+            if (cond <= 65536.0) rho = (float)(cond * 0x1p-16);
+        }
+        rho = __shfl(rho, 0);
+        uint32_t zero_ok = 0u;
+        if (lane == 0) zero_ok = (no_negative_row(A + f * (NA * NA), NA) && no_negative_row(B + f * (NB * NB), NB)) ? 1u : 0u;
         uint4* pk = reinterpret_cast<uint4*>(kpack + f * kPackBytes);
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
@@ -760,7 +1034,9 @@ __global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ A, c
             pk[(1 * 2 + s) * 64 + lane] = __builtin_bit_cast(uint4, ks.mid[s]);
             pk[(2 * 2 + s) * 64 + lane] = __builtin_bit_cast(uint4, ks.lo[s]);
         }
-        if (lane == 0) *reinterpret_cast<uint4*>(kpack + f * kPackBytes + 6 * 64 * 16) = make_uint4(__float_as_uint(kinf), 0u, 0u, 0u);
+        if (lane == 0)
+            *reinterpret_cast<uint4*>(kpack + f * kPackBytes + 6 * 64 * 16) =
+                make_uint4(__float_as_uint(kinf), __float_as_uint(rho), zero_ok, 0u);
     }
 }
 
@@ -848,8 +1124,26 @@ hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st
     switch (kind) {
         case Kind::Plain: return launch_op<PlainOp>(p, map, st, cfg);
         case Kind::Smooth:
-            if (map == Mapping::Flat) return launch_map<Mapping::Flat, SmoothLaneOp>(p, st, cfg);
-            return launch_map<Mapping::Column, SmoothUniformOp>(p, st, cfg);
+            if (cfg.smooth_path == 1) return launch_map<Mapping::Flat, SmoothLaneOp>(p, st, cfg);
+            if (cfg.smooth_path == 2) return launch_map<Mapping::Column, SmoothUniformOp>(p, st, cfg);
+            if (cfg.smooth_path == 3) {
+                Params q = p;
+                q.units = (p.nblocks + 63) / 64;
+                int64_t a = p.nb, b = 64;  // gcd(nb, 64)
+                while (b) { const int64_t t = a % b; a = b; b = t; }
+                const int64_t period = p.nb / a;  // stride multiple that keeps columns fixed
+                int64_t g = (cfg.smooth_waves + period - 1) / period * period;
+                if (g > q.units) g = q.units;  // one unit per workgroup: no stride needed
+                hipLaunchKernelGGL(smooth_stationary_kernel, dim3((unsigned)g), dim3(64), 0, st, q);
+                return hipGetLastError();
+            }
+            {
+                Params q = p;
+                q.units = (p.nblocks + 63) / 64;
+                const int64_t g = q.units < cfg.max_blocks ? q.units : cfg.max_blocks;
+                hipLaunchKernelGGL(smooth_chunk_kernel, dim3((unsigned)g), dim3(64), 0, st, q);
+                return hipGetLastError();
+            }
         case Kind::Hadamard: return launch_op<HadamardOp>(p, map, st, cfg);
         case Kind::KronMfma:
             switch (a) {

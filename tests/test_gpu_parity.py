@@ -127,8 +127,7 @@ def test_kroquant_parity(ab, per_block, M, d):
     assert_exact(gpu_quantize(X, A, B, exact=True), want, f"exact {ab} pb={per_block} {M}x{d}")
     hot = gpu_quantize(X, A, B, exact=False)
     assert_mx_close(hot, want, f"mfma {ab} pb={per_block} {M}x{d}")
-    # the packed-K variant multiplies the same split terms: identical outputs
-    assert_exact(gpu_quantize_packed(X, A, B), hot, f"packed {ab} pb={per_block} {M}x{d}")
+    assert_mx_close(gpu_quantize_packed(X, A, B), want, f"packed {ab} pb={per_block} {M}x{d}")
 
 
 @pytest.mark.parametrize("M,d", [(1, 32), (3, 64), (257, 1152), (64, 2240), (130, 5600)])
@@ -209,6 +208,31 @@ def test_edge_blocks_kron(ab):
     for exact in (True, False):
         c, s, _ = gpu_quantize(X[keep], Ai, Bi, exact=exact)
         assert np.array_equal(c, cr) and np.array_equal(s, sr), exact
+
+
+@pytest.mark.parametrize("ab", AB_SPLITS)
+def test_zero_blocks_signed_zeros(ab):
+    """All-zero input blocks: the matrix-core paths skip the re-evaluation only
+    when the fixed order provably gives +0 everywhere (inputs +0, no factor row
+    with every sign bit set); otherwise the signed zeros of the fixed order
+    decide the codes.  Codes and scales must equal the oracle exactly here."""
+    a, b = ab
+    M, d = 70, 2240
+    X = synth.activations(M, d, "normal", seed=21)
+    X[::3] = 0                       # +0 rows
+    X[1::7, 64:160] = 0x8000         # -0 runs
+    A, B = synth.factors(a, b, d // 32, seed=22)
+    A[3, 0, :] = -np.abs(A[3, 0, :]) - 0.01   # a row of A with every sign bit set (block 3)
+    B[5, -1, :] = -np.abs(B[5, -1, :]) - 0.01  # and one of B (block 5)
+    for nfac_mode in ("shared", "per_block"):
+        Af, Bf = (A[3:4], B[3:4]) if nfac_mode == "shared" else (A, B)
+        want = oracle.quantize(X, Af, Bf, want_y=True)
+        for got in (gpu_quantize(X, Af, Bf, exact=False), gpu_quantize_packed(X, Af, Bf)):
+            assert np.array_equal(got[1], want[1]), f"{ab} {nfac_mode}: scales"
+            zero_rows = np.zeros(M, bool)
+            zero_rows[::3] = True
+            assert np.array_equal(got[0][zero_rows], want[0][zero_rows]), f"{ab} {nfac_mode}: zero-row codes"
+            assert_mx_close(got, want, f"{ab} {nfac_mode}")
 
 
 # ------------------------------------------------------------------ layout, guards, determinism
@@ -310,7 +334,7 @@ def test_full_size_workloads(name):
     assert_mx_close(hot, (cr, sr, yr), name + " mfma")
     kp = kq.pack_factors(dev_f32(w.A), dev_f32(w.B))
     c, s, y = kq.quantize_packed(Xd, dev_f32(w.A), dev_f32(w.B), kp, want_y=True)
-    assert_exact((host(c), host(s), host(y)), hot, name + " packed")
+    assert_mx_close((host(c), host(s), host(y)), (cr, sr, yr), name + " packed")
     c, s, _ = kq.smoothquant(Xd, dev_f32(w.mult))
     cr, sr, _ = oracle.smoothquant(w.X, w.mult)
     assert_exact((host(c), host(s), None), (cr, sr, None), name + " smooth")
@@ -335,4 +359,4 @@ def test_large_per_block_sampled_rows(name):
     assert_mx_close((host(c)[rows], host(s)[rows], None), (cr, sr, None), name + " mfma")
     kp = kq.pack_factors(Ad, Bd)
     c2, s2, _ = kq.quantize_packed(Xd, Ad, Bd, kp)
-    assert np.array_equal(host(c2), host(c)) and np.array_equal(host(s2), host(s))
+    assert_mx_close((host(c2)[rows], host(s2)[rows], None), (cr, sr, None), name + " packed")
