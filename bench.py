@@ -64,13 +64,63 @@ def parse():
     ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--only", choices=["kroquant", "kroquant_onthefly", "kroquant_exact", "smoothquant", "hadamard32", "mxfp4", "copy"],
                     help="run only this kernel for --steps launches (for profiler runs); prints no JSON")
+    ap.add_argument("--summarize-pmc", metavar="DIR",
+                    help="turn the FETCH_SIZE / WRITE_SIZE counter runs under DIR (DIR/<kernel>/p3, p4 from "
+                         "rocprofv3 --pmc, kernels 'kroquant' and 'copy') into the traffic record read by the "
+                         "roofline field; needs no GPU")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")
     return ap.parse_args()
 
 
+KERNEL_NAMES = {"kroquant": "kron_mfma_unit_kernel", "copy": "copyBuffer"}
+COPY_BYTES = 1 << 28  # the --only copy kernel moves 256 MiB in and 256 MiB out
+
+
+def _counter_median(root, kernel, counter):
+    import csv
+    import glob
+    import statistics
+    vals = []
+    for f in glob.glob(os.path.join(root, kernel, "p*", "*counter_collection.csv")):
+        with open(f) as fh:
+            for row in csv.DictReader(fh):
+                if row["Counter_Name"] == counter and KERNEL_NAMES[kernel] in row["Kernel_Name"]:
+                    vals.append(float(row["Counter_Value"]))
+    if not vals:
+        raise SystemExit(f"no {counter} samples for {kernel} under {root}")
+    return statistics.median(vals), len(vals)
+
+
+def summarize_pmc(root, workload):
+    """HBM traffic of one hot-path launch: FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch) of the kernel, each divided by what the same counter reads per
+    byte for a plain 256 MiB copy."""
+    k_fetch, n1 = _counter_median(root, "kroquant", "FETCH_SIZE")
+    k_write, n2 = _counter_median(root, "kroquant", "WRITE_SIZE")
+    c_fetch, _ = _counter_median(root, "copy", "FETCH_SIZE")
+    c_write, _ = _counter_median(root, "copy", "WRITE_SIZE")
+    f_read = c_fetch * 1024 / COPY_BYTES   # counter bytes per real byte read
+    f_write = c_write * 1024 / COPY_BYTES  # counter bytes per real byte written
+    read_b = k_fetch * 1024 / f_read
+    write_b = k_write * 1024 / f_write
+    from synth import WORKLOADS
+    _, M, d = WORKLOADS[workload][:3]
+    rec = {"workload": workload, "kernel": KERNEL_NAMES["kroquant"], "kernel_source_hash": kernel_source_hash(),
+           "fetch_kib_per_dispatch": k_fetch, "write_kib_per_dispatch": k_write, "dispatches": min(n1, n2),
+           "copy_fetch_factor": f_read, "copy_write_factor": f_write,
+           "hbm_read_bytes_per_launch": read_b, "hbm_write_bytes_per_launch": write_b,
+           "hbm_bytes_per_launch": read_b + write_b, "algorithmic_bytes": algorithmic_bytes(M, d)}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec, indent=1))
+
+
 def main():
     args = parse()
+    if args.summarize_pmc:
+        summarize_pmc(args.summarize_pmc, args.workload)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this quantizer benchmark runs on exactly one GPU (--gpus 1); the quantizer "
               "has no cross-GPU step and multi-GPU runs are not part of this build", file=sys.stderr)
@@ -128,7 +178,7 @@ def main():
     if args.only:
         if args.only == "copy":
             # plain copy of a known size (2 x 256 MiB read + write), for counter calibration
-            src = torch.empty(1 << 28, dtype=torch.uint8, device=dev).fill_(1)
+            src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev).fill_(1)
             dst = torch.empty_like(src)
             for _ in range(args.steps):
                 dst.copy_(src)

@@ -31,11 +31,11 @@ struct Params {
 
 struct LaunchConfig {
     int64_t max_blocks = int64_t(1) << 30;  // cap on the workgroup count (grid-stride beyond it)
-    int64_t max_waves = int64_t(1) << 30;   // cap on the matrix-core kernel's workgroups (one wave each)
-    int units_per_wave = 2;                 // 64-block units a matrix-core wave loads per step (1 or 2)
+    int64_t max_waves = 3072;               // workgroups (one wave each) of the on-the-fly matrix-core kernel
+    int units_per_wave = 1;                 // 64-block units it loads per step (1 or 2)
     bool packed_one_unit = true;            // packed K: one unit per wave, no loop
     int smooth_path = 3;                    // SmoothQuant layout: 0 chunk, 1 per-lane, 2 column, 3 stationary
-    int64_t smooth_waves = 3072;            // target workgroups of the column-stationary SmoothQuant
+    int64_t smooth_waves = 2048;            // target workgroups of the column-stationary SmoothQuant
 };
 
 hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg);
