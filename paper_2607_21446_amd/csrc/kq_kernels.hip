@@ -310,6 +310,16 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 
+// Codes of the 8 values a[o .. o+7] at scale sc as one dword (value o + 2i in
+// the low nibble of byte i).  `old` only seeds the register: every byte is
+// overwritten.
+__device__ __forceinline__ uint32_t codes8(const f32x16& a, int o, float sc, uint32_t old) {
+    uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a[o], a[o + 1], sc, 0);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, a[o + 2], a[o + 3], sc, 1);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, a[o + 4], a[o + 5], sc, 2);
+    return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, a[o + 6], a[o + 7], sc, 3);
+}
+
 // The value `v` of lane l ^ 32 (the other half of the wave).
 __device__ __forceinline__ uint32_t other_half(uint32_t v) {
     const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
@@ -325,14 +335,38 @@ __device__ __forceinline__ uint32_t max_with_other_half(uint32_t v) {
     return max((uint32_t)r[0], (uint32_t)r[1]);
 }
 
+// The value of lane l ^ 1 (a DPP quad permutation, no LDS round trip).
+__device__ __forceinline__ uint32_t lane_xor1(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
+}
+
+// Unsigned max over each 32-lane half of the wave (for values >= 0 this is the
+// max of their fp32 bit patterns): DPP steps within rows of 16 lanes (lane ^ 1,
+// lane ^ 2, mirror in 8, mirror in 16), then rows 2k and 2k + 1 swapped.
+__device__ __forceinline__ uint32_t half_wave_max(uint32_t v) {
+    v = max(v, lane_xor1(v));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false));
+    const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    return max((uint32_t)r[0], (uint32_t)r[1]);
+}
+
 // This lane's slice of K = A (x) B as the A operand of v_mfma_f32_32x32x16_bf16:
-// lane l holds K[n][k] for n = l % 32 and k = 16 s + 8 (l / 32) + c (c = 0..7)
-// in k-step s = 0, 1; K[n][k] = fp32(A[n / b][k / b] * B[n % b][k % b])
+// lane l holds K[perm_row(m)][k] for m = l % 32 and k = 16 s + 8 (l / 32) + c
+// (c = 0..7) in k-step s = 0, 1; K[n][k] = fp32(A[n / b][k / b] * B[n % b][k % b])
 // (numpy.kron index order), split as hi + mid + lo with each term the bf16
 // nearest to what the previous terms leave.
 struct KSlices {
     bf16x8 hi[2], mid[2], lo[2];
 };
+
+// Output row m of the 32x32 product is block element perm_row(m).  The
+// product's lane layout puts rows 8q + 4h + r (q, r = 0..3) in acc[4q + r] of
+// lane 32h + block, so with this order lane 32h + block holds elements
+// 16h .. 16h + 15 in acc[0..15]: its 8 code bytes are contiguous and need no
+// exchange with the other half of the wave.
+__device__ __forceinline__ constexpr int perm_row(int m) { return 16 * ((m >> 2) & 1) + 4 * (m >> 3) + (m & 3); }
 
 // The factor entries behind this lane's slice: kv(s, c) = fa[s][c] * fb[s][c].
 template <int NA, int NB>
@@ -342,7 +376,7 @@ struct KFactors {
 
 template <int NA, int NB>
 __device__ __forceinline__ void load_k_factors(const float* A, const float* B, int lane, KFactors<NA, NB>& kf) {
-    const int n = lane & 31, h = lane >> 5;
+    const int n = perm_row(lane & 31), h = lane >> 5;
     const int ia = n / NB, ib = n % NB;
 #pragma unroll
     for (int s = 0; s < 2; ++s)
@@ -560,11 +594,8 @@ __device__ __forceinline__ void exact_blocks_coop(const uint4* unit_lds, int blk
         for (int q = 1; q < NB; ++q) z = __builtin_fmaf(Bf[i * NB + q], x[pr * NB + q], z);
         acc = (pr == 0) ? Af[o * NA] * z : __builtin_fmaf(Af[o * NA + pr], z, acc);
     }
-    float am = fabsf(acc);
-#pragma unroll
-    for (int off = 16; off >= 1; off >>= 1) am = fmaxf(am, __shfl_xor(am, off));  // within the half-wave
-    const uint32_t sb = e8m0_byte(am);
-    const float next = __shfl_down(acc, 1);  // y[n + 1] (n even: same half-wave)
+    const uint32_t sb = e8m0_byte(__uint_as_float(half_wave_max(__float_as_uint(fabsf(acc)))));
+    const float next = __uint_as_float(lane_xor1(__float_as_uint(acc)));  // y[n + 1] for even n
     const uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, acc, next, __uint_as_float(sb << 23), 0);
     if (blk >= 0) {
         if (p.codes) {
@@ -733,7 +764,7 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
                 if (32 * t >= nvalid[k]) break;
                 const int bt = 32 * t + jl;  // this lane's block within the unit
                 const bool valid = bt < nvalid[k];
-                // lane holds y[8q + 4h + r] of block bt in acc[t][4q + r]; all values >= 0 below
+                // lane holds y[16h + i] of block bt in acc[t][i]; all values >= 0 below
                 // compare as their fp32 bit patterns
                 float am = 0.0f;
 #pragma unroll
@@ -754,36 +785,19 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
                     if ((any | other_half(any)) == 0u) near = false;
                 }
                 const uint64_t ob = (uint64_t)first[k] + (uint64_t)((uint32_t)bt * bstride);  // output block
-                const uint32_t sb = e > 2u ? e - 2u : 0u;
+                const uint32_t sb = max(e, 2u) - 2u;
                 const float sc = __uint_as_float(sb << 23);
-                uint32_t w[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, acc[t][4 * q], acc[t][4 * q + 1], sc, 0);
-                    w[q] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, acc[t][4 * q + 2], acc[t][4 * q + 3], sc, 1);
-                }
-                // code dword q of the block = [lower half: lane h=0's w[q]] [upper half: lane h=1's w[q]];
-                // lane h=0 stores dwords 0-1, lane h=1 dwords 2-3
-                const uint32_t send = h ? (w[0] | (w[1] << 16)) : (w[2] | (w[3] << 16));
-                const uint32_t recv = other_half(send);
-                uint2 out;
-                if (h == 0) {
-                    out.x = w[0] | (recv << 16);
-                    out.y = w[1] | (recv & 0xFFFF0000u);
-                } else {
-                    out.x = (recv & 0xFFFFu) | (w[2] << 16);
-                    out.y = (recv >> 16) | (w[3] << 16);
-                }
+                const uint2 out = make_uint2(codes8(acc[t], 0, sc, amb), codes8(acc[t], 8, sc, amb));
                 if (valid && !near) {
                     if (p.codes) {
                         *reinterpret_cast<uint2*>(p.codes + ob * 16 + 8 * h) = out;
                         if (h == 0) p.scales[ob] = (uint8_t)sb;
                     }
                     if (p.y) {
-                        float* yb = p.y + ob * 32 + 4 * h;
+                        float* yb = p.y + ob * 32 + 16 * h;
 #pragma unroll
                         for (int q = 0; q < 4; ++q)
-                            *reinterpret_cast<float4*>(yb + 8 * q) =
+                            *reinterpret_cast<float4*>(yb + 4 * q) =
                                 make_float4(acc[t][4 * q], acc[t][4 * q + 1], acc[t][4 * q + 2], acc[t][4 * q + 3]);
                     }
                 }
@@ -805,9 +819,12 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
 // (|e| <= 116 u sum_k |K_nk||x_k| <= 116 u ||K||_inf max|x|, u = 2^-24) and
 // max|x| <= ||K^-1||_inf max|Kx| <= ||K^-1||_inf (amax + |e|), the two amax
 // differ by at most 116 u cond (1 - 104 u cond)^-1 amax <= 2^-16 cond amax =
-// rho amax whenever cond = cond_inf(K) <= 2^16 (rho is +inf above).  A block
-// whose amax lies within rho amax of a power of two is re-evaluated in the
-// fixed order, so its E8M0 scale equals the fixed-order one.
+// rho amax whenever cond = cond_inf(K) <= 2^16.  amax = (1 + f) 2^E with
+// f = mantissa / 2^23, so amax - 2^E <= rho amax implies f <= 2 rho and
+// 2^(E+1) - amax <= rho amax implies 1 - f <= 2 rho: a block is re-evaluated in
+// the fixed order when its amax mantissa lies within T = ceil(2^24 rho) of 0 or
+// of 2^23 (T from the pack; T = 2^22 flags every block, used above cond 2^16),
+// or when amax < 2^-123, so its E8M0 scale equals the fixed-order one.
 template <Mapping MAP, int NA, int NB>
 __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
     __shared__ uint4 lds[256];
@@ -827,14 +844,17 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
         nvalid = (int)min<int64_t>(64, p.M - row0);
         bstride = (uint32_t)p.nb;
     }
+    // chunk 64c + lane of the unit (block (64c + lane) / 4, chunk (64c + lane) % 4
+    // of that block) goes to LDS slot 64c + wslot (lds_slot is additive in c here)
     const uint4* src = reinterpret_cast<const uint4*>(p.X) + first * 4;
+    const int wslot = lds_slot(lane >> 2, lane & 3);
     {
         uint4 v[4];
         if (nvalid == 64) {
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const uint32_t ci = 64 * c + lane;
-                v[c] = load_nt(src + ((ci >> 2) * bstride * 4 + (ci & 3)));
+                v[c] = load_nt(src + (MAP == Mapping::Flat ? ci : (ci >> 2) * bstride * 4 + (ci & 3)));
             }
         } else {
 #pragma unroll
@@ -845,28 +865,36 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
             }
         }
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const int ci = 64 * c + lane;
-            lds[lds_slot(ci >> 2, ci & 3)] = v[c];
-        }
+        for (int c = 0; c < 4; ++c) lds[wslot + 64 * c] = v[c];
     }
     const int64_t f = (p.nfac == 1) ? 0 : jcol;
-    const uint4* pk = reinterpret_cast<const uint4*>(p.kpack + f * kPackBytes);
+    // K slice i (i = 2 term + k-step) of this lane at byte 1024 i + 16 lane of the
+    // pack: one uniform base 2 KiB in, so every offset fits the load's immediate
+    const uint8_t* const pk0 = p.kpack + f * kPackBytes;
+    const uint8_t* const pkm = pk0 + 2048;
+    const uint32_t lo16 = 16u * (uint32_t)lane;
+    auto kslice = [&](int i) {
+        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(pkm + lo16 + (1024 * i - 2048)));
+    };
     KSlices ks;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-        ks.hi[s] = __builtin_bit_cast(bf16x8, pk[(0 * 2 + s) * 64 + lane]);
-        ks.mid[s] = __builtin_bit_cast(bf16x8, pk[(1 * 2 + s) * 64 + lane]);
-        ks.lo[s] = __builtin_bit_cast(bf16x8, pk[(2 * 2 + s) * 64 + lane]);
+        ks.hi[s] = kslice(0 * 2 + s);
+        ks.mid[s] = kslice(1 * 2 + s);
+        ks.lo[s] = kslice(2 * 2 + s);
     }
-    const float rho = ld_uniform(reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16), 1);
+    const float* hdr = reinterpret_cast<const float*>(pk0 + 6 * 64 * 16);
     // nonzero when no row of A and no row of B has every sign bit set: then an
     // all-(+0) input block gives +0 for every output in the fixed order
-    const bool zero_ok = __float_as_uint(ld_uniform(reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16), 2)) != 0u;
+    const bool zero_ok = __float_as_uint(ld_uniform(hdr, 2)) != 0u;
+    const uint32_t edge_t = __float_as_uint(ld_uniform(hdr, 3));
     // output bases of the unit (wave-uniform) and this lane's block offsets
     uint8_t* const codes_u = p.codes + first * 16;
     uint8_t* const scales_u = p.scales + first;
     float* const y_u = p.y + first * 32;
+    // lane (jl, h) reads chunks h and 2 + h of block 32 t + jl: slots 128 t + rslot
+    // and 128 t + (rslot ^ 2)
+    const int rslot = 4 * jl + (h ^ ((jl >> 2) & 3));
     wave_lds_sync();
     uint64_t edges = 0;  // blocks of the unit on a binade edge (bit = block index)
 #pragma unroll
@@ -875,8 +903,8 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
         const int bt = 32 * t + jl;
         const bool valid = bt < nvalid;
         uint4 raw[2];
-        raw[0] = lds[lds_slot(bt, h)];
-        raw[1] = lds[lds_slot(bt, 2 + h)];
+        raw[0] = lds[128 * t + rslot];
+        raw[1] = lds[128 * t + (rslot ^ 2)];
         f32x16 acc = {};
 #pragma unroll
         for (int s = 0; s < 2; ++s)
@@ -887,52 +915,31 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
 #pragma unroll
         for (int s = 0; s < 2; ++s)
             acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.hi[s], __builtin_bit_cast(bf16x8, raw[s]), acc, 0, 0, 0);
-        // lane holds y[8q + 4h + r] of block bt in acc[4q + r]
+        // lane holds y[16h + i] of block bt in acc[i]
         float am = 0.0f;
 #pragma unroll
         for (int i = 0; i < 16; ++i) am = fmaxf(am, fabsf(acc[i]));
         const uint32_t amb = max_with_other_half(__float_as_uint(am));
-        am = __uint_as_float(amb);
-        const uint32_t e = amb >> 23;
-        const float win = rho * am;
-        bool near = valid && (e <= 3u || am - __uint_as_float(e << 23) <= win ||
-                              __uint_as_float((e + 1u) << 23) - am <= win);
+        bool near = valid && (((amb + edge_t) & 0x7FFFFFu) <= 2u * edge_t || amb < (4u << 23));
         if (amb == 0u && zero_ok) {
             // all outputs +-0: exact when the inputs are all +0 (bit patterns 0)
             const uint32_t any = raw[0].x | raw[0].y | raw[0].z | raw[0].w | raw[1].x | raw[1].y | raw[1].z | raw[1].w;
             if ((any | other_half(any)) == 0u) near = false;
         }
-        const uint32_t sb = e > 2u ? e - 2u : 0u;
+        const uint32_t sb = max(amb >> 23, 2u) - 2u;
         const float sc = __uint_as_float(sb << 23);
-        uint32_t w[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, acc[4 * q], acc[4 * q + 1], sc, 0);
-            w[q] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, acc[4 * q + 2], acc[4 * q + 3], sc, 1);
-        }
-        // code dword q of the block = [lower half: lane h=0's w[q]] [upper half: lane h=1's w[q]];
-        // lane h=0 stores dwords 0-1, lane h=1 dwords 2-3
-        const uint32_t send = h ? (w[0] | (w[1] << 16)) : (w[2] | (w[3] << 16));
-        const uint32_t recv = other_half(send);
-        uint2 out;
-        if (h == 0) {
-            out.x = w[0] | (recv << 16);
-            out.y = w[1] | (recv & 0xFFFF0000u);
-        } else {
-            out.x = (recv & 0xFFFFu) | (w[2] << 16);
-            out.y = (recv >> 16) | (w[3] << 16);
-        }
+        const uint2 out = make_uint2(codes8(acc, 0, sc, amb), codes8(acc, 8, sc, amb));
         const uint32_t ob = (uint32_t)bt * bstride;  // this lane's block, relative to `first`
         if (valid && !near) {
             if (p.codes) {
-                *reinterpret_cast<uint2*>(codes_u + ob * 16u + 8u * h) = out;
+                *reinterpret_cast<uint2*>(codes_u + (ob * 16u + 8u * h)) = out;
                 if (h == 0) scales_u[ob] = (uint8_t)sb;
             }
             if (p.y) {
-                float* yb = y_u + ob * 32u + 4u * h;
+                float* yb = y_u + (ob * 32u + 16u * h);
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
-                    *reinterpret_cast<float4*>(yb + 8 * q) =
+                    *reinterpret_cast<float4*>(yb + 4 * q) =
                         make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
             }
         }
@@ -946,8 +953,8 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
 // of the matrix-core A operand (offline step; the K1 variant of Sec. 3.5
 // keeps the dense 32x32 blocks in HBM).  Layout per pair (kPackBytes):
 // uint4 [3 terms: hi, mid, lo][2 k-steps][64 lanes], then fp32 ||K||_inf,
-// the relative binade-edge window rho (see kron_mfma_unit_kernel) and the
-// all-(+0)-input flag.
+// the relative binade-edge window rho, the all-(+0)-input flag and the
+// mantissa window T derived from rho (see kron_mfma_unit_kernel).
 // true when no row of F has every entry's sign bit set
 __device__ bool no_negative_row(const float* F, int n) {
     for (int i = 0; i < n; ++i) {
@@ -1016,13 +1023,18 @@ __global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ A, c
         // relative binade-edge window rho = 2^-16 cond_inf(K), cond_inf(K) =
         // ||A||_inf ||B||_inf ||A^-1||_inf ||B^-1||_inf (Kronecker norms multiply)
         float rho = __builtin_inff();
+        uint32_t edge_t = 1u << 22;  // every block re-evaluated
         if (lane == 0) {
             double* work = reinterpret_cast<double*>(pack_lds);
             const double na = norm_inf_f64(A + f * (NA * NA), NA), nb_ = norm_inf_f64(B + f * (NB * NB), NB);
             const double nai = inverse_norm_inf_f64(A + f * (NA * NA), NA, work);
             const double nbi = inverse_norm_inf_f64(B + f * (NB * NB), NB, work);
             const double cond = 1.01 * na * nb_ * nai * nbi;
-            if (cond <= 65536.0) rho = (float)(cond * 0x1p-16);
+            if (cond <= 65536.0) {
+                rho = (float)(cond * 0x1p-16);
+                // T = ceil(2^24 rho) = ceil(2^8 cond), at most 2^22
+                edge_t = (uint32_t)fmin(ceil(cond * 256.0), 4194304.0);
+            }
         }
         rho = __shfl(rho, 0);
         uint32_t zero_ok = 0u;
@@ -1036,7 +1048,7 @@ __global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ A, c
         }
         if (lane == 0)
             *reinterpret_cast<uint4*>(kpack + f * kPackBytes + 6 * 64 * 16) =
-                make_uint4(__float_as_uint(kinf), __float_as_uint(rho), zero_ok, 0u);
+                make_uint4(__float_as_uint(kinf), __float_as_uint(rho), zero_ok, edge_t);
     }
 }
 
