@@ -109,7 +109,7 @@ kq_status kq_pack_factors(const float* A, const float* B, int a, int b, int64_t 
  * A and B are still required: blocks on a binade edge are re-evaluated in
  * the fixed order of kq_quantize_exact.  Same result contract as kq_quantize
  * (identical scales, codes within tie flips, y within the stated bound); the
- * edge window is 2^-16 cond_inf(A (x) B) amax here, taken from the pack,
+ * edge window is 2^-17 cond_inf(A (x) B) amax here, taken from the pack,
  * instead of a per-block bound, so the set of re-evaluated blocks can differ.
  */
 kq_status kq_quantize_packed(const uint16_t* X, int64_t M, int64_t d, const float* A,

@@ -16,13 +16,18 @@
 //    v_mfma_f32_32x32x16_bf16 (the bf16 input is the B operand as loaded),
 //    accumulating in fp32 -- the "single 32x32 tensor-core GEMM per block"
 //    of Sec. 3.5 done in enough precision for fp32 parity.  Its rounding
-//    differs from the exact order by at most 116 u sum_k |K_nk||x_k|
-//    (u = 2^-24), which can move a code only next to a rounding tie.  The
-//    E8M0 scale depends on amax only through its binade; whenever a block's
-//    amax lies within 2^-16 ||K||_inf max|x| of a power of two (256 u, over
-//    twice that bound) that block is recomputed on the exact path, so scales
-//    are always those of the exact order and each block's outputs depend on
-//    that block alone.
+//    differs from the exact order by at most 116 u S, S = sum_k |K_nk||x_k|
+//    (u = 2^-24), which can move a code only next to a rounding tie: the
+//    fixed order is within (a + b) u S <= 33 u S of the exact product, the
+//    rounded and split K within 2 u |K|, the bf16 products are exact, and the
+//    accumulation rounds at most 16 times per instruction with relative error
+//    <= 2 u each (nearest or truncating, any internal order), on partial sums
+//    below S for the two hi-term instructions and below 2^-7 S for the other
+//    four: <= 66 u S; 33 + 2 + 66 <= 116.  The E8M0 scale depends on amax only
+//    through its binade; whenever a block's amax lies within 2^-17 ||K||_inf
+//    max|x| of a power of two (128 u) that block is recomputed on the exact
+//    path, so scales are always those of the exact order and each block's
+//    outputs depend on that block alone.
 //
 // Two unit -> block mappings (a unit is the 64 blocks of one wave):
 //   FLAT    the blocks of the matrix are one flat array (rows are contiguous);
@@ -653,7 +658,7 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
             ks.mid[s] = __builtin_bit_cast(bf16x8, pk[(1 * 2 + s) * 64 + lane]);
             ks.lo[s] = __builtin_bit_cast(bf16x8, pk[(2 * 2 + s) * 64 + lane]);
         }
-        kbound = ld_uniform(reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16), 0) * 0x1p-16f;
+        kbound = ld_uniform(reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16), 0) * 0x1p-17f;
     } else {
         load_k_factors<NA, NB>(Af, Bf, lane, kf);  // first, so their latency overlaps the input loads
     }
@@ -693,7 +698,7 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
         }
     };
     if (s0 < nsteps) issue(s0);
-    if (!PACKED) kbound = build_k<NA, NB>(kf, ks) * 0x1p-16f;
+    if (!PACKED) kbound = build_k<NA, NB>(kf, ks) * 0x1p-17f;
     // no row of A and no row of B with every sign bit set: then an all-(+0)
     // input block gives +0 for every output in the fixed order
     bool zero_ok;
@@ -818,12 +823,12 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
 // Binade-edge test.  With e the error of this path and of the fixed order
 // (|e| <= 116 u sum_k |K_nk||x_k| <= 116 u ||K||_inf max|x|, u = 2^-24) and
 // max|x| <= ||K^-1||_inf max|Kx| <= ||K^-1||_inf (amax + |e|), the two amax
-// differ by at most 116 u cond (1 - 104 u cond)^-1 amax <= 2^-16 cond amax =
-// rho amax whenever cond = cond_inf(K) <= 2^16.  amax = (1 + f) 2^E with
+// differ by at most 116 u cond (1 - 104 u cond)^-1 amax <= 2^-17 cond amax =
+// rho amax whenever cond = cond_inf(K) <= 2^13.  amax = (1 + f) 2^E with
 // f = mantissa / 2^23, so amax - 2^E <= rho amax implies f <= 2 rho and
 // 2^(E+1) - amax <= rho amax implies 1 - f <= 2 rho: a block is re-evaluated in
 // the fixed order when its amax mantissa lies within T = ceil(2^24 rho) of 0 or
-// of 2^23 (T from the pack; T = 2^22 flags every block, used above cond 2^16),
+// of 2^23 (T from the pack; T = 2^22 flags every block, used above cond 2^13),
 // or when amax < 2^-123, so its E8M0 scale equals the fixed-order one.
 template <Mapping MAP, int NA, int NB>
 __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
@@ -1020,7 +1025,7 @@ __global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ A, c
         load_k_factors<NA, NB>(A + f * (NA * NA), B + f * (NB * NB), lane, kf);
         KSlices ks;
         const float kinf = build_k<NA, NB>(kf, ks);
-        // relative binade-edge window rho = 2^-16 cond_inf(K), cond_inf(K) =
+        // relative binade-edge window rho = 2^-17 cond_inf(K), cond_inf(K) =
         // ||A||_inf ||B||_inf ||A^-1||_inf ||B^-1||_inf (Kronecker norms multiply)
         float rho = __builtin_inff();
         uint32_t edge_t = 1u << 22;  // every block re-evaluated
@@ -1030,10 +1035,10 @@ __global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ A, c
             const double nai = inverse_norm_inf_f64(A + f * (NA * NA), NA, work);
             const double nbi = inverse_norm_inf_f64(B + f * (NB * NB), NB, work);
             const double cond = 1.01 * na * nb_ * nai * nbi;
-            if (cond <= 65536.0) {
-                rho = (float)(cond * 0x1p-16);
-                // T = ceil(2^24 rho) = ceil(2^8 cond), at most 2^22
-                edge_t = (uint32_t)fmin(ceil(cond * 256.0), 4194304.0);
+            if (cond <= 8192.0) {
+                rho = (float)(cond * 0x1p-17);
+                // T = ceil(2^24 rho) = ceil(2^7 cond) <= 2^20
+                edge_t = (uint32_t)ceil(cond * 128.0);
             }
         }
         rho = __shfl(rho, 0);

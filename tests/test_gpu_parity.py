@@ -235,6 +235,34 @@ def test_zero_blocks_signed_zeros(ab):
             assert_mx_close(got, want, f"{ab} {nfac_mode}")
 
 
+@pytest.mark.parametrize("ab", [(4, 8), (2, 16)])
+def test_binade_edge_stress(ab):
+    """Blocks whose fixed-order amax lies within a few binade-edge windows of a
+    power of two, gathered from 2M random blocks.  Both matrix-core paths
+    re-evaluate those inside their window and must get every other one right
+    from the matrix product alone: scales identical to the oracle's."""
+    a, b = ab
+    A, B = synth.factors(a, b, 1, seed=41)
+    pool = synth.activations(8192, 8192, "student_t3", seed=42)     # 2,097,152 blocks
+    _, sr, yr = oracle.quantize(pool, A, B, want_y=True)
+    amax = np.abs(yr.reshape(-1, 32)).max(-1).astype(np.float32)
+    mant = (amax.view(np.uint32) & 0x7FFFFF).astype(np.int64)
+    dist = np.minimum(mant, (1 << 23) - mant)                        # to the nearer power of two, in 2^-23 units
+    # the packed path's window is T = ceil(2^7 cond_inf) units; take up to 4 T
+    A64, B64 = A[0].astype(np.float64), B[0].astype(np.float64)
+    cinf = lambda F: np.abs(F).sum(1).max() * np.abs(np.linalg.inv(F)).sum(1).max()
+    T = int(np.ceil(128 * 1.01 * cinf(A64) * cinf(B64)))
+    pick = np.flatnonzero(dist <= 4 * T)
+    assert pick.size >= 512, pick.size
+    blocks = pool.reshape(-1, 32)[pick]
+    nb = 96
+    rows = int(np.ceil(blocks.shape[0] / nb))
+    X = np.concatenate([blocks, blocks[: rows * nb - blocks.shape[0]]]).reshape(rows, nb * 32)
+    want = oracle.quantize(X, A, B, want_y=True)
+    for name, got in (("onthefly", gpu_quantize(X, A, B, exact=False)), ("packed", gpu_quantize_packed(X, A, B))):
+        assert_mx_close(got, want, f"{ab} {name} near-edge blocks ({pick.size} picked, T={T})")
+
+
 # ------------------------------------------------------------------ layout, guards, determinism
 def test_guard_bands_and_full_coverage():
     M, d = 77, 2240
