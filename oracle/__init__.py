@@ -58,10 +58,13 @@ def _lib():
     lib.kqo_mxfp4.argtypes = [P, I64, I64, P, P]
     lib.kqo_e2m1_codes.argtypes = [P, I64, I, P]
     lib.kqo_e8m0_scales.argtypes = [P, I64, P]
+    lib.kqo_lu_factors.argtypes = [P, I, I64, P, P]
+    lib.kqo_f32_to_bf16.argtypes = [P, I64, P]
     lib.kqo_num_threads.argtypes = []
     lib.kqo_set_num_threads.argtypes = [I]
     for name in ("kqo_quantize", "kqo_quantize_f32", "kqo_smoothquant", "kqo_hadamard32",
-                 "kqo_mxfp4", "kqo_e2m1_codes", "kqo_e8m0_scales", "kqo_num_threads"):
+                 "kqo_mxfp4", "kqo_e2m1_codes", "kqo_e8m0_scales", "kqo_num_threads", "kqo_lu_factors",
+                 "kqo_f32_to_bf16"):
         getattr(lib, name).restype = ctypes.c_int
     lib.kqo_set_num_threads.restype = None
     return lib
@@ -126,6 +129,37 @@ def quantize_f32(X32, A, B, want_y=False):
     _check(_lib().kqo_quantize_f32(_ptr(X32), M, d, _ptr(A), _ptr(B), a, b, A.shape[0],
                                    _ptr(codes), _ptr(scales), _ptr(y)), "quantize_f32")
     return codes, scales, y
+
+
+def lu_factors_f32(lu, a):
+    """K2 factors decoded from the paper's LU parameters in the oracle's fixed
+    fp32 order (kq_oracle.c, kqo_lu_factors): lu [nfac, 5, 3] = (a_k, b_k, c_k)
+    of G_1..G_5 -> A [nfac, a, a], B [nfac, b, b] fp32 with A (x) B = K^T."""
+    lu = np.ascontiguousarray(lu, dtype=np.float32).reshape(-1, 5, 3)
+    nfac = lu.shape[0]
+    b = 32 // a
+    A = np.empty((nfac, a, a), dtype=np.float32)
+    B = np.empty((nfac, b, b), dtype=np.float32)
+    _check(_lib().kqo_lu_factors(_ptr(lu), a, nfac, _ptr(A), _ptr(B)), "lu_factors_f32")
+    return A, B
+
+
+def quantize_lu(X, lu, a, want_y=False):
+    """KroQuant quantizer with K2-form factors (Sec. 3.5): decode the LU
+    parameters (``lu_factors_f32``), then ``quantize``.  Returns (codes,
+    scales, y fp32 or None, y16 = bf16(y) or None)."""
+    A, B = lu_factors_f32(lu, a)
+    codes, scales, y = quantize(X, A, B, want_y=True)
+    y16 = f32_to_bf16(y)
+    return codes, scales, (y if want_y else None), (y16 if want_y else None)
+
+
+def f32_to_bf16(v):
+    """fp32 -> bf16 bit patterns, round to nearest, ties to even."""
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    out = np.empty(v.shape, dtype=np.uint16)
+    _check(_lib().kqo_f32_to_bf16(_ptr(v), v.size, _ptr(out)), "f32_to_bf16")
+    return out
 
 
 def smoothquant(X, mult, want_y=False):

@@ -252,6 +252,80 @@ int kqo_e8m0_scales(const float* amax, int64_t n, uint8_t* out) {
     return 0;
 }
 
+/* Factors of the on-the-fly variant K2 from the paper's LU parameters (Sec. 3.2
+ * "Parametrization", Sec. 3.5 "K2").  For each factor pair f, lu[f][k] =
+ * (a_k, b_k, c_k), k = 0..4, parametrize the 2x2 factor G_{k+1} = L U with
+ * L = [[1, 0], [c, 1]] and U = [[a, b], [0, -1/a]], so
+ *     G = [[a, b], [c a, c b - 1/a]]   (det G = -1).
+ * The paper's block K = G_1 (x) ... (x) G_5 multiplies row activations from the
+ * right (x^T K, eq. (1)), i.e. y = K^T x per block, and
+ * K^T = A (x) B with A = G_1^T (x) ... (x) G_na^T (a x a, na = log2 a) and
+ * B = G_{na+1}^T (x) ... (x) G_5^T (b x b): entrywise (Kronecker index order,
+ * most significant index bit with the first factor)
+ *     A[o][p] = prod_{k<na}  G_k[bit(p, na-1-k)][bit(o, na-1-k)]
+ *     B[i][q] = prod_{k>=na} G_k[bit(q, 4-k)][bit(i, 4-k)]
+ * (an empty product, A for a = 1, is 1).  fp32 order (the reading adopted for
+ * parity; the paper does not fix it): g10 = c*a, g11 = fmaf(c, b, -(1/a)) with
+ * 1/a correctly rounded, and each product left to right with one rounding per
+ * multiply.  a_k must be nonzero.  Output A [nfac, a, a], B [nfac, b, b]. */
+static float lu_entry(const float* g /* [5][2][2] */, int k0, int k1, int top, int row, int col) {
+    float v = 1.0f;
+    int first = 1;
+    for (int k = k0; k < k1; ++k) {
+        int sh = top - (k - k0);
+        float e = g[k * 4 + ((row >> sh) & 1) * 2 + ((col >> sh) & 1)];
+        v = first ? e : v * e;
+        first = 0;
+    }
+    return v;
+}
+
+int kqo_lu_factors(const float* lu, int a, int64_t nfac, float* A, float* B) {
+    int na = a == 1 ? 0 : a == 2 ? 1 : a == 4 ? 2 : a == 8 ? 3 : -1;
+    if (na < 0 || nfac < 1) return -3;
+    if (!lu || !A || !B) return -2;
+    int b = BLK / a;
+    for (int64_t f = 0; f < nfac; ++f) {
+        float g[5 * 4];
+        for (int k = 0; k < 5; ++k) {
+            float pa = lu[f * 15 + 3 * k], pb = lu[f * 15 + 3 * k + 1], pc = lu[f * 15 + 3 * k + 2];
+            if (pa == 0.0f) return -5;
+            float inv = 1.0f / pa;
+            g[k * 4 + 0] = pa;
+            g[k * 4 + 1] = pb;
+            g[k * 4 + 2] = pc * pa;
+            g[k * 4 + 3] = fmaf(pc, pb, -inv);
+        }
+        /* A^T of the first na factors: entry (o, p) reads G[bit of p][bit of o] */
+        for (int o = 0; o < a; ++o)
+            for (int p = 0; p < a; ++p) A[f * a * a + o * a + p] = lu_entry(g, 0, na, na - 1, p, o);
+        for (int i = 0; i < b; ++i)
+            for (int q = 0; q < b; ++q) B[f * b * b + i * b + q] = lu_entry(g, na, 5, 4 - na, q, i);
+    }
+    return 0;
+}
+
+/* fp32 -> bf16, round to nearest, ties to the even bf16 (the 16-bit output of
+ * the transformed activation): the two bf16 neighbours of v are its 16-bit
+ * truncation toward zero and the next one away from zero; the nearer one
+ * wins, a tie goes to the one whose last mantissa bit is 0.  Finite inputs. */
+int kqo_f32_to_bf16(const float* v, int64_t n, uint16_t* out) {
+    if (n < 0) return -1;
+    if (n > 0 && (!v || !out)) return -2;
+    for (int64_t i = 0; i < n; ++i) {
+        uint32_t u;
+        memcpy(&u, &v[i], 4);
+        uint32_t lo = u & 0xFFFF0000u, hi = lo + 0x10000u;
+        float flo, fhi;
+        memcpy(&flo, &lo, 4);
+        memcpy(&fhi, &hi, 4);
+        double dl = fabs((double)v[i] - (double)flo), dh = fabs((double)fhi - (double)v[i]);
+        uint32_t pick = (dl < dh) ? lo : (dh < dl) ? hi : (((lo >> 16) & 1u) ? hi : lo);
+        out[i] = (uint16_t)(pick >> 16);
+    }
+    return 0;
+}
+
 /* Number of OpenMP threads a parallel region would use (for reporting). */
 #ifdef _OPENMP
 #include <omp.h>

@@ -166,6 +166,80 @@ def test_kronecker_bit_formula_and_lu():
         assert np.allclose(KT, K.T, rtol=0, atol=1e-6 * np.abs(K).max())
 
 
+def _k_paper_f64(abc):
+    """K = G1 (x) ... (x) G5 written out from the K2 entry formula of Sec. 3.5,
+    G_k = [[a, b], [c a, c b - 1/a]] in fp64 (the L U product of Sec. 3.2)."""
+    G = [np.array([[a, b], [c * a, c * b - 1.0 / a]]) for a, b, c in np.asarray(abc, np.float64)]
+    K = np.ones((32, 32))
+    for r in range(32):
+        for c in range(32):
+            for k in range(5):
+                K[r, c] *= G[k][(r >> (4 - k)) & 1, (c >> (4 - k)) & 1]
+    return K, G
+
+
+@pytest.mark.parametrize("seed", [3, 4, 5])
+def test_lu_factors_f32_against_paper_formula(seed):
+    """kqo_lu_factors (fp32 decode of the K2 parameters) against the paper's
+    entry formula in fp64: A (x) B = K^T for every split, to within the
+    roundings of at most five fp32 products, for two factor pairs at once."""
+    rng = np.random.default_rng(seed)
+    lu = rng.normal(size=(2, 5, 3)).astype(np.float32)
+    lu[..., 0] = np.where(np.abs(lu[..., 0]) < 0.3, np.float32(0.7), lu[..., 0])
+    for f in range(2):
+        K, G = _k_paper_f64(lu[f])
+        scale = np.prod([np.abs(g).max() for g in G])
+        Ks = []
+        for a, b in AB_SPLITS:
+            A, B = oracle.lu_factors_f32(lu, a)
+            KT = np.kron(A[f].astype(np.float64), B[f].astype(np.float64))
+            assert np.abs(KT - K.T).max() <= 2e-6 * scale, (a, f)
+            Ks.append(KT)
+        # the split only moves fp32 roundings
+        for KT in Ks[1:]:
+            assert np.abs(KT - Ks[0]).max() <= 2e-6 * scale
+        # det K = prod_k det(G_k)^16 = (-1)^80 = 1
+        assert abs(np.linalg.det(Ks[0]) - 1.0) < 1e-3
+
+
+def test_lu_factors_f32_hadamard_init_and_exact_entries():
+    """LU(1/sqrt2, 1/sqrt2, 1) for all five factors is the Hadamard init
+    H32/sqrt(32) (Sec. 3.2); with a = 1 the A factor is the empty product 1;
+    with integer parameters every product is exact."""
+    from scipy.linalg import hadamard
+    h = np.float32(1 / np.sqrt(2))
+    lu = np.array([[[h, h, 1.0]] * 5], dtype=np.float32)
+    for a, b in AB_SPLITS:
+        A, B = oracle.lu_factors_f32(lu, a)
+        KT = np.kron(A[0].astype(np.float64), B[0].astype(np.float64))
+        assert np.abs(KT - hadamard(32) / np.sqrt(32)).max() < 1e-6
+    A, B = oracle.lu_factors_f32(lu, 1)
+    assert A.shape == (1, 1, 1) and A[0, 0, 0] == 1.0
+    lu = np.array([[[1.0, 2.0, 1.0], [-1.0, 1.0, 2.0], [2.0, 0.0, 1.0], [1.0, -1.0, -1.0], [-2.0, 1.0, 0.0]]],
+                  dtype=np.float32)   # 1/a exact, every entry a small integer or half-integer
+    K, _ = _k_paper_f64(lu[0])
+    for a, b in AB_SPLITS:
+        A, B = oracle.lu_factors_f32(lu, a)
+        assert np.array_equal(np.kron(A[0].astype(np.float64), B[0].astype(np.float64)), K.T), a
+
+
+def test_f32_to_bf16_round_to_nearest_even():
+    """The 16-bit output rounding against torch's fp32 -> bfloat16 conversion
+    (round to nearest, ties to even), on random values and on every kind of
+    exact tie."""
+    import torch
+    rng = np.random.default_rng(9)
+    v = np.concatenate([rng.normal(size=200000) * 10.0 ** rng.integers(-30, 30, 200000),
+                        rng.normal(size=1000)]).astype(np.float32)
+    ties = (rng.integers(0, 1 << 31, 4000, dtype=np.uint64).astype(np.uint32) & 0x7F7F0000) | 0x8000
+    ties[::2] |= 0x10000                       # odd and even bf16 neighbours below
+    sign = (rng.integers(0, 2, ties.size).astype(np.uint32) << 31)
+    v = np.concatenate([v, (ties | sign).view(np.float32), np.float32([0.0, -0.0, 1.0, -3.5])])
+    v = v[np.isfinite(v) & (np.abs(v) < 3e38)]
+    want = torch.from_numpy(v).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(oracle.f32_to_bf16(v), want)
+
+
 def test_sylvester_hadamard_split():
     from scipy.linalg import hadamard
     assert np.array_equal(np.kron(hadamard(4), hadamard(8)), hadamard(32))
