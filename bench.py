@@ -64,7 +64,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=2000)
     ap.add_argument("--workload", default=WORKLOAD)
-    ap.add_argument("--only", choices=["kroquant", "kroquant_onthefly", "kroquant_exact", "smoothquant", "hadamard32", "mxfp4", "copy"],
+    ap.add_argument("--only", choices=["kroquant", "kroquant_onthefly", "kroquant_lu", "kroquant_exact", "smoothquant",
+                                       "hadamard32", "mxfp4", "copy"],
                     help="run only this kernel for --steps launches (for profiler runs); prints no JSON")
     ap.add_argument("--summarize-pmc", metavar="DIR",
                     help="turn the FETCH_SIZE / WRITE_SIZE counter runs under DIR (DIR/<kernel>/p3, p4 from "
@@ -155,6 +156,7 @@ def main():
     sptr = stream.cuda_stream
 
     kpack = kq.pack_factors(A, B, stream=sptr)  # offline, once per layer
+    lu = torch.from_numpy(synth.lu_params(1, seed=7)).to(dev)  # K2-form factors (15 parameters)
 
     def run_kq(i):
         kq.quantize_packed(Xs[i], A, B, kpack, codes=Cs[i], scales=Ss[i], stream=sptr)
@@ -165,6 +167,9 @@ def main():
     def run_kx(i):
         kq.quantize_exact(Xs[i], A, B, codes=Cs[i], scales=Ss[i], stream=sptr)
 
+    def run_lu(i):
+        kq.quantize_lu(Xs[i], lu, 4, codes=Cs[i], scales=Ss[i], stream=sptr)
+
     def run_sq(i):
         kq.smoothquant(Xs[i], mult, codes=Cs[i], scales=Ss[i], stream=sptr)
 
@@ -174,7 +179,8 @@ def main():
     def run_q4(i):
         kq.mxfp4(Xs[i], codes=Cs[i], scales=Ss[i], stream=sptr)
 
-    runs = {"kroquant": run_kq, "kroquant_onthefly": run_k2, "kroquant_exact": run_kx, "smoothquant": run_sq,
+    runs = {"kroquant": run_kq, "kroquant_onthefly": run_k2, "kroquant_lu": run_lu, "kroquant_exact": run_kx,
+            "smoothquant": run_sq,
             "hadamard32": run_h32, "mxfp4": run_q4}
 
     if args.only:
@@ -224,7 +230,7 @@ def main():
     gbs = nbytes / (ms_kq * 1e-3) / 1e9
 
     comparators = {}
-    for name in ("kroquant_onthefly", "kroquant_exact", "smoothquant", "hadamard32", "mxfp4"):
+    for name in ("kroquant_onthefly", "kroquant_lu", "kroquant_exact", "smoothquant", "hadamard32", "mxfp4"):
         ms, _ = timed(runs[name], args.steps, args.warmup)
         comparators[name + "_us"] = round(ms * 1e3, 3)
         comparators[name + "_gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)

@@ -117,6 +117,32 @@ kq_status kq_quantize_packed(const uint16_t* X, int64_t M, int64_t d, const floa
                              uint8_t* codes, uint8_t* scales, float* y_out, void* stream);
 
 /*
+ * kq_quantize_lu -- kq_quantize with the factors given in the paper's K2 form
+ * (Sec. 3.5 "K2", parametrization of Sec. 3.2): 15 scalars per factor pair,
+ * lu[f][k] = (a_k, b_k, c_k), k = 0..4, for G_{k+1} = L U with
+ * L = [[1, 0], [c, 1]], U = [[a, b], [0, -1/a]].  The block applied is the
+ * paper's K = G_1 (x) ... (x) G_5 acting on row activations from the right
+ * (x^T K, eq. (1)), i.e. y = K^T x = (A (x) B) x with
+ * A = G_1^T (x) ... (x) G_log2(a)^T and B = G_{log2(a)+1}^T (x) ... (x) G_5^T.
+ * Every wave decodes its A and B from the 15 parameters on chip, in a fixed
+ * fp32 order:
+ *     g10 = c*a, g11 = fma(c, b, -(1/a)), and each entry of A and B is the
+ *     product of its G entries, left to right.
+ * The result then has the same contract as kq_quantize with those A and B.
+ *   lu       device fp32 [nfac, 5, 3], 4-byte aligned; every a_k nonzero.
+ *   a        1, 2, 4 or 8: how many G factors form A (log2 a); b = 32 / a.
+ *   nfac     1 (shared) or d / 32 (one parameter set per column block).
+ *   y16_out  optional device bf16 [M, d], 16-byte aligned.  It receives the
+ *            transformed values the codes were computed from, rounded to
+ *            bf16 (nearest even): the 16-bit activation of the low-rank
+ *            branch (Sec. 3.4, LoRaQ).
+ * Errors as kq_quantize; a not in {1, 2, 4, 8} -> KQ_ERROR_UNSUPPORTED.
+ */
+kq_status kq_quantize_lu(const uint16_t* X, int64_t M, int64_t d, const float* lu, int a, int64_t nfac,
+                         uint8_t* codes, uint8_t* scales, float* y_out, uint16_t* y16_out, void* stream);
+
+/*
+ * kq_quantize_exact -- kq_quantize with the transform evaluated on the vector/*
  * kq_quantize_exact -- kq_quantize with the transform evaluated on the vector
  * ALUs in one fixed fp32 order, so that every output is a deterministic
  * function of that order:

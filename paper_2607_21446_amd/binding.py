@@ -20,7 +20,8 @@ STATUS = {
 }
 
 EXPORTED = (
-    "kq_quantize", "kq_quantize_exact", "kq_quantize_packed", "kq_pack_factors", "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_mxfp4_quantize",
+    "kq_quantize", "kq_quantize_exact", "kq_quantize_packed", "kq_pack_factors", "kq_quantize_lu",
+    "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_mxfp4_quantize",
     "kq_e2m1_encode", "kq_weight_transform", "kq_factors_inverse_transpose", "kq_lu_to_factors",
     "kq_status_string", "kq_last_error_detail", "kq_version",
 )
@@ -46,6 +47,7 @@ def lib() -> ctypes.CDLL:
     L.kq_quantize_exact.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P]
     L.kq_quantize_packed.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P, P]
     L.kq_pack_factors.argtypes = [P, P, I, I, I64, P, P]
+    L.kq_quantize_lu.argtypes = [P, I64, I64, P, I, I64, P, P, P, P, P]
     L.kq_smoothquant_quantize.argtypes = [P, I64, I64, P, P, P, P, P]
     L.kq_hadamard32_quantize.argtypes = [P, I64, I64, P, P, P, P]
     L.kq_mxfp4_quantize.argtypes = [P, I64, I64, P, P, P]
@@ -53,7 +55,7 @@ def lib() -> ctypes.CDLL:
     L.kq_weight_transform.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P]
     L.kq_factors_inverse_transpose.argtypes = [P, P, I, I, I64, P, P]
     L.kq_lu_to_factors.argtypes = [P, I, I64, P, P]
-    for name in EXPORTED[:11]:
+    for name in EXPORTED[:12]:
         getattr(L, name).restype = ctypes.c_int
     L.kq_status_string.argtypes = [I]
     L.kq_status_string.restype = ctypes.c_char_p
@@ -166,6 +168,27 @@ def quantize_packed(X, A, B, kpack, codes=None, scales=None, y=None, want_y=Fals
     _check(lib().kq_quantize_packed(_ptr(X), M, d, _ptr(A), _ptr(B), a, b, nfac, _ptr(kpack), _ptr(codes),
                                     _ptr(scales), _ptr(y), _stream(stream)), "kq_quantize_packed")
     return codes, scales, y
+
+
+def quantize_lu(X, lu, a=4, codes=None, scales=None, y=None, y16=None, want_y=False, want_y16=False,
+                stream=None):
+    """kq_quantize_lu: K2-form factors, lu fp32 [nfac, 5, 3] = (a_k, b_k, c_k)
+    of G_1..G_5, decoded on chip; a = number of rows of A (1, 2, 4 or 8).
+    Returns (codes, scales, y or None, y16 or None); y16 is bf16 [M, d]."""
+    _need(X, torch.bfloat16, "X")
+    _need(lu, torch.float32, "lu")
+    if lu.numel() % 15:
+        raise ValueError("lu must hold 15 parameters per factor pair")
+    nfac = lu.numel() // 15
+    codes, scales, y = _outputs(X, codes, scales, y, want_y)
+    M, d = X.shape
+    if y16 is None and want_y16:
+        y16 = torch.empty((M, d), dtype=torch.bfloat16, device=X.device)
+    if y16 is not None:
+        _need(y16, torch.bfloat16, "y16")
+    _check(lib().kq_quantize_lu(_ptr(X), M, d, _ptr(lu), a, nfac, _ptr(codes), _ptr(scales), _ptr(y), _ptr(y16),
+                                _stream(stream)), "kq_quantize_lu")
+    return codes, scales, y, y16
 
 
 def smoothquant(X, mult, codes=None, scales=None, y=None, want_y=False, stream=None):

@@ -214,6 +214,25 @@ kq_status kq_quantize_packed(const uint16_t* X, int64_t M, int64_t d, const floa
                          scales, y_out, stream);
 }
 
+kq_status kq_quantize_lu(const uint16_t* X, int64_t M, int64_t d, const float* lu, int a, int64_t nfac,
+                         uint8_t* codes, uint8_t* scales, float* y_out, uint16_t* y16_out, void* stream) {
+    kq_status st = check_common(X, M, d, codes, scales, y_out, true);
+    if (st != KQ_SUCCESS) return st;
+    if (a != 1 && a != 2 && a != 4 && a != 8)
+        return fail(KQ_ERROR_UNSUPPORTED, "a = %d must be 1, 2, 4 or 8 (the number of G factors in A is log2 a)", a);
+    if ((st = check_factors(a, 32 / a, nfac, d)) != KQ_SUCCESS) return st;
+    if (!lu) return fail(KQ_ERROR_NULL_POINTER, "lu must not be NULL");
+    if (!aligned(lu, 4)) return fail(KQ_ERROR_MISALIGNED, "lu must be 4-byte aligned");
+    if (y16_out && !aligned(y16_out, 16)) return fail(KQ_ERROR_MISALIGNED, "y16_out must be 16-byte aligned");
+    if (M == 0) return ok();
+    kq::Params p = make_params(X, M, d, codes, scales, y_out);
+    p.nfac = nfac;
+    p.lu = lu;
+    p.y16 = y16_out;
+    const kq::Mapping map = (nfac == 1) ? kq::Mapping::Flat : kq::Mapping::Column;
+    return from_hip(kq::launch(kq::Kind::KronLU, a, p, map, (hipStream_t)stream, default_config()), "kq_quantize_lu");
+}
+
 kq_status kq_pack_factors(const float* A, const float* B, int a, int b, int64_t nfac, void* kpack, void* stream) {
     if (!supported_split(a, b))
         return fail(KQ_ERROR_UNSUPPORTED, "(a, b) = (%d, %d) is not one of (4,8), (2,16), (8,4), (1,32)", a, b);

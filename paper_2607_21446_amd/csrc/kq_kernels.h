@@ -8,7 +8,7 @@ namespace kq {
 constexpr int kThreads = 256;  // workgroup size of the element-encode kernel
 constexpr int64_t kPackBytes = 6 * 64 * 16 + 16;  // packed K per factor pair
 
-enum class Kind { Plain, Smooth, Hadamard, Kron, KronMfma };
+enum class Kind { Plain, Smooth, Hadamard, Kron, KronMfma, KronLU };
 enum class Mapping { Flat, Column };
 
 // Everything a launch needs; sizes already validated by the caller.
@@ -26,6 +26,8 @@ struct Params {
     uint8_t* scales;     // [M, nb]
     float* y;            // [M, d] or null
     const uint8_t* kpack;  // [nfac, kPackBytes] materialised K terms, or null
+    const float* lu;       // [nfac, 5, 3] LU parameters of G_1..G_5 (KronLU), or null
+    uint16_t* y16;         // [M, d] bf16 of the transformed values, or null (KronLU)
     int64_t units;       // wave units, filled in by the launcher
 };
 

@@ -325,6 +325,13 @@ __device__ __forceinline__ uint32_t codes8(const f32x16& a, int o, float sc, uin
     return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, a[o + 6], a[o + 7], sc, 3);
 }
 
+// Two fp32 values as a bf16 pair (round to nearest even), the first in the low half.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t bf16_pair(float a, float b) {
+    const bf16x2 v = {(__bf16)a, (__bf16)b};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
 // The value `v` of lane l ^ 32 (the other half of the wave).
 __device__ __forceinline__ uint32_t other_half(uint32_t v) {
     const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
@@ -608,6 +615,7 @@ __device__ __forceinline__ void exact_blocks_coop(const uint4* unit_lds, int blk
             if (n == 0) p.scales[out_blk] = (uint8_t)sb;
         }
         if (p.y) p.y[out_blk * 32 + n] = acc;
+        if (p.y16) p.y16[out_blk * 32 + n] = (uint16_t)(bf16_pair(acc, 0.0f) & 0xFFFFu);
     }
 }
 
@@ -628,13 +636,52 @@ __device__ __forceinline__ void exact_flagged(uint64_t edges, const uint4* unit_
     }
 }
 
+// K2-form factors from the LU parameters of G_1..G_5 (Sec. 3.2, Sec. 3.5):
+// G = [[a, b], [c a, c b - 1/a]] and, with na = log2(NA),
+//   A[o][p] = prod_{k < na}  G_k[bit(p, na-1-k)][bit(o, na-1-k)],
+//   B[i][q] = prod_{k >= na} G_k[bit(q, 4-k)][bit(i, 4-k)],
+// so A (x) B = (G_1 (x) ... (x) G_5)^T; every product left to right, one fp32
+// rounding per multiply, g11 = fma(c, b, -(1/a)).  The wave writes A then B
+// (NA*NA + NB*NB floats) to `out`; the parameters come in as scalar loads.
+template <int NA, int NB>
+__device__ __forceinline__ void decode_lu_factors(const float* lu, int lane, float* out) {
+    constexpr int na = NA == 1 ? 0 : NA == 2 ? 1 : NA == 4 ? 2 : 3;
+    float g[5][4];
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+        const float pa = ld_uniform(lu, 3 * k), pb = ld_uniform(lu, 3 * k + 1), pc = ld_uniform(lu, 3 * k + 2);
+        g[k][0] = pa;
+        g[k][1] = pb;
+        g[k][2] = pc * pa;
+        g[k][3] = __builtin_fmaf(pc, pb, -(1.0f / pa));
+    }
+    for (int idx = lane; idx < NA * NA + NB * NB; idx += 64) {
+        const bool in_a = idx < NA * NA;
+        const int rowi = in_a ? idx / NA : (idx - NA * NA) / NB;  // o or i
+        const int coli = in_a ? idx % NA : (idx - NA * NA) % NB;  // p or q
+        float v = 1.0f;
+        bool first = true;
+#pragma unroll
+        for (int k = 0; k < 5; ++k) {
+            if ((k < na) != in_a) continue;
+            const int sh = in_a ? na - 1 - k : 4 - k;
+            const int e = 2 * ((coli >> sh) & 1) + ((rowi >> sh) & 1);  // G_k[bit of col][bit of row]
+            const float ge = e == 0 ? g[k][0] : e == 1 ? g[k][1] : e == 2 ? g[k][2] : g[k][3];
+            v = first ? ge : v * ge;
+            first = false;
+        }
+        out[idx] = v;
+    }
+}
+
 // Matrix-core KroQuant.  A wave handles U consecutive units per step (all
 // their loads issued before any compute).  FLAT: workgroup g handles steps
 // g, g + G, ...;  COLUMN: workgroup g handles column block j = g % nb for
 // steps g / nb, g / nb + G / nb, ... (G a multiple of nb), so one K per wave.
-template <Mapping MAP, int NA, int NB, int U, bool PACKED>
+template <Mapping MAP, int NA, int NB, int U, bool PACKED, bool LU>
 __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
     __shared__ uint4 lds[U][256];
+    __shared__ float lu_fac[LU ? NA * NA + NB * NB : 1];  // decoded A then B (LU form)
     const int lane = threadIdx.x;
     const int h = lane >> 5, jl = lane & 31;
     int64_t jcol = 0, s0 = blockIdx.x, sstep = gridDim.x;
@@ -644,8 +691,12 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
         sstep = gridDim.x / p.nb;
     }
     const int64_t f = (p.nfac == 1) ? 0 : jcol;
-    const float* Af = p.A + f * (NA * NA);
-    const float* Bf = p.B + f * (NB * NB);
+    const float* Af = LU ? lu_fac : p.A + f * (NA * NA);
+    const float* Bf = LU ? lu_fac + NA * NA : p.B + f * (NB * NB);
+    if (LU) {
+        decode_lu_factors<NA, NB>(p.lu + f * 15, lane, lu_fac);
+        wave_lds_sync();
+    }
     // K operand: from the pack (materialised offline) or built here from the factors
     KFactors<NA, NB> kf;
     KSlices ks;
@@ -804,6 +855,15 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
                         for (int q = 0; q < 4; ++q)
                             *reinterpret_cast<float4*>(yb + 4 * q) =
                                 make_float4(acc[t][4 * q], acc[t][4 * q + 1], acc[t][4 * q + 2], acc[t][4 * q + 3]);
+                    }
+                    if (LU && p.y16) {
+                        uint4* yb = reinterpret_cast<uint4*>(p.y16 + ob * 32 + 16 * h);
+#pragma unroll
+                        for (int q = 0; q < 2; ++q)
+                            yb[q] = make_uint4(bf16_pair(acc[t][8 * q], acc[t][8 * q + 1]),
+                                               bf16_pair(acc[t][8 * q + 2], acc[t][8 * q + 3]),
+                                               bf16_pair(acc[t][8 * q + 4], acc[t][8 * q + 5]),
+                                               bf16_pair(acc[t][8 * q + 6], acc[t][8 * q + 7]));
                     }
                 }
                 // blocks whose amax is on a binade edge: the fixed evaluation order decides
@@ -1087,21 +1147,21 @@ static hipError_t launch_op(const Params& p, Mapping map, hipStream_t st, const 
     return launch_map<Mapping::Column, Op>(p, st, cfg);
 }
 
-template <int NA, int NB, int U, bool PACKED>
+template <int NA, int NB, int U, bool PACKED, bool LU = false>
 static hipError_t launch_mfma_u(Params p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
     int64_t g;
     if (map == Mapping::Flat) {
         const int64_t steps = ((p.nblocks + 63) / 64 + U - 1) / U;
         g = steps < cfg.max_waves ? steps : cfg.max_waves;
         if (g < 1) g = 1;
-        hipLaunchKernelGGL((kron_mfma_kernel<Mapping::Flat, NA, NB, U, PACKED>), dim3((unsigned)g), dim3(64), 0, st, p);
+        hipLaunchKernelGGL((kron_mfma_kernel<Mapping::Flat, NA, NB, U, PACKED, LU>), dim3((unsigned)g), dim3(64), 0, st, p);
     } else {
         const int64_t steps = ((p.M + 63) / 64 + U - 1) / U;  // per column block
         int64_t per_col = (cfg.max_waves + p.nb - 1) / p.nb;   // workgroups per column block
         if (per_col > steps) per_col = steps;
         if (per_col < 1) per_col = 1;
         g = per_col * p.nb;
-        hipLaunchKernelGGL((kron_mfma_kernel<Mapping::Column, NA, NB, U, PACKED>), dim3((unsigned)g), dim3(64), 0, st, p);
+        hipLaunchKernelGGL((kron_mfma_kernel<Mapping::Column, NA, NB, U, PACKED, LU>), dim3((unsigned)g), dim3(64), 0, st, p);
     }
     return hipGetLastError();
 }
@@ -1123,6 +1183,12 @@ static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st, cons
     }
     if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, false>(p, map, st, cfg);
     return launch_mfma_u<NA, NB, 1, false>(p, map, st, cfg);
+}
+
+template <int NA, int NB>
+static hipError_t launch_lu(const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
+    if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, false, true>(p, map, st, cfg);
+    return launch_mfma_u<NA, NB, 1, false, true>(p, map, st, cfg);
 }
 
 hipError_t launch_pack(int a, const float* A, const float* B, int64_t nfac, uint8_t* kpack, hipStream_t st) {
@@ -1168,6 +1234,14 @@ hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st
                 case 2: return launch_mfma<2, 16>(p, map, st, cfg);
                 case 8: return launch_mfma<8, 4>(p, map, st, cfg);
                 case 1: return launch_mfma<1, 32>(p, map, st, cfg);
+                default: return hipErrorInvalidValue;
+            }
+        case Kind::KronLU:
+            switch (a) {
+                case 4: return launch_lu<4, 8>(p, map, st, cfg);
+                case 2: return launch_lu<2, 16>(p, map, st, cfg);
+                case 8: return launch_lu<8, 4>(p, map, st, cfg);
+                case 1: return launch_lu<1, 32>(p, map, st, cfg);
                 default: return hipErrorInvalidValue;
             }
         case Kind::Kron:

@@ -109,6 +109,18 @@ def factors(a, b, nfac=1, seed=0, rng=None):
     return A, B
 
 
+def lu_params(nfac=1, seed=0):
+    """Random LU parameters (a_k, b_k, c_k) of five 2x2 factors per factor pair,
+    [nfac, 5, 3] fp32: a_k = 1 + 0.15 N, b_k = 0.3 + 0.15 N, c_k = 0.15 N (a
+    perturbed start in the spirit of a calibrated transform; every a_k stays
+    well away from 0)."""
+    rng = np.random.default_rng(seed)
+    lu = (rng.normal(size=(nfac, 5, 3)) * 0.15).astype(np.float32)
+    lu[..., 0] += np.float32(1.0)
+    lu[..., 1] += np.float32(0.3)
+    return lu
+
+
 def smoothquant_multipliers(X_bits: np.ndarray) -> np.ndarray:
     """Per-channel multipliers m_c = 1 / s_c with s_c = max_r |X[r, c]|^0.5
     (migration strength alpha = 0.5, beta = 0), computed in fp64 and rounded

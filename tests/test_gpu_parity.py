@@ -263,6 +263,43 @@ def test_binade_edge_stress(ab):
         assert_mx_close(got, want, f"{ab} {name} near-edge blocks ({pick.size} picked, T={T})")
 
 
+def gpu_quantize_lu(X, lu, a):
+    c, s, y, y16 = kq.quantize_lu(dev_bf16(X), dev_f32(lu), a, want_y=True, want_y16=True)
+    return host(c), host(s), host(y), host(y16.view(torch.int16)).view(np.uint16)
+
+
+@pytest.mark.parametrize("a", [4, 2, 8, 1])
+@pytest.mark.parametrize("per_block", [False, True])
+@pytest.mark.parametrize("M,d", [(77, 2240), (256, 1152)])
+def test_kroquant_lu_parity(a, per_block, M, d):
+    """K2-form factors decoded on chip (kq_quantize_lu) against the oracle's
+    fp32 decode + fixed-order quantizer; the bf16 output is the rounding of
+    the fp32 values the codes came from."""
+    X = synth.activations(M, d, "student_t3", seed=61, chan_frac=0.02, chan_factor=20.0)
+    X[3] = 0                                  # an all-zero row
+    lu = synth.lu_params(d // 32 if per_block else 1, seed=62 + a)
+    cr, sr, yr, y16r = oracle.quantize_lu(X, lu, a, want_y=True)
+    c, s, y, y16 = gpu_quantize_lu(X, lu, a)
+    assert_mx_close((c, s, y), (cr, sr, yr), f"lu a={a} per_block={per_block}")
+    assert np.array_equal(y16, oracle.f32_to_bf16(y)), "y16 is not bf16(y)"
+    assert (y16 != y16r).mean() <= 1e-3
+
+
+def test_kroquant_lu_hadamard_init():
+    """LU(1/sqrt2, 1/sqrt2, 1) for every factor is the Hadamard init: the
+    codes and scales match the Hadamard-32 comparator up to tie flips."""
+    X = synth.activations(128, 3072, "normal", seed=63)
+    h = np.float32(1 / np.sqrt(2))
+    lu = np.array([[[h, h, 1.0]] * 5], dtype=np.float32)
+    want = oracle.hadamard32(X, want_y=True)
+    for a in (4, 1):
+        c, s, y, _ = gpu_quantize_lu(X, lu, a)
+        ug, ur = oracle.unpack_codes(c), oracle.unpack_codes(want[0])
+        assert np.array_equal(s, want[1])
+        assert (ug != ur).mean() <= 1e-4
+        assert np.max(np.abs(y - want[2])) <= 1e-5 * np.abs(want[2]).max()
+
+
 # ------------------------------------------------------------------ layout, guards, determinism
 def test_guard_bands_and_full_coverage():
     M, d = 77, 2240

@@ -87,6 +87,21 @@ def test_pack_and_packed_reject():
     assert kq.PACK_BYTES_PER_FACTOR == 6 * 64 * 16 + 16
 
 
+def test_quantize_lu_rejects():
+    L = kq.lib()
+    q = lambda **kw: L.kq_quantize_lu(kw.get("X", FAKE), kw.get("M", 4), kw.get("d", 64), kw.get("lu", FAKE),
+                                      kw.get("a", 4), kw.get("nfac", 1), kw.get("codes", FAKE), kw.get("scales", FAKE),
+                                      kw.get("y", None), kw.get("y16", None), None)
+    assert q(a=3) == UNSUPPORTED and q(a=16) == UNSUPPORTED and q(a=0) == UNSUPPORTED
+    assert q(nfac=3) == UNSUPPORTED
+    assert q(lu=None) == NULLP
+    assert q(lu=FAKE + 2) == MISALIGNED
+    assert q(y16=FAKE + 8) == MISALIGNED
+    assert q(d=48) == INVALID
+    assert q(M=0) == SUCCESS
+    assert q(M=0, nfac=2) == SUCCESS
+
+
 def test_comparators_reject():
     L = kq.lib()
     assert L.kq_smoothquant_quantize(FAKE, 4, 64, None, FAKE, FAKE, None, None) == NULLP
