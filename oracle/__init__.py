@@ -59,12 +59,13 @@ def _lib():
     lib.kqo_e2m1_codes.argtypes = [P, I64, I, P]
     lib.kqo_e8m0_scales.argtypes = [P, I64, P]
     lib.kqo_lu_factors.argtypes = [P, I, I64, P, P]
+    lib.kqo_fwht.argtypes = [P, I64, I64, P, P, P]
     lib.kqo_f32_to_bf16.argtypes = [P, I64, P]
     lib.kqo_num_threads.argtypes = []
     lib.kqo_set_num_threads.argtypes = [I]
     for name in ("kqo_quantize", "kqo_quantize_f32", "kqo_smoothquant", "kqo_hadamard32",
                  "kqo_mxfp4", "kqo_e2m1_codes", "kqo_e8m0_scales", "kqo_num_threads", "kqo_lu_factors",
-                 "kqo_f32_to_bf16"):
+                 "kqo_f32_to_bf16", "kqo_fwht"):
         getattr(lib, name).restype = ctypes.c_int
     lib.kqo_set_num_threads.restype = None
     return lib
@@ -152,6 +153,16 @@ def quantize_lu(X, lu, a, want_y=False):
     codes, scales, y = quantize(X, A, B, want_y=True)
     y16 = f32_to_bf16(y)
     return codes, scales, (y if want_y else None), (y16 if want_y else None)
+
+
+def fwht(X, want_y=False):
+    """Full-row FWHT comparator: y = H_d x / sqrt(d) (d a power of two, Sylvester
+    order, butterflies h = 1 .. d/2 in fp32), then MXFP4 (Sec. 4.4, Table 2)."""
+    X = _bf16_bits(X)
+    M, d = X.shape
+    codes, scales, y = _outputs(M, d, want_y)
+    _check(_lib().kqo_fwht(_ptr(X), M, d, _ptr(codes), _ptr(scales), _ptr(y)), "fwht")
+    return codes, scales, y
 
 
 def f32_to_bf16(v):

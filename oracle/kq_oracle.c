@@ -252,6 +252,41 @@ int kqo_e8m0_scales(const float* amax, int64_t n, uint8_t* out) {
     return 0;
 }
 
+/* Full-row fast Walsh-Hadamard transform comparator (the FWHT column of
+ * Sec. 4.4, Table 2; Hadamard rotations of the whole hidden dimension, Sec. 1
+ * and 2): for d = 2^n, y = H_d x / sqrt(d) with H_d the Sylvester matrix
+ * H_2 (x) ... (x) H_2, evaluated by butterflies
+ *     (u_i, u_{i+h}) <- (u_i + u_{i+h}, u_i - u_{i+h}),  h = 1, 2, 4, ..., d/2,
+ * in fp32, then one multiply by the fp32 nearest to 1/sqrt(d); then MXFP4 of
+ * every 32-element block of the transformed row.  For d = 32 this is exactly
+ * the Hadamard-32 comparator. */
+int kqo_fwht(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, uint8_t* scales, float* yout) {
+    if (M < 0 || d < BLK || (d & (d - 1)) != 0) return -1;
+    if (!X || !codes || !scales) return -2;
+    const float inv_sqrt_d = (float)(1.0 / sqrt((double)d));
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < M; ++r) {
+        float u[1 << 16];
+        if (d > (1 << 16)) continue;
+        for (int64_t k = 0; k < d; ++k) u[k] = bf16_to_f32(X[r * d + k]);
+        for (int64_t h = 1; h < d; h <<= 1) {
+            for (int64_t i = 0; i < d; ++i) {
+                if (i & h) continue;
+                float s0 = u[i] + u[i + h];
+                float s1 = u[i] - u[i + h];
+                u[i] = s0;
+                u[i + h] = s1;
+            }
+        }
+        for (int64_t k = 0; k < d; ++k) u[k] = u[k] * inv_sqrt_d;
+        for (int64_t j = 0; j < d / BLK; ++j)
+            encode_block(u + j * BLK, codes + r * (d / 2) + j * (BLK / 2), scales + r * (d / BLK) + j);
+        if (yout)
+            for (int64_t k = 0; k < d; ++k) yout[r * d + k] = u[k];
+    }
+    return 0;
+}
+
 /* Factors of the on-the-fly variant K2 from the paper's LU parameters (Sec. 3.2
  * "Parametrization", Sec. 3.5 "K2").  For each factor pair f, lu[f][k] =
  * (a_k, b_k, c_k), k = 0..4, parametrize the 2x2 factor G_{k+1} = L U with

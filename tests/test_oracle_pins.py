@@ -240,6 +240,28 @@ def test_f32_to_bf16_round_to_nearest_even():
     assert np.array_equal(oracle.f32_to_bf16(v), want)
 
 
+def test_fwht_against_dense_and_hadamard32():
+    """Full-row FWHT comparator: for d = 32 bit-identical to the Hadamard-32
+    comparator (same butterflies, same constant); for larger d within the
+    fp32 butterfly error bound of the dense fp64 H_d x / sqrt(d) (Sylvester
+    order); energy preserved (H_d / sqrt(d) orthonormal)."""
+    from scipy.linalg import hadamard
+    X = synth.activations(48, 32, "normal", seed=11)
+    for got, want in zip(oracle.fwht(X, want_y=True), oracle.hadamard32(X, want_y=True)):
+        assert np.array_equal(got, want)
+    for d in (256, 2048):
+        X = synth.activations(16, d, "student_t3", seed=12, chan_frac=0.02, chan_factor=30.0)
+        x = oracle.bf16_to_f32(X).astype(np.float64)
+        _, _, y = oracle.fwht(X, want_y=True)
+        ref = x @ hadamard(d).T / np.sqrt(d)
+        n = int(np.log2(d))
+        bound = (n + 2) * 2.0 ** -24 * np.abs(x).sum(1, keepdims=True) / np.sqrt(d)
+        assert np.all(np.abs(y - ref) <= bound)
+        assert np.allclose((y.astype(np.float64) ** 2).sum(1), (x ** 2).sum(1), rtol=1e-5)
+    with pytest.raises(ValueError):
+        oracle.fwht(synth.activations(4, 96, "normal", seed=1))
+
+
 def test_sylvester_hadamard_split():
     from scipy.linalg import hadamard
     assert np.array_equal(np.kron(hadamard(4), hadamard(8)), hadamard(32))
