@@ -73,6 +73,8 @@ def parse():
                          "roofline field; needs no GPU")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")
+    ap.add_argument("--no-table2", action="store_true",
+                    help="skip the power-of-two-d comparison (Q4, Scale, K1, K2, FWHT) at the paper's Table 2 shapes")
     return ap.parse_args()
 
 
@@ -235,6 +237,7 @@ def main():
         comparators[name + "_us"] = round(ms * 1e3, 3)
         comparators[name + "_gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
     ms_warm, _ = timed(run_kq, args.steps, args.warmup, rotate=False)
+    table2 = None if args.no_table2 else table2_shapes(kq, synth, dev, stream, sptr)
     dist = per_launch(run_kq)
 
     parity = "skipped"
@@ -282,8 +285,61 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
         "cpu_baseline": cpu,
+        "table2_pow2_d": table2,
     }
     print(json.dumps(line), flush=True)
+
+
+TABLE2_SHAPES = [(4096, 1024), (4096, 4096), (4096, 16384), (512, 4096), (512, 16384)]
+
+
+def table2_shapes(kq, synth, dev, stream, sptr, steps=500, warmup=200):
+    """The paper's power-of-two-d comparison (Sec. 4.4, Table 2): Q4, Scale
+    (SmoothQuant), K1 (kq_quantize_packed), K2 (kq_quantize_lu, 15 parameters
+    decoded on chip) and the full-row FWHT, each timed like the headline
+    (MALL-cold rotation, HIP events around `steps` back-to-back launches)."""
+    import torch
+    A, B = synth.factors(4, 8, 1, seed=5)
+    Ad, Bd = torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev)
+    lu = torch.from_numpy(synth.lu_params(1, seed=7)).to(dev)
+    kpack = kq.pack_factors(Ad, Bd, stream=sptr)
+    out = {}
+    for m, d in TABLE2_SHAPES:
+        X = synth.activations(m, d, "student_t3", seed=m + d, chan_frac=0.005, chan_factor=50.0)
+        mult = torch.from_numpy(synth.smoothquant_multipliers(X)).to(dev)
+        nbytes = algorithmic_bytes(m, d)
+        nsets = max(2, int(np.ceil(2 * MALL_BYTES / nbytes)) + 1)
+        X0 = torch.from_numpy(X.view(np.int16)).view(torch.bfloat16).to(dev)
+        Xs = [X0.clone() for _ in range(nsets)]
+        Cs = [torch.empty((m, d // 2), dtype=torch.uint8, device=dev) for _ in range(nsets)]
+        Ss = [torch.empty((m, d // 32), dtype=torch.uint8, device=dev) for _ in range(nsets)]
+        fns = {
+            "q4": lambda i: kq.mxfp4(Xs[i], codes=Cs[i], scales=Ss[i], stream=sptr),
+            "scale": lambda i: kq.smoothquant(Xs[i], mult, codes=Cs[i], scales=Ss[i], stream=sptr),
+            "k1": lambda i: kq.quantize_packed(Xs[i], Ad, Bd, kpack, codes=Cs[i], scales=Ss[i], stream=sptr),
+            "k2": lambda i: kq.quantize_lu(Xs[i], lu, 4, codes=Cs[i], scales=Ss[i], stream=sptr),
+            "fwht": lambda i: kq.fwht(Xs[i], codes=Cs[i], scales=Ss[i], stream=sptr),
+        }
+        row = {}
+        for name, fn in fns.items():
+            for i in range(warmup):
+                fn(i % nsets)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for i in range(steps):
+                fn(i % nsets)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            row[name + "_us"] = round(e0.elapsed_time(e1) / steps * 1e3, 3)
+        row["k1_gbs"] = round(nbytes / row["k1_us"] * 1e-3, 1)
+        row["scale_over_k1"] = round(row["scale_us"] / row["k1_us"], 3)
+        row["scale_over_k2"] = round(row["scale_us"] / row["k2_us"], 3)
+        row["fwht_over_k2"] = round(row["fwht_us"] / row["k2_us"], 3)
+        out[f"{m}x{d}"] = row
+        del Xs, Cs, Ss, X0
+        torch.cuda.empty_cache()
+    return out
 
 
 def check_parity(w, run_kq, run_k2, run_kx, Cs, Ss):

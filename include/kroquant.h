@@ -176,6 +176,18 @@ kq_status kq_hadamard32_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_
                                  uint8_t* scales, float* y_out, void* stream);
 
 /*
+ * kq_fwht_quantize -- full-row fast Walsh-Hadamard comparator (the FWHT
+ * baseline of Sec. 4.4, Table 2): y = H_d x / sqrt(d) over the whole row,
+ * H_d the Sylvester matrix, computed in fp32 by add/subtract butterflies with
+ * strides 1, 2, 4, ..., d/2 (in that order) and one final multiply by the
+ * fp32 nearest to 1/sqrt(d); then MXFP4 of every 32-element block.  d must be
+ * a power of two from 32 to 16384 (KQ_ERROR_UNSUPPORTED otherwise); d = 32 is
+ * kq_hadamard32_quantize.  Other arguments as kq_hadamard32_quantize.
+ */
+kq_status kq_fwht_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, uint8_t* scales,
+                           float* y_out, void* stream);
+
+/*
  * kq_mxfp4_quantize -- the bare MXFP4 quantizer ("Q4", the lower bound of
  * Sec. 4.4): y = x, then MXFP4.
  */

@@ -21,7 +21,7 @@ STATUS = {
 
 EXPORTED = (
     "kq_quantize", "kq_quantize_exact", "kq_quantize_packed", "kq_pack_factors", "kq_quantize_lu",
-    "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_mxfp4_quantize",
+    "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_fwht_quantize", "kq_mxfp4_quantize",
     "kq_e2m1_encode", "kq_weight_transform", "kq_factors_inverse_transpose", "kq_lu_to_factors",
     "kq_status_string", "kq_last_error_detail", "kq_version",
 )
@@ -50,12 +50,13 @@ def lib() -> ctypes.CDLL:
     L.kq_quantize_lu.argtypes = [P, I64, I64, P, I, I64, P, P, P, P, P]
     L.kq_smoothquant_quantize.argtypes = [P, I64, I64, P, P, P, P, P]
     L.kq_hadamard32_quantize.argtypes = [P, I64, I64, P, P, P, P]
+    L.kq_fwht_quantize.argtypes = [P, I64, I64, P, P, P, P]
     L.kq_mxfp4_quantize.argtypes = [P, I64, I64, P, P, P]
     L.kq_e2m1_encode.argtypes = [P, I64, I, P, P]
     L.kq_weight_transform.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P]
     L.kq_factors_inverse_transpose.argtypes = [P, P, I, I, I64, P, P]
     L.kq_lu_to_factors.argtypes = [P, I, I64, P, P]
-    for name in EXPORTED[:12]:
+    for name in EXPORTED[:13]:
         getattr(L, name).restype = ctypes.c_int
     L.kq_status_string.argtypes = [I]
     L.kq_status_string.restype = ctypes.c_char_p
@@ -209,6 +210,16 @@ def hadamard32(X, codes=None, scales=None, y=None, want_y=False, stream=None):
     M, d = X.shape
     _check(lib().kq_hadamard32_quantize(_ptr(X), M, d, _ptr(codes), _ptr(scales), _ptr(y), _stream(stream)),
            "kq_hadamard32_quantize")
+    return codes, scales, y
+
+
+def fwht(X, codes=None, scales=None, y=None, want_y=False, stream=None):
+    """Full-row FWHT comparator kq_fwht_quantize (d a power of two)."""
+    _need(X, torch.bfloat16, "X")
+    codes, scales, y = _outputs(X, codes, scales, y, want_y)
+    M, d = X.shape
+    _check(lib().kq_fwht_quantize(_ptr(X), M, d, _ptr(codes), _ptr(scales), _ptr(y), _stream(stream)),
+           "kq_fwht_quantize")
     return codes, scales, y
 
 

@@ -273,6 +273,17 @@ kq_status kq_hadamard32_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_
                     "kq_hadamard32_quantize");
 }
 
+kq_status kq_fwht_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, uint8_t* scales,
+                           float* y_out, void* stream) {
+    kq_status st = check_common(X, M, d, codes, scales, y_out, true);
+    if (st != KQ_SUCCESS) return st;
+    if (d > 16384 || (d & (d - 1)) != 0)
+        return fail(KQ_ERROR_UNSUPPORTED, "d = %lld must be a power of two from 32 to 16384", (long long)d);
+    if (M == 0) return ok();
+    kq::Params p = make_params(X, M, d, codes, scales, y_out);
+    return from_hip(kq::launch_fwht(p, (hipStream_t)stream), "kq_fwht_quantize");
+}
+
 kq_status kq_mxfp4_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, uint8_t* scales,
                             void* stream) {
     kq_status st = check_common(X, M, d, codes, scales, nullptr, true);

@@ -43,5 +43,6 @@ struct LaunchConfig {
 hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg);
 hipError_t launch_pack(int a, const float* A, const float* B, int64_t nfac, uint8_t* kpack, hipStream_t st);
 hipError_t launch_e2m1(const float* v, int64_t npairs, uint32_t s, uint8_t* codes, hipStream_t st);
+hipError_t launch_fwht(const Params& p, hipStream_t st);  // d a power of two, 32 .. 16384
 
 }  // namespace kq

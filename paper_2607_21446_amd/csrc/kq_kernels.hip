@@ -1128,6 +1128,103 @@ __global__ __launch_bounds__(kThreads) void e2m1_kernel(const float* __restrict_
     }
 }
 
+// ------------------------------------------------------------------ full-row FWHT comparator
+// y = H_d x / sqrt(d) over the whole row (d = 2^LOG2D, 32 <= d <= 16384): the
+// FWHT baseline of Sec. 4.4 (Table 2), then MXFP4 of every 32-element block.
+// Same butterflies in the same order as the fixed-order definition -- stride
+// h = 1, 2, ..., d/2, then one multiply by the fp32 nearest to 1/sqrt(d) -- so
+// the outputs are bit-identical to it.  A thread owns 32 elements of its row
+// at a time.  Pass q applies the strides 2^(5q) .. 2^(5q+k-1) (k <= 5 index
+// bits) in registers; between passes the row goes through LDS (fp32, one pad
+// float per 32) from one element assignment to the next:
+//   element of slot j in pass (lo, k) =
+//     deposit(v, other bits) | (j mod 2^k) << lo,   v = tl | (j >> k) << (LOG2D - 5),
+// "other bits" being the index bits outside [lo, lo + k) in increasing order,
+// tl the thread's index within its row.  Pass 0 is the thread's own block.
+template <int LOG2D>
+__device__ __forceinline__ int fwht_index(int lo, int k, int j, int tl) {
+    const int v = tl | ((j >> k) << (LOG2D - 5));
+    const int low = v & ((1 << lo) - 1);
+    return low | ((j & ((1 << k) - 1)) << lo) | ((v >> lo) << (lo + k));
+}
+
+template <int LOG2D>
+__global__ __launch_bounds__(LOG2D == 14 ? 512 : 256) void fwht_kernel(const Params p) {
+    constexpr int D = 1 << LOG2D;
+    constexpr int TPR = D / 32;                   // threads per row
+    constexpr int T = TPR < 256 ? 256 : TPR;      // threads per workgroup
+    constexpr int R = T / TPR;                    // rows per workgroup
+    constexpr int NPASS = (LOG2D + 4) / 5;
+    constexpr int RS = D + D / 32;                // padded row stride in LDS
+    __shared__ float buf[NPASS > 1 ? R * RS : 1];
+    const int t = threadIdx.x;
+    const int r = t / TPR, tl = t % TPR;
+    const int64_t row = (int64_t)blockIdx.x * R + r;
+    const bool active = row < p.M;
+    float u[32];
+    {
+        const uint4* src = reinterpret_cast<const uint4*>(p.X + (active ? row : 0) * D) + tl * 4;
+#pragma unroll
+        for (int m = 0; m < 4; ++m) unpack8(active ? src[m] : make_uint4(0u, 0u, 0u, 0u), u + 8 * m);
+    }
+    float* rb = buf + r * RS;
+    auto pad = [](int i) { return i + (i >> 5); };
+#pragma unroll
+    for (int q = 0; q < NPASS; ++q) {
+        const int lo = 5 * q, k = (LOG2D - lo) < 5 ? (LOG2D - lo) : 5;
+        if (q > 0) {
+            const int plo = 5 * (q - 1);
+            __syncthreads();  // earlier reads of buf are done
+#pragma unroll
+            for (int j = 0; j < 32; ++j) rb[pad(fwht_index<LOG2D>(plo, 5, j, tl))] = u[j];
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < 32; ++j) u[j] = rb[pad(fwht_index<LOG2D>(lo, k, j, tl))];
+        }
+#pragma unroll
+        for (int b = 0; b < 5; ++b) {
+            if (b >= k) break;
+            const int h = 1 << b;
+#pragma unroll
+            for (int j = 0; j < 32; ++j) {
+                if (j & h) continue;
+                const float s0 = u[j] + u[j + h];
+                const float s1 = u[j] - u[j + h];
+                u[j] = s0;
+                u[j + h] = s1;
+            }
+        }
+    }
+    if (NPASS > 1) {  // back to the thread's own block
+        const int llo = 5 * (NPASS - 1), lk = LOG2D - llo;
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < 32; ++j) rb[pad(fwht_index<LOG2D>(llo, lk, j, tl))] = u[j];
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < 32; ++j) u[j] = rb[pad(fwht_index<LOG2D>(0, 5, j, tl))];
+    }
+    // fp32 nearest to 1/sqrt(d): 2^(-n/2) for even n, fp32(1/sqrt2) * 2^(-(n-1)/2) for odd n
+    const float inv_sqrt_d = (LOG2D & 1) ? __uint_as_float(0x3F3504F3u - ((uint32_t)(LOG2D - 1) / 2u << 23))
+                                         : __uint_as_float((uint32_t)(127 - LOG2D / 2) << 23);
+    float y[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) y[j] = u[j] * inv_sqrt_d;
+    if (!active) return;
+    uint32_t w[4];
+    const uint32_t sbyte = encode32(y, w);
+    const int64_t blk = row * TPR + tl;
+    if (p.codes) {
+        *reinterpret_cast<uint4*>(p.codes + blk * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+        p.scales[blk] = (uint8_t)sbyte;
+    }
+    if (p.y) {
+        float4* dst = reinterpret_cast<float4*>(p.y + blk * 32);
+#pragma unroll
+        for (int m = 0; m < 8; ++m) dst[m] = make_float4(y[4 * m], y[4 * m + 1], y[4 * m + 2], y[4 * m + 3]);
+    }
+}
+
 // ------------------------------------------------------------------ launchers
 template <Mapping MAP, class Op>
 static hipError_t launch_map(Params p, hipStream_t st, const LaunchConfig& cfg) {
@@ -1254,6 +1351,32 @@ hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st
             }
     }
     return hipErrorInvalidValue;
+}
+
+template <int LOG2D>
+static hipError_t launch_fwht_n(const Params& p, hipStream_t st) {
+    constexpr int TPR = (1 << LOG2D) / 32;
+    constexpr int T = TPR < 256 ? 256 : TPR;
+    constexpr int R = T / TPR;
+    const int64_t g = (p.M + R - 1) / R;
+    hipLaunchKernelGGL((fwht_kernel<LOG2D>), dim3((unsigned)g), dim3(T), 0, st, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_fwht(const Params& p, hipStream_t st) {
+    switch (p.d) {
+        case 32: return launch_fwht_n<5>(p, st);
+        case 64: return launch_fwht_n<6>(p, st);
+        case 128: return launch_fwht_n<7>(p, st);
+        case 256: return launch_fwht_n<8>(p, st);
+        case 512: return launch_fwht_n<9>(p, st);
+        case 1024: return launch_fwht_n<10>(p, st);
+        case 2048: return launch_fwht_n<11>(p, st);
+        case 4096: return launch_fwht_n<12>(p, st);
+        case 8192: return launch_fwht_n<13>(p, st);
+        case 16384: return launch_fwht_n<14>(p, st);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_e2m1(const float* v, int64_t npairs, uint32_t s, uint8_t* codes, hipStream_t st) {

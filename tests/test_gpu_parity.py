@@ -300,6 +300,18 @@ def test_kroquant_lu_hadamard_init():
         assert np.max(np.abs(y - want[2])) <= 1e-5 * np.abs(want[2]).max()
 
 
+@pytest.mark.parametrize("d", [32, 64, 256, 1024, 2048, 4096, 8192, 16384])
+def test_fwht_parity(d):
+    """Full-row FWHT comparator: bit-identical to the oracle's butterflies
+    (every pass layout, including partial last passes and ragged row counts)."""
+    M = {32: 300, 64: 130, 256: 37, 1024: 19, 2048: 9, 4096: 7, 8192: 3, 16384: 2}[d]
+    X = synth.activations(M, d, "student_t3", seed=71, chan_frac=0.01, chan_factor=40.0)
+    X[M // 2] = 0
+    want = oracle.fwht(X, want_y=True)
+    c, s_, y = kq.fwht(dev_bf16(X), want_y=True)
+    assert_exact((host(c), host(s_), host(y)), want, f"fwht d={d}")
+
+
 # ------------------------------------------------------------------ layout, guards, determinism
 def test_guard_bands_and_full_coverage():
     M, d = 77, 2240

@@ -102,6 +102,15 @@ def test_quantize_lu_rejects():
     assert q(M=0, nfac=2) == SUCCESS
 
 
+def test_fwht_rejects():
+    L = kq.lib()
+    for d in (96, 3072, 32768, 48):
+        st = L.kq_fwht_quantize(FAKE, 4, d, FAKE, FAKE, None, None)
+        assert st == (INVALID if d % 32 else UNSUPPORTED), d
+    assert L.kq_fwht_quantize(FAKE, 0, 4096, FAKE, FAKE, None, None) == SUCCESS
+    assert L.kq_fwht_quantize(FAKE + 8, 4, 4096, FAKE, FAKE, None, None) == MISALIGNED
+
+
 def test_comparators_reject():
     L = kq.lib()
     assert L.kq_smoothquant_quantize(FAKE, 4, 64, None, FAKE, FAKE, None, None) == NULLP
