@@ -890,7 +890,7 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
 // the fixed order when its amax mantissa lies within T = ceil(2^24 rho) of 0 or
 // of 2^23 (T from the pack; T = 2^22 flags every block, used above cond 2^13),
 // or when amax < 2^-123, so its E8M0 scale equals the fixed-order one.
-template <Mapping MAP, int NA, int NB>
+template <Mapping MAP, int NA, int NB, bool ILV>
 __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
     __shared__ uint4 lds[256];
     const int lane = threadIdx.x;
@@ -962,14 +962,8 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
     const int rslot = 4 * jl + (h ^ ((jl >> 2) & 3));
     wave_lds_sync();
     uint64_t edges = 0;  // blocks of the unit on a binade edge (bit = block index)
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-        if (32 * t >= nvalid) break;
-        const int bt = 32 * t + jl;
-        const bool valid = bt < nvalid;
-        uint4 raw[2];
-        raw[0] = lds[128 * t + rslot];
-        raw[1] = lds[128 * t + (rslot ^ 2)];
+    // the three terms, smallest first, of tile t: acc[n][block] += K[n][k-step] . x[block][k-step]
+    auto product = [&](const uint4 (&raw)[2]) {
         f32x16 acc = {};
 #pragma unroll
         for (int s = 0; s < 2; ++s)
@@ -980,6 +974,12 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
 #pragma unroll
         for (int s = 0; s < 2; ++s)
             acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.hi[s], __builtin_bit_cast(bf16x8, raw[s]), acc, 0, 0, 0);
+        return acc;
+    };
+    // amax, binade-edge flag, scale, codes and stores of tile t
+    auto epilogue = [&](int t, const f32x16& acc, const uint4 (&raw)[2]) {
+        const int bt = 32 * t + jl;
+        const bool valid = bt < nvalid;
         // lane holds y[16h + i] of block bt in acc[i]
         float am = 0.0f;
 #pragma unroll
@@ -1009,6 +1009,29 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
             }
         }
         edges |= (__builtin_amdgcn_ballot_w64(near) & 0xFFFFFFFFull) << (32 * t);
+    };
+    if (ILV && nvalid > 32) {
+        // both tiles' products first (two accumulators): the second chain runs
+        // on the matrix cores while the first tile's epilogue is on the VALU
+        uint4 raw[2][2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            raw[t][0] = lds[128 * t + rslot];
+            raw[t][1] = lds[128 * t + (rslot ^ 2)];
+        }
+        const f32x16 acc0 = product(raw[0]);
+        const f32x16 acc1 = product(raw[1]);
+        epilogue(0, acc0, raw[0]);
+        epilogue(1, acc1, raw[1]);
+    } else {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            if (32 * t >= nvalid) break;
+            uint4 raw[2];
+            raw[0] = lds[128 * t + rslot];
+            raw[1] = lds[128 * t + (rslot ^ 2)];
+            epilogue(t, product(raw), raw);
+        }
     }
     // blocks whose amax is on a binade edge: the fixed evaluation order decides
     exact_flagged<NA, NB>(edges, lds, first, bstride, p.A + f * (NA * NA), p.B + f * (NB * NB), p);
@@ -1269,10 +1292,19 @@ static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st, cons
         if (cfg.packed_one_unit) {
             const int64_t units =
                 (map == Mapping::Flat) ? (p.nblocks + 63) / 64 : ((p.M + 63) / 64) * p.nb;
-            if (map == Mapping::Flat)
-                hipLaunchKernelGGL((kron_mfma_unit_kernel<Mapping::Flat, NA, NB>), dim3((unsigned)units), dim3(64), 0, st, p);
-            else
-                hipLaunchKernelGGL((kron_mfma_unit_kernel<Mapping::Column, NA, NB>), dim3((unsigned)units), dim3(64), 0, st, p);
+            // small grids (few waves per SIMD) hide less latency: interleave the two tiles
+            const bool ilv = units <= cfg.interleave_max_units;
+            if (map == Mapping::Flat) {
+                if (ilv)
+                    hipLaunchKernelGGL((kron_mfma_unit_kernel<Mapping::Flat, NA, NB, true>), dim3((unsigned)units), dim3(64), 0, st, p);
+                else
+                    hipLaunchKernelGGL((kron_mfma_unit_kernel<Mapping::Flat, NA, NB, false>), dim3((unsigned)units), dim3(64), 0, st, p);
+            } else {
+                if (ilv)
+                    hipLaunchKernelGGL((kron_mfma_unit_kernel<Mapping::Column, NA, NB, true>), dim3((unsigned)units), dim3(64), 0, st, p);
+                else
+                    hipLaunchKernelGGL((kron_mfma_unit_kernel<Mapping::Column, NA, NB, false>), dim3((unsigned)units), dim3(64), 0, st, p);
+            }
             return hipGetLastError();
         }
         if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, true>(p, map, st, cfg);

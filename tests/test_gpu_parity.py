@@ -312,6 +312,45 @@ def test_fwht_parity(d):
     assert_exact((host(c), host(s_), host(y)), want, f"fwht d={d}")
 
 
+def test_hip_graph_replays_match_eager():
+    """The hot-path and comparator launches captured into one HIP graph (as the
+    benchmark's power-of-two-d table does) and replayed three times, with eager
+    work and synchronizations between the replays: every replay reproduces the
+    eager outputs (no allocation, memset or host sync inside the calls)."""
+    X = synth.activations(512, 4096, "student_t3", seed=81)
+    A, B = synth.factors(4, 8, 1, seed=82)
+    lu = synth.lu_params(1, seed=83)
+    Xd, Ad, Bd, lud = dev_bf16(X), dev_f32(A), dev_f32(B), dev_f32(lu)
+    mult = dev_f32(synth.smoothquant_multipliers(X))
+    kpack = kq.pack_factors(Ad, Bd)
+    outs = [(torch.empty((512, 2048), dtype=torch.uint8, device="cuda"),
+             torch.empty((512, 128), dtype=torch.uint8, device="cuda")) for _ in range(4)]
+    calls = [
+        lambda c, s: kq.quantize_packed(Xd, Ad, Bd, kpack, codes=c, scales=s),
+        lambda c, s: kq.quantize_lu(Xd, lud, 4, codes=c, scales=s),
+        lambda c, s: kq.smoothquant(Xd, mult, codes=c, scales=s),
+        lambda c, s: kq.fwht(Xd, codes=c, scales=s),
+    ]
+    for call, (c, s) in zip(calls, outs):
+        call(c, s)
+    eager = [(host(c).copy(), host(s).copy()) for c, s in outs]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for call, (c, s) in zip(calls, outs):
+            call(c, s)
+    other = dev_bf16(synth.activations(256, 1024, "normal", seed=84))
+    for rep in range(3):
+        for c, s in outs:
+            c.fill_(0xAB)
+            s.fill_(0xCD)
+        kq.mxfp4(other)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k, (c, s) in enumerate(outs):
+            assert np.array_equal(host(c), eager[k][0]) and np.array_equal(host(s), eager[k][1]), (rep, k)
+
+
 # ------------------------------------------------------------------ layout, guards, determinism
 def test_guard_bands_and_full_coverage():
     M, d = 77, 2240
