@@ -188,6 +188,25 @@ kq_status kq_fwht_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* cod
                            float* y_out, void* stream);
 
 /*
+ * kq_mxfp4_gemm -- the W4A4 product that consumes the quantizer's output (the
+ * quantized linear layer of Sec. 3.1 eq. (1) and Sec. 3.4):
+ *     C[M, N] = deq(A)[M, K] . deq(B)[N, K]^T        (accumulate = 0)
+ *     C[M, N] += deq(A)[M, K] . deq(B)[N, K]^T       (accumulate = 1)
+ * with deq(code, s) = (-1)^sign E2M1[magnitude] 2^(s - 127).  A is an MXFP4
+ * activation as written by kq_quantize* (codes [M, K/2], scales [M, K/32]) and
+ * B an MXFP4 weight as written by kq_weight_transform (codes [N, K/2], scales
+ * [N, K/32]); both row-major and contiguous, K a positive multiple of 32.  C
+ * is fp32 [M, ldc] (ldc >= N).  Runs on the matrix cores (scaled E2M1 x E2M1
+ * products, exact; fp32 accumulation in an unspecified order).  All pointers
+ * are device pointers; codes 16-byte aligned, C 4-byte aligned.  M, N = 0 is
+ * a no-op; M may be at most 65535 * 128.  Enqueued on `stream`; no
+ * allocation, no synchronization.
+ */
+kq_status kq_mxfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, int64_t M, const uint8_t* b_codes,
+                        const uint8_t* b_scales, int64_t N, int64_t K, float* C, int64_t ldc, int accumulate,
+                        void* stream);
+
+/*
  * kq_mxfp4_quantize -- the bare MXFP4 quantizer ("Q4", the lower bound of
  * Sec. 4.4): y = x, then MXFP4.
  */

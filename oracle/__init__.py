@@ -252,6 +252,26 @@ def dequantize(codes, scales):
     return sign * mag * np.exp2(s - 127.0)
 
 
+def mxfp4_gemm(a_codes, a_scales, b_codes, b_scales):
+    """The W4A4 product that consumes the quantizer's output (Sec. 3.1 eq. (1)):
+    C[M, N] = deq(A)[M, K] . deq(B)[N, K]^T in fp64 (every product of two
+    dequantized values is exact in fp64; the sum is a library matmul)."""
+    return dequantize(a_codes, a_scales) @ dequantize(b_codes, b_scales).T
+
+
+def layer_error(X, W, A, B):
+    """E(T) of Sec. 3.1: || X W^T - Q(X T) Q(W T^-T)^T ||_F with the KroQuant
+    block transform T = diag(A (x) B) on the activation (oracle quantizer) and
+    the inverse transpose on the weight (Sec. 3.4), in fp64.  Also returns the
+    two quantized operands and the fp64 X W^T."""
+    x = bf16_to_f32(X).astype(np.float64) if np.asarray(X).dtype == np.uint16 else np.asarray(X, np.float64)
+    w = bf16_to_f32(W).astype(np.float64) if np.asarray(W).dtype == np.uint16 else np.asarray(W, np.float64)
+    xc, xs, _ = quantize(X, A, B)
+    _, wc, ws = weight_transform(W, A, B)
+    ref = x @ w.T
+    return float(np.linalg.norm(ref - mxfp4_gemm(xc, xs, wc, ws))), (xc, xs), (wc, ws), ref
+
+
 def kron_dense(A, B):
     """Materialised 32x32 blocks K = A (x) B, fp64, numpy.kron index order
     (row index = i_A * b + i_B): [nfac, 32, 32]."""

@@ -21,7 +21,7 @@ STATUS = {
 
 EXPORTED = (
     "kq_quantize", "kq_quantize_exact", "kq_quantize_packed", "kq_pack_factors", "kq_quantize_lu",
-    "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_fwht_quantize", "kq_mxfp4_quantize",
+    "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_fwht_quantize", "kq_mxfp4_quantize", "kq_mxfp4_gemm",
     "kq_e2m1_encode", "kq_weight_transform", "kq_factors_inverse_transpose", "kq_lu_to_factors",
     "kq_status_string", "kq_last_error_detail", "kq_version",
 )
@@ -51,12 +51,13 @@ def lib() -> ctypes.CDLL:
     L.kq_smoothquant_quantize.argtypes = [P, I64, I64, P, P, P, P, P]
     L.kq_hadamard32_quantize.argtypes = [P, I64, I64, P, P, P, P]
     L.kq_fwht_quantize.argtypes = [P, I64, I64, P, P, P, P]
+    L.kq_mxfp4_gemm.argtypes = [P, P, I64, P, P, I64, I64, P, I64, I, P]
     L.kq_mxfp4_quantize.argtypes = [P, I64, I64, P, P, P]
     L.kq_e2m1_encode.argtypes = [P, I64, I, P, P]
     L.kq_weight_transform.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P]
     L.kq_factors_inverse_transpose.argtypes = [P, P, I, I, I64, P, P]
     L.kq_lu_to_factors.argtypes = [P, I, I64, P, P]
-    for name in EXPORTED[:13]:
+    for name in EXPORTED[:14]:
         getattr(L, name).restype = ctypes.c_int
     L.kq_status_string.argtypes = [I]
     L.kq_status_string.restype = ctypes.c_char_p
@@ -221,6 +222,22 @@ def fwht(X, codes=None, scales=None, y=None, want_y=False, stream=None):
     _check(lib().kq_fwht_quantize(_ptr(X), M, d, _ptr(codes), _ptr(scales), _ptr(y), _stream(stream)),
            "kq_fwht_quantize")
     return codes, scales, y
+
+
+def mxfp4_gemm(a_codes, a_scales, b_codes, b_scales, C=None, accumulate=False, stream=None):
+    """kq_mxfp4_gemm: C[M, N] (+)= deq(A) deq(B)^T for MXFP4 operands (codes
+    uint8 [rows, K/2], scales uint8 [rows, K/32]).  Returns C (fp32)."""
+    for t, name in ((a_codes, "a_codes"), (a_scales, "a_scales"), (b_codes, "b_codes"), (b_scales, "b_scales")):
+        _need(t, torch.uint8, name)
+    M, N, K = a_codes.shape[0], b_codes.shape[0], 2 * a_codes.shape[1]
+    if b_codes.shape[1] * 2 != K or a_scales.shape != (M, K // 32) or b_scales.shape != (N, K // 32):
+        raise ValueError("operand shapes do not match")
+    if C is None:
+        C = torch.empty((M, N), dtype=torch.float32, device=a_codes.device)
+    _need(C, torch.float32, "C")
+    _check(lib().kq_mxfp4_gemm(_ptr(a_codes), _ptr(a_scales), M, _ptr(b_codes), _ptr(b_scales), N, K, _ptr(C),
+                               C.stride(0), int(accumulate), _stream(stream)), "kq_mxfp4_gemm")
+    return C
 
 
 def mxfp4(X, codes=None, scales=None, stream=None):

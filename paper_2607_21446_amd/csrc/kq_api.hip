@@ -284,6 +284,34 @@ kq_status kq_fwht_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* cod
     return from_hip(kq::launch_fwht(p, (hipStream_t)stream), "kq_fwht_quantize");
 }
 
+kq_status kq_mxfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, int64_t M, const uint8_t* b_codes,
+                        const uint8_t* b_scales, int64_t N, int64_t K, float* C, int64_t ldc, int accumulate,
+                        void* stream) {
+    if (M < 0 || N < 0) return fail(KQ_ERROR_INVALID_VALUE, "M = %lld and N = %lld must be >= 0", (long long)M, (long long)N);
+    if (K <= 0 || K % 32 != 0) return fail(KQ_ERROR_INVALID_VALUE, "K = %lld must be a positive multiple of 32", (long long)K);
+    if (ldc < N) return fail(KQ_ERROR_INVALID_VALUE, "ldc = %lld must be >= N = %lld", (long long)ldc, (long long)N);
+    if (accumulate != 0 && accumulate != 1) return fail(KQ_ERROR_INVALID_VALUE, "accumulate must be 0 or 1");
+    if ((M + 127) / 128 > 65535 || (N + 127) / 128 > 2147483647)
+        return fail(KQ_ERROR_INVALID_VALUE, "M = %lld is too large (at most 65535 * 128 rows)", (long long)M);
+    if (M == 0 || N == 0) return ok();
+    if (!a_codes || !a_scales || !b_codes || !b_scales || !C)
+        return fail(KQ_ERROR_NULL_POINTER, "codes, scales and C must not be NULL");
+    if (!aligned(a_codes, 16) || !aligned(b_codes, 16)) return fail(KQ_ERROR_MISALIGNED, "codes must be 16-byte aligned");
+    if (!aligned(C, 4)) return fail(KQ_ERROR_MISALIGNED, "C must be 4-byte aligned");
+    kq::GemmParams g{};
+    g.a_codes = a_codes;
+    g.a_scales = a_scales;
+    g.M = M;
+    g.b_codes = b_codes;
+    g.b_scales = b_scales;
+    g.N = N;
+    g.K = K;
+    g.C = C;
+    g.ldc_out = ldc;
+    g.accumulate = accumulate;
+    return from_hip(kq::launch_mxfp4_gemm(g, (hipStream_t)stream), "kq_mxfp4_gemm");
+}
+
 kq_status kq_mxfp4_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, uint8_t* scales,
                             void* stream) {
     kq_status st = check_common(X, M, d, codes, scales, nullptr, true);

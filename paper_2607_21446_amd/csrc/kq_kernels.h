@@ -41,7 +41,22 @@ struct LaunchConfig {
     int64_t smooth_waves = 2048;            // target workgroups of the column-stationary SmoothQuant
 };
 
+// W4A4 MXFP4 GEMM C[M, N] (+)= deq(A)[M, K] . deq(B)[N, K]^T (kq_gemm.hip).
+struct GemmParams {
+    const uint8_t* a_codes;   // [M, K/2]
+    const uint8_t* a_scales;  // [M, K/32]
+    int64_t M;
+    const uint8_t* b_codes;   // [N, K/2]
+    const uint8_t* b_scales;  // [N, K/32]
+    int64_t N;
+    int64_t K;                // multiple of 32
+    float* C;                 // [M, ldc_out]
+    int64_t ldc_out;
+    int accumulate;           // 1: C += product, 0: C = product
+};
+
 hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg);
+hipError_t launch_mxfp4_gemm(const GemmParams& g, hipStream_t st);
 hipError_t launch_pack(int a, const float* A, const float* B, int64_t nfac, uint8_t* kpack, hipStream_t st);
 hipError_t launch_e2m1(const float* v, int64_t npairs, uint32_t s, uint8_t* codes, hipStream_t st);
 hipError_t launch_fwht(const Params& p, hipStream_t st);  // d a power of two, 32 .. 16384

@@ -432,6 +432,59 @@ def test_weight_transform(ab, per_block):
     assert np.max(np.abs(lhs - xf @ wf.T) / (np.abs(xf) @ np.abs(wf).T)) < 2e-5
 
 
+# ------------------------------------------------------------------ W4A4 GEMM consumer
+def _rand_mx(rows, K, seed):
+    rng = np.random.default_rng(seed)
+    codes = rng.integers(0, 256, (rows, K // 2), dtype=np.uint8)
+    scales = rng.integers(110, 140, (rows, K // 32), dtype=np.uint8)
+    return codes, scales
+
+
+def _gemm_tolerance(ac, as_, bc, bs):
+    # fp32 accumulation of K exact products in any order: |error| <= K u sum |a||b|
+    K = ac.shape[1] * 2
+    return K * 2.0 ** -24 * (np.abs(oracle.dequantize(ac, as_)) @ np.abs(oracle.dequantize(bc, bs)).T)
+
+
+@pytest.mark.parametrize("M,N,K", [(77, 200, 2240), (128, 128, 64), (33, 70, 1120), (300, 257, 3072), (1, 1, 32)])
+def test_mxfp4_gemm_parity(M, N, K):
+    """C = deq(A) deq(B)^T on the matrix cores against the oracle's fp64
+    product, within the fp32 accumulation bound; ragged tiles, odd block
+    counts along K, and the accumulate mode."""
+    ac, as_ = _rand_mx(M, K, seed=M + K)
+    bc, bs = _rand_mx(N, K, seed=N + 2 * K)
+    ref = oracle.mxfp4_gemm(ac, as_, bc, bs)
+    tol = _gemm_tolerance(ac, as_, bc, bs)
+    t = lambda a: torch.from_numpy(a).cuda()
+    C = host(kq.mxfp4_gemm(t(ac), t(as_), t(bc), t(bs)))
+    assert C.shape == (M, N)
+    assert np.all(np.abs(C - ref) <= tol), np.max(np.abs(C - ref) - tol)
+    C0 = np.random.default_rng(7).normal(size=(M, N)).astype(np.float32)
+    Cd = t(C0)
+    kq.mxfp4_gemm(t(ac), t(as_), t(bc), t(bs), C=Cd, accumulate=True)
+    assert np.all(np.abs(host(Cd) - (ref + C0)) <= tol + 2.0 ** -23 * np.abs(ref + C0))
+
+
+def test_w4a4_layer_end_to_end():
+    """X -> kq_quantize_packed, W -> kq_weight_transform, then kq_mxfp4_gemm:
+    the layer output against the oracle's W4A4 product, and E(T) (Sec. 3.1)
+    against the oracle's layer error."""
+    M, N, d = 256, 192, 3072
+    X = synth.activations(M, d, "student_t3", seed=91, chan_frac=0.005, chan_factor=50.0)
+    W = synth.activations(N, d, "normal", seed=92, chan_frac=0.0)
+    A, B = synth.factors(4, 8, 1, seed=93)
+    Ad, Bd = dev_f32(A), dev_f32(B)
+    kpack = kq.pack_factors(Ad, Bd)
+    xc, xs, _ = kq.quantize_packed(dev_bf16(X), Ad, Bd, kpack)
+    _, wc, ws = kq.weight_transform(dev_bf16(W), torch.from_numpy(A), torch.from_numpy(B))
+    C = host(kq.mxfp4_gemm(xc, xs, wc, ws))
+    e_ref, (oxc, oxs), (owc, ows), xw = oracle.layer_error(X, W, A, B)
+    ref = oracle.mxfp4_gemm(host(xc), host(xs), host(wc), host(ws))
+    assert np.all(np.abs(C - ref) <= _gemm_tolerance(host(xc), host(xs), host(wc), host(ws)))
+    e_gpu = float(np.linalg.norm(xw - C))
+    assert abs(e_gpu - e_ref) <= 1e-3 * e_ref, (e_gpu, e_ref)
+
+
 # ------------------------------------------------------------------ full-size workloads
 FULL = ["pixart_8192x1152", "pixart_8192x4608", "sana_4096x2240", "sana_4096x5600", "flux_4608x3072",
         "flux_4608x12288"]

@@ -111,6 +111,19 @@ def test_fwht_rejects():
     assert L.kq_fwht_quantize(FAKE + 8, 4, 4096, FAKE, FAKE, None, None) == MISALIGNED
 
 
+def test_mxfp4_gemm_rejects():
+    L = kq.lib()
+    g = lambda **kw: L.kq_mxfp4_gemm(kw.get("ac", FAKE), kw.get("as_", FAKE), kw.get("M", 4), kw.get("bc", FAKE),
+                                     kw.get("bs", FAKE), kw.get("N", 4), kw.get("K", 64), kw.get("C", FAKE),
+                                     kw.get("ldc", 4), kw.get("acc", 0), None)
+    assert g(K=48) == INVALID and g(K=0) == INVALID and g(M=-1) == INVALID
+    assert g(ldc=3) == INVALID and g(acc=2) == INVALID
+    assert g(M=65535 * 128 + 1) == INVALID
+    assert g(ac=None) == NULLP and g(C=None) == NULLP
+    assert g(ac=FAKE + 8) == MISALIGNED and g(C=FAKE + 2) == MISALIGNED
+    assert g(M=0) == SUCCESS and g(N=0, ldc=0) == SUCCESS
+
+
 def test_comparators_reject():
     L = kq.lib()
     assert L.kq_smoothquant_quantize(FAKE, 4, 64, None, FAKE, FAKE, None, None) == NULLP

@@ -262,6 +262,47 @@ def test_fwht_against_dense_and_hadamard32():
         oracle.fwht(synth.activations(4, 96, "normal", seed=1))
 
 
+def test_mxfp4_gemm_brute_force_and_layer_error():
+    """W4A4 product: against a scalar triple loop over decoded codes (pins the
+    operand orientation: C = deq(A) deq(B)^T) on a tiny case; E(T) of
+    eq. (1): zero for lossless stand-ins, equal to the plain MXFP4 error for
+    identity factors, and the exact-arithmetic invariance X W^T = (X T)(W T^-T)^T."""
+    rng = np.random.default_rng(13)
+    M, N, K = 3, 5, 64
+    ac = rng.integers(0, 256, (M, K // 2), dtype=np.uint8)
+    bc = rng.integers(0, 256, (N, K // 2), dtype=np.uint8)
+    as_ = rng.integers(120, 134, (M, K // 32), dtype=np.uint8)
+    bs = rng.integers(120, 134, (N, K // 32), dtype=np.uint8)
+    C = oracle.mxfp4_gemm(ac, as_, bc, bs)
+    mags = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]
+
+    def val(codes, scales, r, k):
+        byte = int(codes[r, k // 2])
+        c = byte & 15 if k % 2 == 0 else byte >> 4
+        return (-1.0 if c & 8 else 1.0) * mags[c & 7] * 2.0 ** (int(scales[r, k // 32]) - 127)
+    for m in range(M):
+        for n in range(N):
+            ref = sum(val(ac, as_, m, k) * val(bc, bs, n, k) for k in range(K))
+            assert C[m, n] == ref
+    # identity factors: E(T) is the plain MXFP4 layer error
+    X = synth.activations(32, 256, "student_t3", seed=14)
+    W = synth.activations(48, 256, "normal", seed=15)
+    a, b = 4, 8
+    Ai, Bi = np.eye(a, dtype=np.float32)[None], np.eye(b, dtype=np.float32)[None]
+    e_id, _, _, ref = oracle.layer_error(X, W, Ai, Bi)
+    xc, xs = oracle.mxfp4(X)
+    wc, ws = oracle.mxfp4(W)
+    assert np.isclose(e_id, np.linalg.norm(ref - oracle.mxfp4_gemm(xc, xs, wc, ws)), rtol=1e-12)
+    # eq. (1): the unquantized transformed product equals X W^T
+    A, B = synth.factors(a, b, 1, seed=16)
+    Ait, Bit = oracle.factors_inverse_transpose(A, B)
+    xt = oracle.transform_f64(X, A, B)
+    wt = oracle.transform_f64(oracle.bf16_to_f32(W), Ait, Bit)
+    assert np.allclose(xt @ wt.T, ref, rtol=0, atol=1e-5 * np.abs(ref).max())
+    e_kq, _, _, _ = oracle.layer_error(X, W, A, B)
+    assert 0 < e_kq < 0.5 * np.linalg.norm(ref)
+
+
 def test_sylvester_hadamard_split():
     from scipy.linalg import hadamard
     assert np.array_equal(np.kron(hadamard(4), hadamard(8)), hadamard(32))
