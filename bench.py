@@ -73,6 +73,7 @@ def parse():
                          "roofline field; needs no GPU")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")
+    ap.add_argument("--no-gemm", action="store_true", help="skip the W4A4 MXFP4 GEMM consumer timing")
     ap.add_argument("--no-table2", action="store_true",
                     help="skip the power-of-two-d comparison (Q4, Scale, K1, K2, FWHT) at the paper's Table 2 shapes")
     return ap.parse_args()
@@ -238,6 +239,7 @@ def main():
         comparators[name + "_gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
     ms_warm, _ = timed(run_kq, args.steps, args.warmup, rotate=False)
     table2 = None if args.no_table2 else table2_shapes(kq, synth, dev, stream, sptr)
+    gemm = None if args.no_gemm else gemm_timing(kq, synth, dev, stream, sptr, Cs[0], Ss[0], M, d)
     dist = per_launch(run_kq)
 
     parity = "skipped"
@@ -286,6 +288,7 @@ def main():
                      "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
         "cpu_baseline": cpu,
         "table2_pow2_d": table2,
+        "w4a4_gemm": gemm,
     }
     print(json.dumps(line), flush=True)
 
@@ -351,6 +354,39 @@ def table2_shapes(kq, synth, dev, stream, sptr, steps=500, warmup=3):
         del Xs, Cs, Ss, X0
         torch.cuda.empty_cache()
     out["timing"] = "HIP graph of 500 launches per kernel, replayed; MALL-cold rotation"
+    return out
+
+
+FP4_PEAK_TFLOPS = 10100.0  # MI355X dense MXFP4 matrix-core peak, TFLOP/s
+
+
+def gemm_timing(kq, synth, dev, stream, sptr, xc, xs, M, K, steps=100):
+    """The W4A4 product that consumes the quantizer output (kq_mxfp4_gemm):
+    the headline activation's MXFP4 codes times an MXFP4 weight from
+    kq_weight_transform (synthetic weights, N = 3072 and 12288), fp32 output."""
+    import torch
+    out = {}
+    A, B = synth.factors(4, 8, 1, seed=5)
+    for N in (3072, 12288):
+        W = synth.activations(N, K, "normal", seed=N, chan_frac=0.0)
+        Wd = torch.from_numpy(W.view(np.int16)).view(torch.bfloat16).to(dev)
+        _, wc, ws = kq.weight_transform(Wd, torch.from_numpy(A), torch.from_numpy(B))
+        C = torch.empty((M, N), dtype=torch.float32, device=dev)
+        for _ in range(10):
+            kq.mxfp4_gemm(xc, xs, wc, ws, C=C, stream=sptr)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            kq.mxfp4_gemm(xc, xs, wc, ws, C=C, stream=sptr)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / steps * 1e3
+        tf = 2.0 * M * N * K / us * 1e-6
+        out[f"{M}x{N}x{K}"] = {"us": round(us, 2), "tflops": round(tf, 1),
+                                "frac_fp4_peak": round(tf / FP4_PEAK_TFLOPS, 4)}
+        del W, Wd, wc, ws, C
+    out["peak_tflops"] = FP4_PEAK_TFLOPS
     return out
 
 

@@ -27,9 +27,13 @@
  *    caller's next synchronization, as for any HIP launch.
  *  - Alignment: X, codes and y_out must be 16-byte aligned; scales need no
  *    alignment; the factors need 4 B and the SmoothQuant multipliers 16 B.
- *  - Environment: KQ_MAX_WAVES (cap on workgroups) and KQ_UNITS_PER_WAVE
- *    (1 or 2) set the launch shape of the matrix-core kernel; read once,
- *    tuning knobs that never change results.
+ *  - Environment (read once; tuning knobs that never change results):
+ *    KQ_MAX_WAVES (cap on workgroups) and KQ_UNITS_PER_WAVE (1 or 2) set the
+ *    launch shape of the on-the-fly matrix-core kernel; KQ_PACKED_PERSISTENT,
+ *    KQ_SMOOTH_PATH and KQ_SMOOTH_WAVES select alternative kernel shapes of
+ *    kq_quantize_packed and kq_smoothquant_quantize; KQ_GEMM_TILE_M (2 or 4)
+ *    selects the register-staged kq_mxfp4_gemm kernel instead of the
+ *    LDS-pipelined one.
  *  - Inputs must be finite; NaN or Inf inputs give unspecified codes.
  *  - Arguments are validated before any HIP call.  On failure the call
  *    returns the status and kq_last_error_detail() describes the argument

@@ -309,6 +309,16 @@ kq_status kq_mxfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, int64_t
     g.C = C;
     g.ldc_out = ldc;
     g.accumulate = accumulate;
+    g.vec_ok = aligned(C, 16) && ldc % 4 == 0;
+    g.scales_aligned = aligned(a_scales, 4) && aligned(b_scales, 4);
+    // KQ_GEMM_TILE_M (optional, read once): 0 = LDS-pipelined kernel (default), 2 or 4 = register-staged
+    // kernel with that many instruction tiles per wave along M (tuning only)
+    static const int tile_m = [] {
+        const char* e = std::getenv("KQ_GEMM_TILE_M");
+        const int v = e ? std::atoi(e) : 0;
+        return (v == 2 || v == 4) ? v : 0;
+    }();
+    g.tile_m = tile_m;
     return from_hip(kq::launch_mxfp4_gemm(g, (hipStream_t)stream), "kq_mxfp4_gemm");
 }
 

@@ -116,9 +116,351 @@ __global__ __launch_bounds__(256) void mxfp4_gemm_kernel(const GemmParams g) {
         }
 }
 
+// Tiled variant for K a multiple of 128 (the usual case; the kernel above
+// takes any K).  The matrix-core rows are the weights (N) and its columns the
+// activations (M), so each lane ends with four consecutive C columns of one C
+// row per accumulator row-group: 16-byte stores.  Workgroup tile 128 (N) x 256
+// (M), waves 2 x 2 of 64 x 128 (2 x 4 instruction tiles, eight accumulators).
+// K advances 128 at a time (four blocks, two instruction steps): the next
+// stage's codes are loaded into registers while the current stage is
+// multiplied out of LDS, then written to the other LDS buffer (one barrier
+// per stage).  LDS holds each operand block-major, [step][half][row][16 B],
+// so a wave's fragment read is 64 consecutive 16-byte slots.  A lane's scale
+// bytes for a stage are one aligned dword per row (four blocks), rearranged
+// with v_perm so that byte s is block 2 s + (lane / 32): the instruction's
+// opsel then picks step s.
+constexpr int kGemmTileN = 128, kGemmTileK = 128;
+
+// Staging of one stage: chunk c = row * 4 + block; W 512 chunks (2 per
+// thread), X 1024 (4 per thread).
+template <int TM>
+struct Stage {
+    uint4 w[2], x[TM];
+};
+
+template <int TM>
+__device__ __forceinline__ void load_stage(const GemmParams& g, int t, int64_t nb0, int64_t mb0, int64_t row_bytes,
+                                           int64_t st, Stage<TM>& sg) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int c = t + 256 * i;
+        const int64_t n = nb0 + (c >> 2);
+        sg.w[i] = make_uint4(0u, 0u, 0u, 0u);
+        if (n < g.N) sg.w[i] = *reinterpret_cast<const uint4*>(g.b_codes + n * row_bytes + (4 * st + (c & 3)) * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        const int c = t + 256 * i;
+        const int64_t m = mb0 + (c >> 2);
+        sg.x[i] = make_uint4(0u, 0u, 0u, 0u);
+        if (m < g.M) sg.x[i] = *reinterpret_cast<const uint4*>(g.a_codes + m * row_bytes + (4 * st + (c & 3)) * 16);
+    }
+}
+
+template <int TM>
+__device__ __forceinline__ void store_stage(uint4* lw, uint4* lx, int t, const Stage<TM>& sg) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int c = t + 256 * i;
+        lw[(c & 3) * kGemmTileN + (c >> 2)] = sg.w[i];  // block b = 2 step + half
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        const int c = t + 256 * i;
+        lx[(c & 3) * (64 * TM) + (c >> 2)] = sg.x[i];
+    }
+}
+
+// A lane's scale bytes of one stage for one row: byte s = block 2 s + half.
+__device__ __forceinline__ uint32_t stage_scales(const uint8_t* sc, int64_t row, int64_t nrows, int64_t nkb, int64_t st,
+                                                 uint32_t psel) {
+    uint32_t w = 0x7F7F7F7Fu;
+    if (row < nrows) w = *reinterpret_cast<const uint32_t*>(sc + row * nkb + 4 * st);
+    return __builtin_amdgcn_perm(0u, w, psel);
+}
+
+template <int STEP, int TM>
+__device__ __forceinline__ void stage_step(const uint4* lw, const uint4* lx, int h, int wn, int wm, int r,
+                                           const uint32_t (&scw)[2], const uint32_t (&scx)[TM], f32x16g (&acc)[2][TM]) {
+    uint4 fw[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) fw[i] = lw[(2 * STEP + h) * kGemmTileN + wn * 64 + 32 * i + r];
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+        const uint4 fx = lx[(2 * STEP + h) * (64 * TM) + wm * (32 * TM) + 32 * j + r];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                operand(Frag{fw[i], 0u}), operand(Frag{fx, 0u}), acc[i][j], 4, 4, STEP, (int)scw[i], STEP, (int)scx[j]);
+    }
+}
+
+template <int TM>
+__global__ __launch_bounds__(256) void mxfp4_gemm_tiled_kernel(const GemmParams g) {
+    constexpr int kTileM = 64 * TM;  // two waves of TM instruction tiles along M
+    __shared__ uint4 lds_w[2][4 * kGemmTileN];
+    __shared__ uint4 lds_x[2][4 * kTileM];
+    const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+    const int r = lane & 31, h = lane >> 5;
+    const int wn = wave >> 1, wm = wave & 1;
+    const int64_t nb0 = (int64_t)blockIdx.x * kGemmTileN, mb0 = (int64_t)blockIdx.y * kTileM;
+    const int64_t nkb = g.K / 32, row_bytes = g.K / 2, nst = g.K / kGemmTileK;
+    const uint32_t psel = h ? 0x0c0c0301u : 0x0c0c0200u;
+    uint32_t scw[2], scx[TM];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) scw[i] = stage_scales(g.b_scales, nb0 + wn * 64 + 32 * i + r, g.N, nkb, 0, psel);
+#pragma unroll
+    for (int j = 0; j < TM; ++j) scx[j] = stage_scales(g.a_scales, mb0 + wm * (32 * TM) + 32 * j + r, g.M, nkb, 0, psel);
+    f32x16g acc[2][TM];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < TM; ++j) acc[i][j] = f32x16g{};
+    Stage<TM> sg;
+    load_stage(g, t, nb0, mb0, row_bytes, 0, sg);
+    store_stage(lds_w[0], lds_x[0], t, sg);
+    __syncthreads();
+    for (int64_t st = 0; st < nst; ++st) {
+        const int buf = (int)(st & 1);
+        const bool more = st + 1 < nst;
+        uint32_t nscw[2], nscx[TM];
+        if (more) {
+            load_stage(g, t, nb0, mb0, row_bytes, st + 1, sg);
+#pragma unroll
+            for (int i = 0; i < 2; ++i) nscw[i] = stage_scales(g.b_scales, nb0 + wn * 64 + 32 * i + r, g.N, nkb, st + 1, psel);
+#pragma unroll
+            for (int j = 0; j < TM; ++j) nscx[j] = stage_scales(g.a_scales, mb0 + wm * (32 * TM) + 32 * j + r, g.M, nkb, st + 1, psel);
+        }
+        stage_step<0, TM>(lds_w[buf], lds_x[buf], h, wn, wm, r, scw, scx, acc);
+        stage_step<1, TM>(lds_w[buf], lds_x[buf], h, wn, wm, r, scw, scx, acc);
+        if (more) {
+            store_stage(lds_w[buf ^ 1], lds_x[buf ^ 1], t, sg);
+#pragma unroll
+            for (int i = 0; i < 2; ++i) scw[i] = nscw[i];
+#pragma unroll
+            for (int j = 0; j < TM; ++j) scx[j] = nscx[j];
+        }
+        __syncthreads();
+    }
+    // acc[i][j][4q + e] = C[mb0 + wm 32 TM + 32 j + r][nb0 + wn 64 + 32 i + 8 q + 4 h + e]
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+        const int64_t m = mb0 + wm * (32 * TM) + 32 * j + r;
+        if (m >= g.M) continue;
+        float* crow = g.C + m * g.ldc_out;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int64_t n = nb0 + wn * 64 + 32 * i + 8 * q + 4 * h;
+                float4 v = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+                if (g.vec_ok && n + 3 < g.N) {
+                    float4* dst = reinterpret_cast<float4*>(crow + n);
+                    if (g.accumulate) {
+                        const float4 o = *dst;
+                        v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
+                    }
+                    *dst = v;
+                } else {
+                    if (n + 0 < g.N) crow[n + 0] = g.accumulate ? crow[n + 0] + v.x : v.x;
+                    if (n + 1 < g.N) crow[n + 1] = g.accumulate ? crow[n + 1] + v.y : v.y;
+                    if (n + 2 < g.N) crow[n + 2] = g.accumulate ? crow[n + 2] + v.z : v.z;
+                    if (n + 3 < g.N) crow[n + 3] = g.accumulate ? crow[n + 3] + v.w : v.w;
+                }
+            }
+    }
+}
+
+// Pipelined variant (K a multiple of 128, 4-byte-aligned scales): workgroup
+// tile 128 (N) x 128 (M), waves 2 x 2 of 64 x 64, K 128 per stage.  Codes and
+// scales go from global memory straight into LDS (global_load_lds: lane l's
+// 16 or 4 bytes land at the wave-uniform LDS address + 16 l or 4 l) with
+// kGemmStages stages in flight, so no register staging and no ds_write.
+// Per stage the workgroup issues 20 such loads, 5 per wave:
+//   W and X codes of rows 32 w .. 32 w + 31 (two loads each, 16 rows x 64 B), and
+//   one scale group: wave 0 W rows 0-63, 1 W rows 64-127, 2 X rows 0-63, 3 X rows 64-127;
+// rows past N or M load row N-1 or M-1 (their products land in C rows or
+// columns that are never stored).  Before a stage is used each wave waits
+// until only its later stages' loads are outstanding, then one barrier.
+constexpr int kGemmStages = 3;
+constexpr int kPipeLoadsPerWave = 5;
+
+struct PipeBuf {
+    uint4 wc[4 * 128];   // 128 rows x 4 blocks of 16 B, slot pipe_slot(row, block)
+    uint4 xc[4 * 128];
+    uint32_t ws[128];    // scales of the stage's 4 blocks, one dword per row
+    uint32_t xs[128];
+};
+
+__device__ __forceinline__ void lds_load16(const uint8_t* src, void* lds_base) {
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                     (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+__device__ __forceinline__ void lds_load4(const uint8_t* src, void* lds_base) {
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                     (__attribute__((address_space(3))) void*)lds_base, 4, 0, 0);
+}
+
+// LDS slot of block b of tile row q: 4 q + (b ^ ((q >> 2) & 3)).  A DMA
+// instruction fills 64 consecutive slots (16 rows), so lane l reads row
+// 16 i + l / 4, block (l % 4) ^ (((l / 4) >> 2) & 3): each instruction reads
+// 16 contiguous 64-byte row segments, and a fragment read (32 rows, one
+// block) spreads over all LDS banks.
+__device__ __forceinline__ int pipe_slot(int q, int b) { return 4 * q + (b ^ ((q >> 2) & 3)); }
+
+__device__ __forceinline__ void pipe_issue(const GemmParams& g, PipeBuf& b, int wave, int lane, int64_t nb0,
+                                           int64_t mb0, int64_t row_bytes, int64_t nkb, int64_t st) {
+    const int q = lane >> 2;                                  // row within the instruction's 16
+    const int blk = (lane & 3) ^ ((q >> 2) & 3);
+    const int64_t kbyte = (4 * st + blk) * 16;
+#pragma unroll
+    for (int gr = 0; gr < 2; ++gr) {
+        const int row = 16 * (2 * wave + gr) + q;             // this wave fills rows 32 w .. 32 w + 31
+        const int64_t n = min(nb0 + row, g.N - 1);
+        const int64_t m = min(mb0 + row, g.M - 1);
+        lds_load16(g.b_codes + n * row_bytes + kbyte, &b.wc[64 * (2 * wave + gr)]);
+        lds_load16(g.a_codes + m * row_bytes + kbyte, &b.xc[64 * (2 * wave + gr)]);
+    }
+    const int gr = wave & 1;
+    if (wave < 2) {
+        const int64_t n = min(nb0 + 64 * gr + lane, g.N - 1);
+        lds_load4(g.b_scales + n * nkb + 4 * st, &b.ws[64 * gr]);
+    } else {
+        const int64_t m = min(mb0 + 64 * gr + lane, g.M - 1);
+        lds_load4(g.a_scales + m * nkb + 4 * st, &b.xs[64 * gr]);
+    }
+}
+
+template <int STEP>
+__device__ __forceinline__ void pipe_step(const PipeBuf& b, int h, int wn, int wm, int r, const uint32_t (&scw)[2],
+                                          const uint32_t (&scx)[2], f32x16g (&acc)[2][2]) {
+    uint4 fw[2], fx[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) fw[i] = b.wc[pipe_slot(wn * 64 + 32 * i + r, 2 * STEP + h)];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) fx[j] = b.xc[pipe_slot(wm * 64 + 32 * j + r, 2 * STEP + h)];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                operand(Frag{fw[i], 0u}), operand(Frag{fx[j], 0u}), acc[i][j], 4, 4, STEP, (int)scw[i], STEP, (int)scx[j]);
+}
+
+// The three stage buffers are distinct LDS objects, and the main loop is
+// unrolled by three so that every access names its buffer at compile time:
+// the waits the compiler adds before LDS reads then cover only loads into
+// that buffer, and the barrier between stages is a bare s_barrier after an
+// explicit vmcnt wait (a fenced barrier would drain the loads in flight for
+// the later stages).
+__shared__ PipeBuf g_pipe0, g_pipe1, g_pipe2;
+
+template <int B>
+__device__ __forceinline__ PipeBuf& pipe_buf() {
+    if constexpr (B == 0) return g_pipe0;
+    else if constexpr (B == 1) return g_pipe1;
+    else return g_pipe2;
+}
+
+struct PipeCtx {
+    int wave, lane, r, h, wn, wm;
+    int64_t nb0, mb0, nkb, row_bytes, nst;
+    uint32_t psel;
+};
+
+// stage st lives in buffer CUR = st % 3; stage st + 2 is issued into NXT = (st + 2) % 3
+template <int CUR, int NXT>
+__device__ __forceinline__ void pipe_iter(const GemmParams& g, const PipeCtx& c, int64_t st, f32x16g (&acc)[2][2]) {
+    if (st + 1 < c.nst)
+        __builtin_amdgcn_s_waitcnt((kPipeLoadsPerWave & 15) | (7 << 4) | (15 << 8));  // vmcnt(5)
+    else
+        __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    if (st + 2 < c.nst) pipe_issue(g, pipe_buf<NXT>(), c.wave, c.lane, c.nb0, c.mb0, c.row_bytes, c.nkb, st + 2);
+    const PipeBuf& b = pipe_buf<CUR>();
+    uint32_t scw[2], scx[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) scw[i] = __builtin_amdgcn_perm(0u, b.ws[c.wn * 64 + 32 * i + c.r], c.psel);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) scx[j] = __builtin_amdgcn_perm(0u, b.xs[c.wm * 64 + 32 * j + c.r], c.psel);
+    pipe_step<0>(b, c.h, c.wn, c.wm, c.r, scw, scx, acc);
+    pipe_step<1>(b, c.h, c.wn, c.wm, c.r, scw, scx, acc);
+}
+
+__global__ __launch_bounds__(256) void mxfp4_gemm_pipe_kernel(const GemmParams g) {
+    PipeCtx c;
+    const int t = threadIdx.x;
+    c.wave = t >> 6;
+    c.lane = t & 63;
+    c.r = c.lane & 31;
+    c.h = c.lane >> 5;
+    c.wn = c.wave >> 1;
+    c.wm = c.wave & 1;
+    c.nb0 = (int64_t)blockIdx.x * 128;
+    c.mb0 = (int64_t)blockIdx.y * 128;
+    c.nkb = g.K / 32;
+    c.row_bytes = g.K / 2;
+    c.nst = g.K / 128;
+    c.psel = c.h ? 0x0c0c0301u : 0x0c0c0200u;
+    f32x16g acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16g{};
+    pipe_issue(g, g_pipe0, c.wave, c.lane, c.nb0, c.mb0, c.row_bytes, c.nkb, 0);
+    if (c.nst > 1) pipe_issue(g, g_pipe1, c.wave, c.lane, c.nb0, c.mb0, c.row_bytes, c.nkb, 1);
+    for (int64_t st = 0; st < c.nst; st += 3) {
+        pipe_iter<0, 2>(g, c, st, acc);
+        if (st + 1 < c.nst) pipe_iter<1, 0>(g, c, st + 1, acc);
+        if (st + 2 < c.nst) pipe_iter<2, 1>(g, c, st + 2, acc);
+    }
+    const int r = c.r, h = c.h, wn = c.wn, wm = c.wm;
+    const int64_t nb0 = c.nb0, mb0 = c.mb0;
+    // acc[i][j][4q + e] = C[mb0 + wm 64 + 32 j + r][nb0 + wn 64 + 32 i + 8 q + 4 h + e]
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int64_t m = mb0 + wm * 64 + 32 * j + r;
+        if (m >= g.M) continue;
+        float* crow = g.C + m * g.ldc_out;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int64_t n = nb0 + wn * 64 + 32 * i + 8 * q + 4 * h;
+                float4 v = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+                if (g.vec_ok && n + 3 < g.N) {
+                    float4* dst = reinterpret_cast<float4*>(crow + n);
+                    if (g.accumulate) {
+                        const float4 o = *dst;
+                        v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
+                    }
+                    *dst = v;
+                } else {
+                    if (n + 0 < g.N) crow[n + 0] = g.accumulate ? crow[n + 0] + v.x : v.x;
+                    if (n + 1 < g.N) crow[n + 1] = g.accumulate ? crow[n + 1] + v.y : v.y;
+                    if (n + 2 < g.N) crow[n + 2] = g.accumulate ? crow[n + 2] + v.z : v.z;
+                    if (n + 3 < g.N) crow[n + 3] = g.accumulate ? crow[n + 3] + v.w : v.w;
+                }
+            }
+    }
+}
+
 hipError_t launch_mxfp4_gemm(const GemmParams& g, hipStream_t st) {
-    const dim3 grid((unsigned)((g.N + 127) / 128), (unsigned)((g.M + 127) / 128));
-    hipLaunchKernelGGL(mxfp4_gemm_kernel, grid, dim3(256), 0, st, g);
+    if (g.K % kGemmTileK == 0 && g.scales_aligned && g.tile_m == 0) {
+        const dim3 grid((unsigned)((g.N + 127) / 128), (unsigned)((g.M + 127) / 128));
+        hipLaunchKernelGGL(mxfp4_gemm_pipe_kernel, grid, dim3(256), 0, st, g);
+    } else if (g.K % kGemmTileK == 0 && g.scales_aligned) {
+        if (g.tile_m == 4) {
+            const dim3 grid((unsigned)((g.N + kGemmTileN - 1) / kGemmTileN), (unsigned)((g.M + 255) / 256));
+            hipLaunchKernelGGL(mxfp4_gemm_tiled_kernel<4>, grid, dim3(256), 0, st, g);
+        } else {
+            const dim3 grid((unsigned)((g.N + kGemmTileN - 1) / kGemmTileN), (unsigned)((g.M + 127) / 128));
+            hipLaunchKernelGGL(mxfp4_gemm_tiled_kernel<2>, grid, dim3(256), 0, st, g);
+        }
+    } else {
+        const dim3 grid((unsigned)((g.N + 127) / 128), (unsigned)((g.M + 127) / 128));
+        hipLaunchKernelGGL(mxfp4_gemm_kernel, grid, dim3(256), 0, st, g);
+    }
     return hipGetLastError();
 }
 

@@ -53,6 +53,9 @@ struct GemmParams {
     float* C;                 // [M, ldc_out]
     int64_t ldc_out;
     int accumulate;           // 1: C += product, 0: C = product
+    int vec_ok;               // C 16-byte aligned and ldc_out a multiple of 4
+    int scales_aligned;       // both scale arrays 4-byte aligned
+    int tile_m = 2;           // instruction tiles per wave along M in the tiled kernel (2 or 4)
 };
 
 hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg);

@@ -446,7 +446,8 @@ def _gemm_tolerance(ac, as_, bc, bs):
     return K * 2.0 ** -24 * (np.abs(oracle.dequantize(ac, as_)) @ np.abs(oracle.dequantize(bc, bs)).T)
 
 
-@pytest.mark.parametrize("M,N,K", [(77, 200, 2240), (128, 128, 64), (33, 70, 1120), (300, 257, 3072), (1, 1, 32)])
+@pytest.mark.parametrize("M,N,K", [(77, 200, 2240), (128, 128, 64), (33, 70, 1120), (300, 257, 3072), (1, 1, 32),
+                                   (5, 3, 128), (64, 130, 256), (130, 64, 384), (200, 200, 512), (129, 127, 1280)])
 def test_mxfp4_gemm_parity(M, N, K):
     """C = deq(A) deq(B)^T on the matrix cores against the oracle's fp64
     product, within the fp32 accumulation bound; ragged tiles, odd block
