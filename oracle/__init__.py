@@ -59,13 +59,14 @@ def _lib():
     lib.kqo_e2m1_codes.argtypes = [P, I64, I, P]
     lib.kqo_e8m0_scales.argtypes = [P, I64, P]
     lib.kqo_lu_factors.argtypes = [P, I, I64, P, P]
+    lib.kqo_lu_inverse_factors.argtypes = [P, I, I64, P, P]
     lib.kqo_fwht.argtypes = [P, I64, I64, P, P, P]
     lib.kqo_f32_to_bf16.argtypes = [P, I64, P]
     lib.kqo_num_threads.argtypes = []
     lib.kqo_set_num_threads.argtypes = [I]
     for name in ("kqo_quantize", "kqo_quantize_f32", "kqo_smoothquant", "kqo_hadamard32",
                  "kqo_mxfp4", "kqo_e2m1_codes", "kqo_e8m0_scales", "kqo_num_threads", "kqo_lu_factors",
-                 "kqo_f32_to_bf16", "kqo_fwht"):
+                 "kqo_lu_inverse_factors", "kqo_f32_to_bf16", "kqo_fwht"):
         getattr(lib, name).restype = ctypes.c_int
     lib.kqo_set_num_threads.restype = None
     return lib
@@ -142,6 +143,20 @@ def lu_factors_f32(lu, a):
     A = np.empty((nfac, a, a), dtype=np.float32)
     B = np.empty((nfac, b, b), dtype=np.float32)
     _check(_lib().kqo_lu_factors(_ptr(lu), a, nfac, _ptr(A), _ptr(B)), "lu_factors_f32")
+    return A, B
+
+
+def lu_inverse_factors_f32(lu, a):
+    """Weight-side factors for the same parameters: A' (x) B' = K^-1 with the
+    closed-form inverse of every unit-determinant factor, G^-1 = [[-g11, g01],
+    [g10, -g00]] (Sec. 3.2), fp32 products left to right (kq_oracle.c,
+    kqo_lu_inverse_factors).  quantize(W, A', B') is then Q(W T^-T) (Sec. 3.4)."""
+    lu = np.ascontiguousarray(lu, dtype=np.float32).reshape(-1, 5, 3)
+    nfac = lu.shape[0]
+    b = 32 // a
+    A = np.empty((nfac, a, a), dtype=np.float32)
+    B = np.empty((nfac, b, b), dtype=np.float32)
+    _check(_lib().kqo_lu_inverse_factors(_ptr(lu), a, nfac, _ptr(A), _ptr(B)), "lu_inverse_factors_f32")
     return A, B
 
 

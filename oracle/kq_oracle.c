@@ -340,6 +340,38 @@ int kqo_lu_factors(const float* lu, int a, int64_t nfac, float* A, float* B) {
     return 0;
 }
 
+/* Weight-side factors for the same parameters (Sec. 3.2, Sec. 3.4): the
+ * weight is multiplied by T^-T, i.e. every block row w^T becomes w^T K^-T, so
+ * as a column map w -> K^-1 w with K^-1 = G1^-1 (x) ... (x) G5^-1 (the inverse
+ * of a Kronecker product is the product of the inverses).  A unit-determinant
+ * factor has det G = -1, so G^-1 = -adj(G) = [[-g11, g01], [g10, -g00]].
+ * Writes A' (x) B' = K^-1: A'[o][p] = prod over the first na factors of
+ * G_k^-1[bit of o][bit of p], B' likewise over the rest, fp32 products left to
+ * right from the fp32 g entries of kqo_lu_factors. */
+int kqo_lu_inverse_factors(const float* lu, int a, int64_t nfac, float* A, float* B) {
+    int na = a == 1 ? 0 : a == 2 ? 1 : a == 4 ? 2 : a == 8 ? 3 : -1;
+    if (na < 0 || nfac < 1) return -3;
+    if (!lu || !A || !B) return -2;
+    int b = BLK / a;
+    for (int64_t f = 0; f < nfac; ++f) {
+        float gi[5 * 4];
+        for (int k = 0; k < 5; ++k) {
+            float pa = lu[f * 15 + 3 * k], pb = lu[f * 15 + 3 * k + 1], pc = lu[f * 15 + 3 * k + 2];
+            if (pa == 0.0f) return -5;
+            float g00 = pa, g01 = pb, g10 = pc * pa, g11 = fmaf(pc, pb, -(1.0f / pa));
+            gi[k * 4 + 0] = -g11;
+            gi[k * 4 + 1] = g01;
+            gi[k * 4 + 2] = g10;
+            gi[k * 4 + 3] = -g00;
+        }
+        for (int o = 0; o < a; ++o)
+            for (int p = 0; p < a; ++p) A[f * a * a + o * a + p] = lu_entry(gi, 0, na, na - 1, o, p);
+        for (int i = 0; i < b; ++i)
+            for (int q = 0; q < b; ++q) B[f * b * b + i * b + q] = lu_entry(gi, na, 5, 4 - na, i, q);
+    }
+    return 0;
+}
+
 /* fp32 -> bf16, round to nearest, ties to the even bf16 (the 16-bit output of
  * the transformed activation): the two bf16 neighbours of v are its 16-bit
  * truncation toward zero and the next one away from zero; the nearer one

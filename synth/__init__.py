@@ -121,6 +121,31 @@ def lu_params(nfac=1, seed=0):
     return lu
 
 
+def weights(o, d, seed=0, chan_frac=0.01, chan_factor=4.0):
+    """bf16 weight matrix [o, d] of a linear layer: N(0, 1/d) entries (the
+    usual initialisation scale), with round(chan_frac * d) input channels
+    scaled by chan_factor so that the weight side has outlier columns too."""
+    rv, rc = (np.random.default_rng(s) for s in np.random.SeedSequence(seed).spawn(2))
+    w = (rv.standard_normal((o, d)) / np.sqrt(d)).astype(np.float32)
+    n_ch = int(round(chan_frac * d))
+    if n_ch > 0:
+        ch = rc.choice(d, size=n_ch, replace=False)
+        w[:, ch] *= np.float32(chan_factor)
+    return to_bf16_bits(w)
+
+
+def calib_layer(R, o, d, seed=0, dist="student_t3", chan_frac=0.005, chan_factor=50.0):
+    """A synthetic layer for the calibration of Sec. 3.3: calibration
+    activations X [R, d] (R = samples x tokens, the FLUX recipe of
+    ``activations``: Student-t(3) values and 0.5% outlier channels x50) and a
+    weight W [o, d] (``weights``).  Returns (X, W) as bf16 bit patterns."""
+    ss = np.random.SeedSequence([seed, 7]).spawn(2)
+    X = activations(R, d, dist, chan_frac=chan_frac, chan_factor=chan_factor,
+                    seeds=np.random.SeedSequence(ss[0].entropy).spawn(4))
+    W = weights(o, d, seed=int(ss[1].generate_state(1)[0]))
+    return X, W
+
+
 def smoothquant_multipliers(X_bits: np.ndarray) -> np.ndarray:
     """Per-channel multipliers m_c = 1 / s_c with s_c = max_r |X[r, c]|^0.5
     (migration strength alpha = 0.5, beta = 0), computed in fp64 and rounded
