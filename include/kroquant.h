@@ -263,6 +263,84 @@ kq_status kq_factors_inverse_transpose(const float* A, const float* B, int a, in
  */
 kq_status kq_lu_to_factors(const float* abc, int a, int64_t nfac, float* A, float* B);
 
+/*
+ * Layer-wise calibration of the block transform (Sec. 3.3), on device.
+ *
+ * For the activations X [R, d] of one layer (R = N m rows: N calibration
+ * samples of m tokens, stacked) and its weight W [o, d], both bf16 row-major,
+ * and the transform T = diag(T_f), T_f = G_1 (x) ... (x) G_5 with the LU
+ * parameters lu [nfac, 5, 3] of kq_quantize_lu (nfac = 1: one T_f for every
+ * 32-column block; nfac = d / 32: one per block), the objective is
+ *     L_out = || Q(X T) Q(W T^-T)^T - X W^T ||_F^2 / (R o)
+ *     L_A   = || Q(X T) - X T ||_F^2 / (R d)
+ *     L_W   = || Q(W T^-T) - W T^-T ||_F^2 / (o d)
+ *     L     = L_out + lambda_A L_A + lambda_W L_W
+ * with Q the MXFP4 quantizer of this library (Sec. 3.1).  Q(X T) is
+ * kq_quantize_lu; W T^-T applies T_f^-1 = G_1^-1 (x) ... (x) G_5^-1 with the
+ * closed-form inverse of a unit-determinant factor, G^-1 = [[-g11, g01],
+ * [g10, -g00]] (det G = -1, Sec. 3.2), each entry of the two Kronecker
+ * factors a left-to-right fp32 product of those entries, then kq_quantize;
+ * the product is kq_mxfp4_gemm.
+ * The gradient uses a straight-through estimator: the E2M1 rounding passes
+ * the gradient unchanged, the E8M0 scale is held fixed, and an element with
+ * |v| > 6 * scale (clipped) passes none.  Products and sums of the backward
+ * pass run in fp32 on the matrix cores; the loss sums in fp64.
+ *
+ * kq_calib_workspace_size -- bytes of device workspace that kq_calib_step and
+ * kq_calibrate need for these sizes (about 4 R d + 4 R o + 4 o d bytes plus
+ * per-workgroup partial sums).  Same size checks as kq_calib_step.
+ */
+kq_status kq_calib_workspace_size(int64_t R, int64_t o, int64_t d, int a, int64_t nfac, size_t* bytes);
+
+/*
+ * kq_calib_reference -- Yneg = -(X W^T), fp32 [R, o] row-major (products of
+ * bf16 values exact, fp32 accumulation on the matrix cores): the fixed
+ * reference of L_out, computed once per layer.  X, W device, 16-byte aligned;
+ * R, o >= 1, at most 65535 * 128; d a positive multiple of 32.
+ */
+kq_status kq_calib_reference(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o, float* Yneg,
+                             void* stream);
+
+/*
+ * kq_calib_step -- one evaluation of the objective and its gradient at the
+ * parameters lu, optionally followed by one Adam update of lu in place.
+ *   Yneg      from kq_calib_reference (device fp32 [R, o], 16-byte aligned)
+ *   lambdas   device fp32 [2] = (lambda_A, lambda_W)
+ *   grad      device fp32 [nfac, 5, 3]: dL/d(a_k, b_k, c_k)
+ *   losses    device fp64 [4]: L_out, L_A, L_W, L at lu (before any update)
+ *   adam_t    0: no update; t >= 1: Adam step t (Kingma and Ba; beta1 0.9,
+ *             beta2 0.999, eps 1e-8, learning rate lr) with the moment
+ *             buffers adam_m, adam_v (device fp32 [nfac * 15], zero before
+ *             step 1)
+ *   workspace device, 256-byte aligned, >= kq_calib_workspace_size bytes;
+ *             its contents are scratch between calls.
+ * Enqueued on `stream`; no allocation, no synchronization.  Errors as for
+ * kq_quantize_lu and kq_mxfp4_gemm, plus KQ_ERROR_INVALID_VALUE for a short
+ * workspace.
+ */
+kq_status kq_calib_step(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o, const float* Yneg,
+                        float* lu, int a, int64_t nfac, const float* lambdas, float* grad, double* losses,
+                        float* adam_m, float* adam_v, int adam_t, float lr, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/*
+ * kq_calibrate -- the per-layer optimisation of Sec. 3.3 in one call:
+ *   1. evaluate the objective at the given lu (the initial transform T_0,
+ *      normally the Hadamard initialisation a = b = 1/sqrt(2), c = 1) with
+ *      lambda = 0, and set lambda_A = L_out(T_0) / L_A(T_0),
+ *      lambda_W = L_out(T_0) / L_W(T_0) (0 where the denominator is 0);
+ *   2. `steps` Adam steps of learning rate lr on L, updating lu in place;
+ *   3. evaluate the objective at the final lu.
+ * losses: device fp64 [(steps + 2), 4], 8-byte aligned; row 0 is step 1's
+ * evaluation (lambda = 0), row t the evaluation before update t, row
+ * steps + 1 the final one (each row L_out, L_A, L_W, L).  The Adam moments,
+ * lambdas and gradient live in the workspace.  Enqueued on `stream`; no
+ * allocation, no synchronization.
+ */
+kq_status kq_calibrate(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o, const float* Yneg,
+                       float* lu, int a, int64_t nfac, int steps, float lr, double* losses, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
 /* Stable name of a status ("KQ_SUCCESS", ...). Never NULL. */
 const char* kq_status_string(kq_status s);
 

@@ -8,7 +8,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libkroquant.so")
-SOURCES = ["kq_kernels.hip", "kq_gemm.hip", "kq_api.hip"]
+SOURCES = ["kq_kernels.hip", "kq_gemm.hip", "kq_calib.hip", "kq_api.hip"]
 
 # -packed-fp32-ops off: no v_pk_{add,mul,fma}_f32 in the device code.
 # -ffp-contract=off: only the explicit fmaf calls fuse, which keeps the

@@ -23,6 +23,7 @@ EXPORTED = (
     "kq_quantize", "kq_quantize_exact", "kq_quantize_packed", "kq_pack_factors", "kq_quantize_lu",
     "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_fwht_quantize", "kq_mxfp4_quantize", "kq_mxfp4_gemm",
     "kq_e2m1_encode", "kq_weight_transform", "kq_factors_inverse_transpose", "kq_lu_to_factors",
+    "kq_calib_workspace_size", "kq_calib_reference", "kq_calib_step", "kq_calibrate",
     "kq_status_string", "kq_last_error_detail", "kq_version",
 )
 
@@ -57,7 +58,11 @@ def lib() -> ctypes.CDLL:
     L.kq_weight_transform.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P]
     L.kq_factors_inverse_transpose.argtypes = [P, P, I, I, I64, P, P]
     L.kq_lu_to_factors.argtypes = [P, I, I64, P, P]
-    for name in EXPORTED[:14]:
+    L.kq_calib_workspace_size.argtypes = [I64, I64, I64, I, I64, ctypes.POINTER(ctypes.c_size_t)]
+    L.kq_calib_reference.argtypes = [P, I64, I64, P, I64, P, P]
+    L.kq_calib_step.argtypes = [P, I64, I64, P, I64, P, P, I, I64, P, P, P, P, P, I, F, P, ctypes.c_size_t, P]
+    L.kq_calibrate.argtypes = [P, I64, I64, P, I64, P, P, I, I64, I, F, P, P, ctypes.c_size_t, P]
+    for name in EXPORTED[:18]:
         getattr(L, name).restype = ctypes.c_int
     L.kq_status_string.argtypes = [I]
     L.kq_status_string.restype = ctypes.c_char_p
@@ -65,7 +70,6 @@ def lib() -> ctypes.CDLL:
     L.kq_last_error_detail.restype = ctypes.c_char_p
     L.kq_version.argtypes = []
     L.kq_version.restype = ctypes.c_int
-    del F
     return L
 
 
@@ -307,3 +311,89 @@ def status_string(status: int) -> str:
 
 def version() -> int:
     return int(lib().kq_version())
+
+
+# ------------------------------------------------------------ calibration
+
+def hadamard_lu(nfac, device="cuda"):
+    """LU parameters of the Hadamard initialisation (Sec. 3.2): a = b = 1/sqrt(2),
+    c = 1 for every factor; fp32 [nfac, 5, 3] on ``device``."""
+    lu = torch.empty((nfac, 5, 3), dtype=torch.float32)
+    lu[..., 0] = 2.0 ** -0.5
+    lu[..., 1] = 2.0 ** -0.5
+    lu[..., 2] = 1.0
+    return lu.to(device)
+
+
+def calib_workspace(R, o, d, a=4, nfac=1, device="cuda"):
+    """Device workspace of kq_calib_step / kq_calibrate for these sizes."""
+    n = ctypes.c_size_t(0)
+    _check(lib().kq_calib_workspace_size(R, o, d, a, nfac, ctypes.byref(n)), "kq_calib_workspace_size")
+    return torch.empty(int(n.value), dtype=torch.uint8, device=device)
+
+
+def calib_reference(X, W, Yneg=None, stream=None):
+    """kq_calib_reference: Yneg = -(X W^T), fp32 [R, o]."""
+    _need(X, torch.bfloat16, "X")
+    _need(W, torch.bfloat16, "W")
+    R, d = X.shape
+    o = W.shape[0]
+    if W.shape[1] != d:
+        raise ValueError("X and W must have the same number of columns")
+    if Yneg is None:
+        Yneg = torch.empty((R, o), dtype=torch.float32, device=X.device)
+    _need(Yneg, torch.float32, "Yneg")
+    _check(lib().kq_calib_reference(_ptr(X), R, d, _ptr(W), o, _ptr(Yneg), _stream(stream)), "kq_calib_reference")
+    return Yneg
+
+
+def calib_step(X, W, Yneg, lu, lambdas, a=4, workspace=None, adam=None, grad=None, losses=None, stream=None):
+    """kq_calib_step: losses (fp64 [4]: L_out, L_A, L_W, L) and gradient (fp32
+    [nfac, 5, 3]) of the calibration objective at ``lu``; with
+    ``adam = (m, v, t, lr)`` (t >= 1) also one Adam update of ``lu`` in place.
+    ``lambdas``: device fp32 [2].  Returns (losses, grad)."""
+    _need(X, torch.bfloat16, "X")
+    _need(W, torch.bfloat16, "W")
+    _need(Yneg, torch.float32, "Yneg")
+    _need(lu, torch.float32, "lu")
+    _need(lambdas, torch.float32, "lambdas")
+    R, d = X.shape
+    o = W.shape[0]
+    nfac = lu.numel() // 15
+    if workspace is None:
+        workspace = calib_workspace(R, o, d, a, nfac, X.device)
+    if grad is None:
+        grad = torch.empty((nfac, 5, 3), dtype=torch.float32, device=X.device)
+    if losses is None:
+        losses = torch.empty(4, dtype=torch.float64, device=X.device)
+    m = v = None
+    t, lr = 0, 0.0
+    if adam is not None:
+        m, v, t, lr = adam
+    _check(lib().kq_calib_step(_ptr(X), R, d, _ptr(W), o, _ptr(Yneg), _ptr(lu), a, nfac, _ptr(lambdas), _ptr(grad),
+                               _ptr(losses), _ptr(m), _ptr(v), int(t), float(lr), _ptr(workspace),
+                               workspace.numel(), _stream(stream)), "kq_calib_step")
+    return losses, grad
+
+
+def calibrate(X, W, lu=None, a=4, per_block=True, steps=100, lr=1e-2, Yneg=None, workspace=None, stream=None):
+    """kq_calibrate: the per-layer optimisation of Sec. 3.3 (automatic lambdas
+    at the start, ``steps`` Adam steps of rate ``lr``), from the Hadamard
+    initialisation unless ``lu`` is given (updated in place).  Returns (lu,
+    losses fp64 [steps + 2, 4])."""
+    _need(X, torch.bfloat16, "X")
+    _need(W, torch.bfloat16, "W")
+    R, d = X.shape
+    o = W.shape[0]
+    if lu is None:
+        lu = hadamard_lu(d // 32 if per_block else 1, X.device)
+    _need(lu, torch.float32, "lu")
+    nfac = lu.numel() // 15
+    if Yneg is None:
+        Yneg = calib_reference(X, W, stream=stream)
+    if workspace is None:
+        workspace = calib_workspace(R, o, d, a, nfac, X.device)
+    losses = torch.empty((steps + 2, 4), dtype=torch.float64, device=X.device)
+    _check(lib().kq_calibrate(_ptr(X), R, d, _ptr(W), o, _ptr(Yneg), _ptr(lu), a, nfac, int(steps), float(lr),
+                              _ptr(losses), _ptr(workspace), workspace.numel(), _stream(stream)), "kq_calibrate")
+    return lu, losses

@@ -3,6 +3,7 @@
 // for the contract of every entry point.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -11,6 +12,7 @@
 #include <string>
 #include <vector>
 
+#include "kq_calib.h"
 #include "kq_kernels.h"
 #include "kroquant.h"
 
@@ -427,6 +429,133 @@ kq_status kq_lu_to_factors(const float* abc, int a, int64_t nfac, float* A, floa
             }
     }
     return ok();
+}
+
+// ------------------------------------------------ layer-wise calibration
+
+static kq_status check_calib(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o, int a,
+                             int64_t nfac) {
+    if (R < 1 || o < 1) return fail(KQ_ERROR_INVALID_VALUE, "R = %lld and o = %lld must be >= 1", (long long)R,
+                                    (long long)o);
+    if (d <= 0 || d % 32 != 0)
+        return fail(KQ_ERROR_INVALID_VALUE, "d = %lld must be a positive multiple of 32", (long long)d);
+    if (R > int64_t(65535) * 128 || o > int64_t(65535) * 128)
+        return fail(KQ_ERROR_INVALID_VALUE, "R and o must be at most 65535 * 128");
+    if (R > INT64_MAX / 4 / std::max(d, o) || o > INT64_MAX / 4 / d)
+        return fail(KQ_ERROR_INVALID_VALUE, "R, o, d = %lld, %lld, %lld are too large", (long long)R, (long long)o,
+                    (long long)d);
+    if (a != 1 && a != 2 && a != 4 && a != 8) return fail(KQ_ERROR_UNSUPPORTED, "a = %d must be 1, 2, 4 or 8", a);
+    if (nfac != 1 && nfac != d / 32)
+        return fail(KQ_ERROR_UNSUPPORTED, "nfac = %lld must be 1 or d / 32 = %lld", (long long)nfac,
+                    (long long)(d / 32));
+    if (!X || !W) return fail(KQ_ERROR_NULL_POINTER, "X and W must not be NULL");
+    if (!aligned(X, 16) || !aligned(W, 16)) return fail(KQ_ERROR_MISALIGNED, "X and W must be 16-byte aligned");
+    return ok();
+}
+
+kq_status kq_calib_workspace_size(int64_t R, int64_t o, int64_t d, int a, int64_t nfac, size_t* bytes) {
+    if (!bytes) return fail(KQ_ERROR_NULL_POINTER, "bytes is NULL");
+    static const uint16_t dummy[8] __attribute__((aligned(16))) = {0};
+    const kq_status st = check_calib(dummy, R, d, dummy, o, a, nfac);
+    if (st != KQ_SUCCESS) return st;
+    *bytes = kq::calib_plan(R, o, d, a, nfac).total;
+    return ok();
+}
+
+kq_status kq_calib_reference(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o, float* Yneg,
+                             void* stream) {
+    const kq_status st = check_calib(X, R, d, W, o, 4, 1);
+    if (st != KQ_SUCCESS) return st;
+    if (!Yneg) return fail(KQ_ERROR_NULL_POINTER, "Yneg is NULL");
+    if (!aligned(Yneg, 4)) return fail(KQ_ERROR_MISALIGNED, "Yneg must be 4-byte aligned");
+    return from_hip(kq::launch_calib_reference(X, R, d, W, o, Yneg, (hipStream_t)stream), "kq_calib_reference");
+}
+
+// Forward products of one step into the workspace, then the backward pass.
+static kq_status calib_step_impl(const kq::CalibPlan& pl, const uint16_t* X, const uint16_t* W, const float* Yneg,
+                                 float* lu, const float* lambdas, float* grad, double* losses, float* adam_m,
+                                 float* adam_v, int adam_t, float lr, unsigned char* ws, hipStream_t s) {
+    const int a = pl.a, b = 32 / a;
+    float* fa = reinterpret_cast<float*>(ws + pl.fa);
+    float* fb = reinterpret_cast<float*>(ws + pl.fb);
+    hipError_t e = kq::launch_calib_inverse_factors(lu, a, pl.nfac, fa, fb, s);
+    if (e != hipSuccess) return from_hip(e, "kq_calib_step (inverse factors)");
+    kq_status st = kq_quantize_lu(X, pl.R, pl.d, lu, a, pl.nfac, ws + pl.cA, ws + pl.sA,
+                                  reinterpret_cast<float*>(ws + pl.yA), nullptr, s);
+    if (st != KQ_SUCCESS) return st;
+    st = kq_quantize(W, pl.o, pl.d, fa, fb, a, b, pl.nfac, ws + pl.cW, ws + pl.sW,
+                     reinterpret_cast<float*>(ws + pl.yW), s);
+    if (st != KQ_SUCCESS) return st;
+    float* res = reinterpret_cast<float*>(ws + pl.res);
+    e = kq::launch_calib_copy(Yneg, res, pl.R * pl.o, s);
+    if (e != hipSuccess) return from_hip(e, "kq_calib_step (residual)");
+    st = kq_mxfp4_gemm(ws + pl.cA, ws + pl.sA, pl.R, ws + pl.cW, ws + pl.sW, pl.o, pl.d, res, pl.o, 1, s);
+    if (st != KQ_SUCCESS) return st;
+    kq::CalibStepArgs args{X, W, lu, lambdas, grad, losses, lu, adam_m, adam_v, adam_t, lr, ws};
+    return from_hip(kq::launch_calib_backward(pl, args, s), "kq_calib_step (backward)");
+}
+
+static kq_status check_workspace(const kq::CalibPlan& pl, const void* ws, size_t ws_bytes) {
+    if (!ws) return fail(KQ_ERROR_NULL_POINTER, "workspace is NULL");
+    if (!aligned(ws, 256)) return fail(KQ_ERROR_MISALIGNED, "workspace must be 256-byte aligned");
+    if (ws_bytes < pl.total)
+        return fail(KQ_ERROR_INVALID_VALUE, "workspace_bytes = %zu, need %zu", ws_bytes, pl.total);
+    return ok();
+}
+
+kq_status kq_calib_step(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o, const float* Yneg,
+                        float* lu, int a, int64_t nfac, const float* lambdas, float* grad, double* losses,
+                        float* adam_m, float* adam_v, int adam_t, float lr, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+    kq_status st = check_calib(X, R, d, W, o, a, nfac);
+    if (st != KQ_SUCCESS) return st;
+    if (!Yneg || !lu || !lambdas || !grad || !losses)
+        return fail(KQ_ERROR_NULL_POINTER, "Yneg, lu, lambdas, grad and losses must not be NULL");
+    if (!aligned(Yneg, 16) || !aligned(lu, 4) || !aligned(lambdas, 4) || !aligned(grad, 4) || !aligned(losses, 8))
+        return fail(KQ_ERROR_MISALIGNED, "Yneg must be 16-byte, losses 8-byte and lu, lambdas, grad 4-byte aligned");
+    if (adam_t < 0) return fail(KQ_ERROR_INVALID_VALUE, "adam_t = %d must be >= 0", adam_t);
+    if (adam_t > 0 && (!adam_m || !adam_v))
+        return fail(KQ_ERROR_NULL_POINTER, "adam_m and adam_v must not be NULL when adam_t > 0");
+    if (adam_t > 0 && (!aligned(adam_m, 4) || !aligned(adam_v, 4)))
+        return fail(KQ_ERROR_MISALIGNED, "adam_m and adam_v must be 4-byte aligned");
+    const kq::CalibPlan pl = kq::calib_plan(R, o, d, a, nfac);
+    st = check_workspace(pl, workspace, workspace_bytes);
+    if (st != KQ_SUCCESS) return st;
+    return calib_step_impl(pl, X, W, Yneg, lu, lambdas, grad, losses, adam_m, adam_v, adam_t, lr,
+                           static_cast<unsigned char*>(workspace), (hipStream_t)stream);
+}
+
+kq_status kq_calibrate(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o, const float* Yneg,
+                       float* lu, int a, int64_t nfac, int steps, float lr, double* losses, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+    kq_status st = check_calib(X, R, d, W, o, a, nfac);
+    if (st != KQ_SUCCESS) return st;
+    if (steps < 0) return fail(KQ_ERROR_INVALID_VALUE, "steps = %d must be >= 0", steps);
+    if (!Yneg || !lu || !losses) return fail(KQ_ERROR_NULL_POINTER, "Yneg, lu and losses must not be NULL");
+    if (!aligned(Yneg, 16) || !aligned(lu, 4) || !aligned(losses, 8))
+        return fail(KQ_ERROR_MISALIGNED, "Yneg must be 16-byte, losses 8-byte and lu 4-byte aligned");
+    const kq::CalibPlan pl = kq::calib_plan(R, o, d, a, nfac);
+    st = check_workspace(pl, workspace, workspace_bytes);
+    if (st != KQ_SUCCESS) return st;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    const hipStream_t s = (hipStream_t)stream;
+    float* lam = reinterpret_cast<float*>(ws + pl.lam);
+    float* am = reinterpret_cast<float*>(ws + pl.am);
+    float* av = reinterpret_cast<float*>(ws + pl.av);
+    float* grad = reinterpret_cast<float*>(ws + pl.grad);
+    hipError_t e = kq::launch_calib_init(am, av, pl.nfac * 15, lam, s);
+    if (e != hipSuccess) return from_hip(e, "kq_calibrate (init)");
+    // losses at the initial transform, with lambda = 0, set the automatic weights
+    st = calib_step_impl(pl, X, W, Yneg, lu, lam, grad, losses, am, av, 0, lr, ws, s);
+    if (st != KQ_SUCCESS) return st;
+    e = kq::launch_calib_set_lambdas(losses, lam, s);
+    if (e != hipSuccess) return from_hip(e, "kq_calibrate (lambdas)");
+    for (int t = 1; t <= steps; ++t) {
+        st = calib_step_impl(pl, X, W, Yneg, lu, lam, grad, losses + 4 * int64_t(t), am, av, t, lr, ws, s);
+        if (st != KQ_SUCCESS) return st;
+    }
+    // losses of the final transform
+    return calib_step_impl(pl, X, W, Yneg, lu, lam, grad, losses + 4 * (int64_t(steps) + 1), am, av, 0, lr, ws, s);
 }
 
 const char* kq_status_string(kq_status s) {

@@ -204,3 +204,28 @@ def test_product_path_has_no_oracle_dependency():
                     text = f.read()
                 assert "oracle" not in text.lower(), fn
                 assert "kqo_" not in text, fn
+
+
+def test_calibration_rejects():
+    import ctypes
+    L = kq.lib()
+    n = ctypes.c_size_t(0)
+    ws = lambda R=64, o=32, d=64, a=4, nfac=1: L.kq_calib_workspace_size(R, o, d, a, nfac, ctypes.byref(n))
+    assert ws() == SUCCESS and n.value > 0
+    assert ws(R=0) == INVALID and ws(o=0) == INVALID and ws(d=48) == INVALID
+    assert ws(a=3) == UNSUPPORTED and ws(nfac=3) == UNSUPPORTED and ws(nfac=2) == SUCCESS
+    assert L.kq_calib_workspace_size(64, 32, 64, 4, 1, None) == NULLP
+    assert L.kq_calib_reference(FAKE, 4, 64, FAKE, 4, None, None) == NULLP
+    assert L.kq_calib_reference(FAKE + 8, 4, 64, FAKE, 4, FAKE, None) == MISALIGNED
+    assert ws() == SUCCESS
+    need = n.value  # the size for exactly the shape the calls below pass
+    step = lambda **kw: L.kq_calib_step(
+        kw.get("X", FAKE), 64, 64, FAKE, 32, kw.get("Y", FAKE), FAKE, 4, 1, FAKE, FAKE, FAKE,
+        kw.get("m", None), None, kw.get("t", 0), 0.01, kw.get("ws", FAKE), kw.get("wsb", need), None)
+    assert step(Y=None) == NULLP and step(X=FAKE + 2) == MISALIGNED
+    assert step(t=-1) == INVALID and step(t=1) == NULLP
+    assert step(wsb=need - 1) == INVALID and step(ws=FAKE + 16) == MISALIGNED and step(ws=None) == NULLP
+    cal = lambda **kw: L.kq_calibrate(FAKE, 64, 64, FAKE, 32, FAKE, FAKE, 4, 1, kw.get("steps", 10), 0.01,
+                                      kw.get("losses", FAKE), FAKE, kw.get("wsb", need), None)
+    assert cal(steps=-1) == INVALID and cal(losses=None) == NULLP and cal(losses=FAKE + 4) == MISALIGNED
+    assert cal(wsb=0) == INVALID
