@@ -65,8 +65,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2000)
     ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--only", choices=["kroquant", "kroquant_onthefly", "kroquant_lu", "kroquant_exact", "smoothquant",
-                                       "hadamard32", "mxfp4", "copy"],
-                    help="run only this kernel for --steps launches (for profiler runs); prints no JSON")
+                                       "hadamard32", "mxfp4", "copy", "calib"],
+                    help="run only this kernel for --steps launches (for profiler runs); prints no JSON "
+                         "(calib: only the calibration timing, printed as JSON)")
     ap.add_argument("--summarize-pmc", metavar="DIR",
                     help="turn the FETCH_SIZE / WRITE_SIZE counter runs under DIR (DIR/<kernel>/p3, p4 from "
                          "rocprofv3 --pmc, kernels 'kroquant' and 'copy') into the traffic record read by the "
@@ -74,6 +75,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")
     ap.add_argument("--no-gemm", action="store_true", help="skip the W4A4 MXFP4 GEMM consumer timing")
+    ap.add_argument("--no-calib", action="store_true", help="skip the layer-wise calibration timing")
+    ap.add_argument("--calib-samples", type=int, default=128,
+                    help="calibration samples of 4608 tokens for the calibration timing")
     ap.add_argument("--no-table2", action="store_true",
                     help="skip the power-of-two-d comparison (Q4, Scale, K1, K2, FWHT) at the paper's Table 2 shapes")
     return ap.parse_args()
@@ -152,6 +156,10 @@ def main():
         torch.cuda.synchronize()
         print(f"ran copy x{args.steps}", flush=True)
         return
+    if args.only == "calib":
+        stream = torch.cuda.current_stream()
+        print(json.dumps(calib_timing(kq, synth, dev, stream, stream.cuda_stream, args.calib_samples)), flush=True)
+        return
 
     w = synth.workload(args.workload)
     M, d = w.X.shape
@@ -198,7 +206,7 @@ def main():
             "hadamard32": run_h32, "mxfp4": run_q4}
 
     if args.only:
-        if args.only == "copy":
+        if args.only in ("copy", "calib"):
             raise AssertionError("handled before the workload setup")
         else:
             fn = runs[args.only]
@@ -247,6 +255,7 @@ def main():
     ms_warm, _ = timed(run_kq, args.steps, args.warmup, rotate=False)
     table2 = None if args.no_table2 else table2_shapes(kq, synth, dev, stream, sptr)
     gemm = None if args.no_gemm else gemm_timing(kq, synth, dev, stream, sptr, Cs[0], Ss[0], M, d)
+    calib = None if args.no_calib else calib_timing(kq, synth, dev, stream, sptr, args.calib_samples)
     dist = per_launch(run_kq)
 
     parity = "skipped"
@@ -296,6 +305,7 @@ def main():
         "cpu_baseline": cpu,
         "table2_pow2_d": table2,
         "w4a4_gemm": gemm,
+        "calibration": calib,
     }
     print(json.dumps(line), flush=True)
 
@@ -364,6 +374,7 @@ def table2_shapes(kq, synth, dev, stream, sptr, steps=500, warmup=3):
     return out
 
 
+FP32_PEAK_TFLOPS = 157.3  # dense fp32 matrix-core peak of the MI355X
 FP4_PEAK_TFLOPS = 10100.0  # MI355X dense MXFP4 matrix-core peak, TFLOP/s
 
 
@@ -394,6 +405,66 @@ def gemm_timing(kq, synth, dev, stream, sptr, xc, xs, M, K, steps=100):
                                 "frac_fp4_peak": round(tf / FP4_PEAK_TFLOPS, 4)}
         del W, Wd, wc, ws, C
     out["peak_tflops"] = FP4_PEAK_TFLOPS
+    return out
+
+
+def calib_timing(kq, synth, dev, stream, sptr, samples, steps=5, warmup=2):
+    """Layer-wise calibration (Sec. 3.3) of one FLUX.1 linear layer: `samples`
+    calibration activations of 4608 tokens (d = 3072, the Student-t(3) recipe
+    drawn on the device), a synthetic 3072 x 3072 weight, one LU parameter set
+    per 32-column block (96 x 15 parameters), Hadamard start.  Times
+    kq_calib_reference once and kq_calib_step with the Adam update (HIP events
+    on the launch stream); the paper's 100 steps then take
+    reference + 102 steps (lambda evaluation, 100 updates, final evaluation)."""
+    import torch
+    d = o = 3072
+    R = samples * 4608
+    nfac = d // 32
+    X = synth.activations_device(R, d, seed=samples, device=dev)
+    W = torch.from_numpy(synth.weights(o, d, seed=1).view(np.int16)).view(torch.bfloat16).to(dev)
+    Yneg = torch.empty((R, o), dtype=torch.float32, device=dev)
+    ws = kq.calib_workspace(R, o, d, 4, nfac, dev)
+    lu = kq.hadamard_lu(nfac, dev)
+    lam = torch.zeros(2, dtype=torch.float32, device=dev)
+    m = torch.zeros(nfac * 15, dtype=torch.float32, device=dev)
+    v = torch.zeros_like(m)
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    st = stream
+    torch.cuda.synchronize()
+    e0, e1 = ev(), ev()
+    e0.record(st)
+    kq.calib_reference(X, W, Yneg, stream=sptr)
+    e1.record(st)
+    losses, _ = kq.calib_step(X, W, Yneg, lu, lam, workspace=ws, stream=sptr)
+    torch.cuda.synchronize()
+    ms_ref = e0.elapsed_time(e1)
+    L0 = losses.cpu().numpy()
+    lam.copy_(torch.tensor([L0[0] / L0[1], L0[0] / L0[2]], dtype=torch.float32))  # automatic lambdas
+    for t in range(1, warmup + 1):
+        kq.calib_step(X, W, Yneg, lu, lam, workspace=ws, adam=(m, v, t, 1e-2), stream=sptr)
+    torch.cuda.synchronize()
+    e0.record(st)
+    for t in range(warmup + 1, warmup + steps + 1):
+        losses, _ = kq.calib_step(X, W, Yneg, lu, lam, workspace=ws, adam=(m, v, t, 1e-2), stream=sptr)
+    e1.record(st)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    back = 2 * 2.0 * R * o * d     # the two backward products (fp32 matrix cores)
+    fwd = 2.0 * R * o * d          # the W4A4 product of the forward pass
+    out = {
+        "workload": f"FLUX.1 layer: {samples} samples x 4608 tokens, d = o = 3072, per-block LU ({nfac} x 15)",
+        "rows": R, "steps": steps, "warmup": warmup,
+        "ms_per_step": round(ms, 3),
+        "ms_reference": round(ms_ref, 3),
+        "s_per_layer_100_steps": round((ms_ref + 102 * ms) / 1e3, 3),
+        "losses_t0": [float(x) for x in L0],
+        "losses_last": [float(x) for x in losses.cpu().numpy()],
+        "flops_per_step": {"backward_fp32": back, "forward_w4a4": fwd},
+        "backward_tflops_whole_step": round(back / (ms * 1e-3) / 1e12, 1),
+        "peak_fp32_tflops": FP32_PEAK_TFLOPS,
+    }
+    del X, W, Yneg, ws
+    torch.cuda.empty_cache()
     return out
 
 

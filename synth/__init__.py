@@ -146,6 +146,28 @@ def calib_layer(R, o, d, seed=0, dist="student_t3", chan_frac=0.005, chan_factor
     return X, W
 
 
+def activations_device(R, d, seed=0, chan_frac=0.005, chan_factor=50.0, device="cuda", chunk=8192):
+    """The FLUX activation recipe of ``activations`` drawn on the device with
+    torch's generator, for sizes too large to draw on the host (calibration
+    sets of 128 samples x 4608 tokens): Student-t(3) values as z / sqrt(chi2_3 / 3)
+    (z and the three chi-square terms standard normal), round(chan_frac * d)
+    channels times chan_factor, rounded to bf16.  Not bit-identical to
+    ``activations`` (another generator); used for timing only."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    X = torch.empty((R, d), dtype=torch.bfloat16, device=device)
+    ch = torch.randperm(d, generator=g, device=device)[: max(1, int(round(chan_frac * d)))]
+    for r0 in range(0, R, chunk):
+        r1 = min(R, r0 + chunk)
+        z = torch.randn((r1 - r0, d), generator=g, device=device)
+        c = (torch.randn((r1 - r0, d, 3), generator=g, device=device) ** 2).sum(-1) / 3.0
+        t = z / c.sqrt()
+        t[:, ch] *= chan_factor
+        X[r0:r1] = t.to(torch.bfloat16)
+    return X
+
+
 def smoothquant_multipliers(X_bits: np.ndarray) -> np.ndarray:
     """Per-channel multipliers m_c = 1 / s_c with s_c = max_r |X[r, c]|^0.5
     (migration strength alpha = 0.5, beta = 0), computed in fp64 and rounded
