@@ -283,12 +283,15 @@ kq_status kq_lu_to_factors(const float* abc, int a, int64_t nfac, float* A, floa
  * the product is kq_mxfp4_gemm.
  * The gradient uses a straight-through estimator: the E2M1 rounding passes
  * the gradient unchanged, the E8M0 scale is held fixed, and an element with
- * |v| > 6 * scale (clipped) passes none.  Products and sums of the backward
- * pass run in fp32 on the matrix cores; the loss sums in fp64.
+ * |v| > 6 * scale (clipped) passes none.  The backward products run on the
+ * bf16 matrix cores: the dequantized MXFP4 operands are exact in bf16, the
+ * fp32 residual enters as two bf16 terms (hi = bf16(r), lo = bf16(r - hi),
+ * within 2^-17 |r|), every product term is exact and sums are fp32; the
+ * loss sums are fp64.
  *
  * kq_calib_workspace_size -- bytes of device workspace that kq_calib_step and
- * kq_calibrate need for these sizes (about 4 R d + 4 R o + 4 o d bytes plus
- * per-workgroup partial sums).  Same size checks as kq_calib_step.
+ * kq_calibrate need for these sizes (about 6.6 R d + 8 R o + 6.6 o d bytes
+ * plus per-workgroup partial sums).  Same size checks as kq_calib_step.
  */
 kq_status kq_calib_workspace_size(int64_t R, int64_t o, int64_t d, int a, int64_t nfac, size_t* bytes);
 
@@ -296,7 +299,8 @@ kq_status kq_calib_workspace_size(int64_t R, int64_t o, int64_t d, int a, int64_
  * kq_calib_reference -- Yneg = -(X W^T), fp32 [R, o] row-major (products of
  * bf16 values exact, fp32 accumulation on the matrix cores): the fixed
  * reference of L_out, computed once per layer.  X, W device, 16-byte aligned;
- * R, o >= 1, at most 65535 * 128; d a positive multiple of 32.
+ * 1 <= R <= 65535 * 128, 1 <= o <= 65535 * 64; d a positive multiple of 32,
+ * at most 65535 * 64.
  */
 kq_status kq_calib_reference(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o, float* Yneg,
                              void* stream);

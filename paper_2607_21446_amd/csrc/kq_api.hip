@@ -286,6 +286,34 @@ kq_status kq_fwht_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* cod
     return from_hip(kq::launch_fwht(p, (hipStream_t)stream), "kq_fwht_quantize");
 }
 
+static kq::GemmParams gemm_params(const uint8_t* a_codes, const uint8_t* a_scales, int64_t M, const uint8_t* b_codes,
+                                  const uint8_t* b_scales, int64_t N, int64_t K, float* C, int64_t ldc, int accumulate,
+                                  const float* bias) {
+    kq::GemmParams g{};
+    g.a_codes = a_codes;
+    g.a_scales = a_scales;
+    g.M = M;
+    g.b_codes = b_codes;
+    g.b_scales = b_scales;
+    g.N = N;
+    g.K = K;
+    g.C = C;
+    g.ldc_out = ldc;
+    g.accumulate = accumulate;
+    g.bias = bias;
+    g.vec_ok = aligned(C, 16) && ldc % 4 == 0 && (!bias || aligned(bias, 16));
+    g.scales_aligned = aligned(a_scales, 4) && aligned(b_scales, 4);
+    // KQ_GEMM_TILE_M (optional, read once): 0 = LDS-pipelined kernel (default), 2 or 4 = register-staged
+    // kernel with that many instruction tiles per wave along M (tuning only)
+    static const int tile_m = [] {
+        const char* e = std::getenv("KQ_GEMM_TILE_M");
+        const int v = e ? std::atoi(e) : 0;
+        return (v == 2 || v == 4) ? v : 0;
+    }();
+    g.tile_m = tile_m;
+    return g;
+}
+
 kq_status kq_mxfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, int64_t M, const uint8_t* b_codes,
                         const uint8_t* b_scales, int64_t N, int64_t K, float* C, int64_t ldc, int accumulate,
                         void* stream) {
@@ -300,27 +328,7 @@ kq_status kq_mxfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, int64_t
         return fail(KQ_ERROR_NULL_POINTER, "codes, scales and C must not be NULL");
     if (!aligned(a_codes, 16) || !aligned(b_codes, 16)) return fail(KQ_ERROR_MISALIGNED, "codes must be 16-byte aligned");
     if (!aligned(C, 4)) return fail(KQ_ERROR_MISALIGNED, "C must be 4-byte aligned");
-    kq::GemmParams g{};
-    g.a_codes = a_codes;
-    g.a_scales = a_scales;
-    g.M = M;
-    g.b_codes = b_codes;
-    g.b_scales = b_scales;
-    g.N = N;
-    g.K = K;
-    g.C = C;
-    g.ldc_out = ldc;
-    g.accumulate = accumulate;
-    g.vec_ok = aligned(C, 16) && ldc % 4 == 0;
-    g.scales_aligned = aligned(a_scales, 4) && aligned(b_scales, 4);
-    // KQ_GEMM_TILE_M (optional, read once): 0 = LDS-pipelined kernel (default), 2 or 4 = register-staged
-    // kernel with that many instruction tiles per wave along M (tuning only)
-    static const int tile_m = [] {
-        const char* e = std::getenv("KQ_GEMM_TILE_M");
-        const int v = e ? std::atoi(e) : 0;
-        return (v == 2 || v == 4) ? v : 0;
-    }();
-    g.tile_m = tile_m;
+    const kq::GemmParams g = gemm_params(a_codes, a_scales, M, b_codes, b_scales, N, K, C, ldc, accumulate, nullptr);
     return from_hip(kq::launch_mxfp4_gemm(g, (hipStream_t)stream), "kq_mxfp4_gemm");
 }
 
@@ -439,8 +447,8 @@ static kq_status check_calib(const uint16_t* X, int64_t R, int64_t d, const uint
                                     (long long)o);
     if (d <= 0 || d % 32 != 0)
         return fail(KQ_ERROR_INVALID_VALUE, "d = %lld must be a positive multiple of 32", (long long)d);
-    if (R > int64_t(65535) * 128 || o > int64_t(65535) * 128)
-        return fail(KQ_ERROR_INVALID_VALUE, "R and o must be at most 65535 * 128");
+    if (R > int64_t(65535) * 128 || o > int64_t(65535) * 64 || d > int64_t(65535) * 64)
+        return fail(KQ_ERROR_INVALID_VALUE, "R must be at most 65535 * 128, o and d at most 65535 * 64");
     if (R > INT64_MAX / 4 / std::max(d, o) || o > INT64_MAX / 4 / d)
         return fail(KQ_ERROR_INVALID_VALUE, "R, o, d = %lld, %lld, %lld are too large", (long long)R, (long long)o,
                     (long long)d);
@@ -486,11 +494,12 @@ static kq_status calib_step_impl(const kq::CalibPlan& pl, const uint16_t* X, con
     st = kq_quantize(W, pl.o, pl.d, fa, fb, a, b, pl.nfac, ws + pl.cW, ws + pl.sW,
                      reinterpret_cast<float*>(ws + pl.yW), s);
     if (st != KQ_SUCCESS) return st;
+    // residual Q(X T) Q(W T^-T)^T - X W^T on the W4A4 GEMM with Yneg as its bias
     float* res = reinterpret_cast<float*>(ws + pl.res);
-    e = kq::launch_calib_copy(Yneg, res, pl.R * pl.o, s);
+    const kq::GemmParams g =
+        gemm_params(ws + pl.cA, ws + pl.sA, pl.R, ws + pl.cW, ws + pl.sW, pl.o, pl.d, res, pl.o, 0, Yneg);
+    e = kq::launch_mxfp4_gemm(g, s);
     if (e != hipSuccess) return from_hip(e, "kq_calib_step (residual)");
-    st = kq_mxfp4_gemm(ws + pl.cA, ws + pl.sA, pl.R, ws + pl.cW, ws + pl.sW, pl.o, pl.d, res, pl.o, 1, s);
-    if (st != KQ_SUCCESS) return st;
     kq::CalibStepArgs args{X, W, lu, lambdas, grad, losses, lu, adam_m, adam_v, adam_t, lr, ws};
     return from_hip(kq::launch_calib_backward(pl, args, s), "kq_calib_step (backward)");
 }

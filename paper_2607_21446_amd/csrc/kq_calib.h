@@ -14,9 +14,11 @@ struct CalibPlan {
     int64_t ntn = 0;                      // 128-column tiles of the d axis
     int64_t act_mt = 0, act_chunks = 0;   // activation-side backward: row tiles, workgroup rows
     int64_t w_mt = 0, w_ks = 0, w_kchunk = 0, w_chunks = 0;  // weight side: row tiles, K splits
-    int64_t nsum = 0;                     // partial sums of the residual's squares
+    int64_t nsum = 0;                     // partial sums of the residual's squares (one per 64 x 64 tile)
+    int64_t Rp = 0, op = 0;               // R and o rounded up to the 32-deep K stage
     // byte offsets into the workspace (each 256-byte aligned)
     size_t yA = 0, cA = 0, sA = 0, yW = 0, cW = 0, sW = 0, res = 0, fa = 0, fb = 0;
+    size_t rnh = 0, rnl = 0, rth = 0, rtl = 0, aht = 0, wht = 0;  // K-contiguous bf16 operands of the backward products
     size_t gpa = 0, gpw = 0, sqa = 0, sqw = 0, sr = 0, ga = 0, gw = 0;
     size_t grad = 0, am = 0, av = 0, lam = 0;
     size_t total = 0;
@@ -24,7 +26,7 @@ struct CalibPlan {
 
 CalibPlan calib_plan(int64_t R, int64_t o, int64_t d, int a, int64_t nfac);
 
-// Yneg[r][n] = -sum_c X[r][c] W[n][c] (fp32 matrix cores, fp32 accumulation).
+// Yneg[r][n] = -sum_c X[r][c] W[n][c] (bf16 matrix cores, exact products, fp32 accumulation).
 hipError_t launch_calib_reference(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o,
                                   float* Yneg, hipStream_t st);
 
@@ -54,6 +56,5 @@ hipError_t launch_calib_backward(const CalibPlan& pl, const CalibStepArgs& s, hi
 // Small helpers of the calibration loop.
 hipError_t launch_calib_init(float* adam_m, float* adam_v, int64_t n, float* lambdas, hipStream_t st);
 hipError_t launch_calib_set_lambdas(const double* losses, float* lambdas, hipStream_t st);
-hipError_t launch_calib_copy(const float* src, float* dst, int64_t n, hipStream_t st);
 
 }  // namespace kq

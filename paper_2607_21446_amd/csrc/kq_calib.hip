@@ -11,13 +11,20 @@
 // is held fixed, and an element clipped at +-6 * scale passes none.  The
 // forward products come from the quantizers and the W4A4 GEMM of the
 // library; this file holds the backward pass:
-//   * calib_gemm_kernel: fp32 matrix-core GEMM (v_mfma_f32_32x32x2_f32,
-//     128 x 128 workgroup tile, 16-deep K stages double-buffered in LDS) with
-//     two epilogues -- the reference product X W^T, and the fused gradient
-//     epilogue that turns a tile of dL/dQ into dL/d(transformed operand)
-//     (mask, regulariser term) and contracts it at once with the untransformed
-//     operand into 32 x 32 per-block sums  sum_rows left^T g  on the matrix
-//     cores, so the R x d gradient never reaches memory;
+//   * calib_gemm_kernel: bf16 matrix-core GEMM (v_mfma_f32_32x32x16_bf16,
+//     128 x 128 workgroup tile, 32-deep K stages loaded straight into three
+//     LDS buffers, two in flight) on operands stored K-contiguous.  The dequantized MXFP4 operands are exact
+//     in bf16; the fp32 residual enters as two bf16 terms (hi = bf16(r),
+//     lo = bf16(r - hi), |r - hi - lo| <= 2^-17 |r|), so every product term
+//     is exact and sums run in fp32.  Two epilogues: the reference product
+//     X W^T, and the fused gradient epilogue that turns a tile of dL/dQ into
+//     dL/d(transformed operand) (mask, regulariser term) and contracts it at
+//     once with the untransformed operand into 32 x 32 per-block sums
+//     sum_rows left^T g (fp32 matrix cores), so the R x d gradient never
+//     reaches memory;
+//   * residual_prep_kernel / decode_t_kernel: the residual as its two bf16
+//     terms (in its own layout and transposed, plus its sum of squares) and
+//     the dequantized operands laid out K-contiguous for the products;
 //   * gram_reduce_kernel: fixed-order sum of the per-workgroup block sums;
 //   * lu_grad_kernel: chain rule through T^-T and the Kronecker product to the
 //     2 x 2 factors and their (a, b, c), the losses, and the Adam update.
@@ -32,17 +39,22 @@ namespace kq {
 namespace {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int CT = 128;      // C tile edge of a workgroup (rows and columns)
-constexpr int CK = 16;       // K rows per LDS stage
-constexpr int CS = CT + 4;   // LDS row stride (floats): the two MFMA k-halves read rows 8 apart,
-                             // 8 * 132 = 32 (mod 64) banks apart
-constexpr int kSumParts = 1024;  // partial sums of the residual's squares
+constexpr int CT = 128;          // C tile edge of a workgroup (rows and columns)
+constexpr int BK = 32;           // K per LDS stage (bf16 elements; 64-byte rows)
+constexpr int kTileBytes = CT * BK * 2;
 constexpr int kTargetWg = 2048;  // workgroups the backward GEMMs aim for
 
 __device__ __forceinline__ float bf16f(uint16_t v) { return __uint_as_float(uint32_t(v) << 16); }
 
-// Value of an E2M1 code at E8M0 scale byte s (OCP MX v1.0), exact in fp32.
+// bf16 nearest-even of a finite fp32 value.
+__device__ __forceinline__ uint32_t bf16_rne(float x) {
+    const uint32_t u = __float_as_uint(x);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// Value of an E2M1 code at E8M0 scale byte s (OCP MX v1.0), exact in fp32 (and in bf16).
 __device__ __forceinline__ float mx_value(uint32_t nib, uint32_t s) {
     const uint32_t m = nib & 7u;
     const uint32_t bits = m >= 2 ? (((126u + (m >> 1)) << 23) | ((m & 1u) << 22)) : (m == 1 ? (126u << 23) : 0u);
@@ -59,148 +71,103 @@ __device__ __forceinline__ f32x16 mfma32(float a, float b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
 }
 
-// ---------------------------------------------------------------- loaders
-// Each loader stages a CK x CT slab of one operand (K rows, 128 M or N
-// columns) into an LDS buffer laid out [k][col] with stride CS; load() reads
-// global memory into registers (rows/cols beyond the matrix and k >= kend
-// read as 0), store() writes them to LDS.
+// LDS stage of one operand: 128 rows x 32 bf16 (four 16-byte chunks per
+// row); chunk c of row r sits at slot c ^ ((r >> 2) & 3), so the 16 lanes of
+// a ds_read_b128 phase (rows r .. r + 15, one chunk each) cover all banks.
+__device__ __forceinline__ int lds_off(int r, int c) { return r * 64 + 16 * (c ^ ((r >> 2) & 3)); }
 
-// fp32 row-major [rows][ld], K contiguous (the residual read along o).
-struct LoadRowF32 {
-    const float* src;
-    int64_t rows, ld;
-    bool vec;
-    float4 v[2];
-    __device__ void load(int64_t r0, int64_t k0, int64_t kend, int t) {
+// ---------------------------------------------------------------- operands
+// A GEMM operand: bf16 [rows][ld], K contiguous, K extent a multiple of 32
+// (zero padded by the producer), 16-byte aligned rows.  Stages of 32 K
+// columns x 128 rows go straight from global memory into LDS
+// (global_load_lds: lane l's 16 bytes land at the wave-uniform LDS address
+// + 16 l); one instruction fills 16 rows, lane l taking row l / 4 and the
+// chunk whose swizzled slot is l % 4.  Rows past the matrix load its last row
+// (their products land in rows or columns the epilogues never use).
+struct Opnd {
+    const uint8_t* p;
+    int64_t rows, ld;  // ld in bytes
+};
+
+__device__ __forceinline__ void lds_load16(const uint8_t* src, void* lds_base) {
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                     (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+
+template <int TA>
+struct StageBuf {
+    uint4 a[TA][512];  // 128 rows x 4 slots of 16 bytes, slot lds_off(r, c) / 16
+    uint4 b[512];
+};
+
+// this wave's loads of one stage: rows 32 w .. 32 w + 31 of every operand,
+// 2 (TA + 1) instructions
+template <int TA>
+__device__ __forceinline__ void stage_issue(const Opnd (&A)[TA], const Opnd& B, StageBuf<TA>& sb, int wave, int lane,
+                                            int64_t m0, int64_t n0, int64_t k0) {
+    const int q = lane >> 2;
+    const int blk = (lane & 3) ^ ((q >> 2) & 3);
+    const int64_t kb = k0 * 2 + 16 * blk;
+#pragma unroll
+    for (int gr = 0; gr < 2; ++gr) {
+        const int grp = 2 * wave + gr;
+        const int row = 16 * grp + q;
+#pragma unroll
+        for (int x = 0; x < TA; ++x) {
+            const int64_t m = min(m0 + row, A[x].rows - 1);
+            lds_load16(A[x].p + m * A[x].ld + kb, &sb.a[x][64 * grp]);
+        }
+        const int64_t n = min(n0 + row, B.rows - 1);
+        lds_load16(B.p + n * B.ld + kb, &sb.b[64 * grp]);
+    }
+}
+
+template <int TA>
+struct Frags {
+    bf16x8 a[2][TA][2], b[2][2];  // [k half s][term][tile]
+};
+
+// this wave's fragments of one stage (all LDS reads of the stage, before any
+// later stage is issued)
+template <int TA>
+__device__ __forceinline__ void stage_frags(const StageBuf<TA>& sb, int h, int wm, int wn, int l32, Frags<TA>& f) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
-            const int64_t gr = r0 + t / 4 + 64 * i;
-            const int64_t gk = k0 + 4 * (t % 4);
-            float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (gr < rows) {
-                const float* p = src + gr * ld + gk;
-                if (vec && gk + 3 < kend) {
-                    x = *reinterpret_cast<const float4*>(p);
-                } else {
-                    if (gk < kend) x.x = p[0];
-                    if (gk + 1 < kend) x.y = p[1];
-                    if (gk + 2 < kend) x.z = p[2];
-                    if (gk + 3 < kend) x.w = p[3];
-                }
-            }
-            v[i] = x;
-        }
-    }
-    __device__ void store(float* lds, int t) const {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int row = t / 4 + 64 * i, k = 4 * (t % 4);
-            lds[(k + 0) * CS + row] = v[i].x;
-            lds[(k + 1) * CS + row] = v[i].y;
-            lds[(k + 2) * CS + row] = v[i].z;
-            lds[(k + 3) * CS + row] = v[i].w;
+            for (int x = 0; x < TA; ++x)
+                f.a[s][x][i] = __builtin_bit_cast(bf16x8, sb.a[x][lds_off(wm * 64 + 32 * i + l32, 2 * h + s) / 16]);
+            f.b[s][i] = __builtin_bit_cast(bf16x8, sb.b[lds_off(wn * 64 + 32 * i + l32, 2 * h + s) / 16]);
         }
-    }
-};
+}
 
-// bf16 row-major [rows][ld], K contiguous (X and W of the reference product).
-struct LoadRowBF16 {
-    const uint16_t* src;
-    int64_t rows, ld;
-    bool vec;
-    uint16_t v[8];
-    __device__ void load(int64_t r0, int64_t k0, int64_t kend, int t) {
-        const int64_t gr = r0 + t / 2;
-        const int64_t gk = k0 + 8 * (t % 2);
+template <int TA>
+__device__ __forceinline__ void stage_mfma(const Frags<TA>& f, f32x16 (&acc)[2][2]) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = 0;
-        if (gr < rows) {
-            const uint16_t* p = src + gr * ld + gk;
-            if (vec && gk + 7 < kend) {
-                const uint4 x = *reinterpret_cast<const uint4*>(p);
-                const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+    for (int s = 0; s < 2; ++s)
 #pragma unroll
-                for (int e = 0; e < 8; ++e) v[e] = uint16_t(w[e / 2] >> (16 * (e % 2)));
-            } else {
+        for (int x = 0; x < TA; ++x)
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    if (gk + e < kend) v[e] = p[e];
-            }
-        }
-    }
-    __device__ void store(float* lds, int t) const {
-        const int row = t / 2, k = 8 * (t % 2);
+            for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) lds[(k + e) * CS + row] = bf16f(v[e]);
-    }
-};
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[s][x][i], f.b[s][j], acc[i][j], 0, 0, 0);
+}
 
-// fp32 [K][ld] with the M index contiguous (the residual read as its transpose).
-struct LoadColF32 {
-    const float* src;
-    int64_t cols, ld;  // cols: extent of the contiguous index
-    bool vec;
-    float4 v[2];
-    __device__ void load(int64_t m0, int64_t k0, int64_t kend, int t) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int64_t gk = k0 + t / 32 + 8 * i;
-            const int64_t gm = m0 + 4 * (t % 32);
-            float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (gk < kend) {
-                const float* p = src + gk * ld + gm;
-                if (vec && gm + 3 < cols) {
-                    x = *reinterpret_cast<const float4*>(p);
-                } else {
-                    if (gm < cols) x.x = p[0];
-                    if (gm + 1 < cols) x.y = p[1];
-                    if (gm + 2 < cols) x.z = p[2];
-                    if (gm + 3 < cols) x.w = p[3];
-                }
-            }
-            v[i] = x;
-        }
-    }
-    __device__ void store(float* lds, int t) const {
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-            *reinterpret_cast<float4*>(&lds[(t / 32 + 8 * i) * CS + 4 * (t % 32)]) = v[i];
-    }
-};
-
-// MXFP4 matrix [K][N] as the quantizer writes it (codes [K][N/2], two per
-// byte, low nibble first; scales [K][N/32]); N a multiple of 32.  Decoded to
-// exact fp32 values.
-struct LoadMx {
-    const uint8_t* codes;
-    const uint8_t* scales;
-    int64_t N;
-    uint32_t c, s;
-    __device__ void load(int64_t n0, int64_t k0, int64_t kend, int t) {
-        const int64_t gk = k0 + t / 16;
-        const int64_t gn = n0 + 8 * (t % 16);
-        c = 0;
-        s = 127;
-        if (gk < kend && gn < N) {
-            c = *reinterpret_cast<const uint32_t*>(codes + gk * (N / 2) + gn / 2);
-            s = scales[gk * (N / 32) + gn / 32];
-        }
-    }
-    __device__ void store(float* lds, int t) const {
-        float4 lo, hi;
-        lo.x = mx_value(c, s);
-        lo.y = mx_value(c >> 4, s);
-        lo.z = mx_value(c >> 8, s);
-        lo.w = mx_value(c >> 12, s);
-        hi.x = mx_value(c >> 16, s);
-        hi.y = mx_value(c >> 20, s);
-        hi.z = mx_value(c >> 24, s);
-        hi.w = mx_value(c >> 28, s);
-        float* p = &lds[(t / 16) * CS + 8 * (t % 16)];
-        *reinterpret_cast<float4*>(p) = lo;
-        *reinterpret_cast<float4*>(p + 4) = hi;
-    }
-};
+// Before stage st is used (buffer st % 3; stage st + 2 is then issued into
+// buffer (st + 2) % 3, which every wave finished reading before the barrier)
+// each wave waits until only its loads of stage st + 1 are outstanding, then
+// a bare s_barrier (a fenced barrier would drain the loads in flight).
+template <int TA>
+__device__ __forceinline__ void pipe_wait(int64_t st, int64_t nst) {
+    constexpr int kLoads = 2 * (TA + 1);
+    if (st + 1 < nst)
+        __builtin_amdgcn_s_waitcnt((kLoads & 15) | (7 << 4) | (15 << 8));  // vmcnt(kLoads)
+    else
+        __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+    __builtin_amdgcn_s_barrier();
+}
 
 // --------------------------------------------------------------- epilogues
 // The accumulator of a 32 x 32 MFMA tile holds, in lane l (h = l / 32) and
@@ -266,28 +233,38 @@ struct EpiGram {
             for (int i = 0; i < 2; ++i) {
                 const int64_t rbase = m0 + wm * 64 + 32 * i;
                 if (rbase >= M) continue;
+                // per half of the 16 rows: all loads first (rows past M read row M - 1 and are
+                // masked), then the arithmetic
                 f32x16 g;
                 float lv[16];
 #pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int64_t row = rbase + 8 * (e / 4) + 4 * h + (e % 4);
-                    float gv = 0.f, lf = 0.f;
-                    if (row < M) {
-                        const float yv = y[row * d + col];
-                        const uint32_t byte = codes[row * (d / 2) + col / 2];
-                        const uint32_t sb = scales[row * nb + blk];
-                        const float qv = mx_value((col & 1) ? byte >> 4 : byte, sb);
-                        const bool pass = fabsf(yv) <= 6.0f * scale_value(sb);
-                        gv = pass ? c1 * acc[i][jj][e] : 0.f;
-                        if (ks == 0) {
-                            const float diff = qv - yv;
-                            if (!pass) gv -= c2 * diff;
-                            sq += double(diff) * double(diff);
-                        }
-                        lf = bf16f(left[row * d + col]);
+                for (int half = 0; half < 2; ++half) {
+                    float yv[8];
+                    uint32_t byte[8], sbyte[8], lraw[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        const int e = 8 * half + u;
+                        const int64_t row = min(rbase + 8 * (e / 4) + 4 * h + (e % 4), M - 1);
+                        yv[u] = y[row * d + col];
+                        byte[u] = codes[row * (d / 2) + col / 2];
+                        sbyte[u] = scales[row * nb + blk];
+                        lraw[u] = left[row * d + col];
                     }
-                    g[e] = gv;
-                    lv[e] = lf;
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        const int e = 8 * half + u;
+                        const bool valid = rbase + 8 * (e / 4) + 4 * h + (e % 4) < M;
+                        const float qv = mx_value((col & 1) ? byte[u] >> 4 : byte[u], sbyte[u]);
+                        const bool pass = fabsf(yv[u]) <= 6.0f * scale_value(sbyte[u]);
+                        float gv = pass ? c1 * acc[i][jj][e] : 0.f;
+                        if (ks == 0) {
+                            const float diff = qv - yv[u];
+                            if (!pass) gv -= c2 * diff;
+                            if (valid) sq += double(diff) * double(diff);
+                        }
+                        g[e] = valid ? gv : 0.f;
+                        lv[e] = valid ? bf16f(uint16_t(lraw[u])) : 0.f;
+                    }
                 }
 #pragma unroll
                 for (int e = 0; e < 16; ++e) gram[jj] = mfma32(lv[e], g[e], gram[jj]);
@@ -301,10 +278,22 @@ struct GemmGrid {
     int64_t m_tiles, ks, kchunk, chunks;
 };
 
-template <class LA, class LB, class EPI>
-__global__ __launch_bounds__(256) void calib_gemm_kernel(LA la, LB lb, const EPI epi, const GemmGrid g) {
-    __shared__ float lds[2][2][CK * CS];
+template <int TA, class EPI>
+struct GemmArgs {
+    Opnd A[TA];
+    Opnd B;
+    EPI epi;
+    GemmGrid g;
+};
+
+// C tile = sum_k A[m][k] B[n][k] over the work items (m tile, K split) of
+// this workgroup, each handed to the epilogue; A has TA bf16 terms.  Three
+// stage buffers, two stages in flight.
+template <int TA, class EPI>
+__global__ __launch_bounds__(256) void calib_gemm_kernel(const GemmArgs<TA, EPI> args) {
+    __shared__ StageBuf<TA> sb0, sb1, sb2;
     __shared__ double sq_lds[4];
+    const GemmGrid& g = args.g;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int h = lane >> 5, l32 = lane & 31;
@@ -325,46 +314,40 @@ __global__ __launch_bounds__(256) void calib_gemm_kernel(LA la, LB lb, const EPI
         for (int i = 0; i < 2; ++i)
 #pragma unroll
             for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-
-        if (k_lo < k_hi) {
-            la.load(m0, k_lo, k_hi, t);
-            lb.load(n0, k_lo, k_hi, t);
-            la.store(lds[0][0], t);
-            lb.store(lds[0][1], t);
+        const int64_t nst = k_hi > k_lo ? (k_hi - k_lo) / BK : 0;
+        if (nst > 0) {
+            // every wave is done with the buffers (and its earlier memory operations) before they refill
+            __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
             __syncthreads();
-            int buf = 0;
-            for (int64_t k0 = k_lo; k0 < k_hi; k0 += CK) {
-                const bool more = k0 + CK < k_hi;
-                if (more) {
-                    la.load(m0, k0 + CK, k_hi, t);
-                    lb.load(n0, k0 + CK, k_hi, t);
+            stage_issue<TA>(args.A, args.B, sb0, wave, lane, m0, n0, k_lo);
+            if (nst > 1) stage_issue<TA>(args.A, args.B, sb1, wave, lane, m0, n0, k_lo + BK);
+            Frags<TA> f;
+            for (int64_t st = 0; st < nst; st += 3) {
+                pipe_wait<TA>(st, nst);
+                stage_frags<TA>(sb0, h, wm, wn, l32, f);
+                if (st + 2 < nst) stage_issue<TA>(args.A, args.B, sb2, wave, lane, m0, n0, k_lo + (st + 2) * BK);
+                stage_mfma<TA>(f, acc);
+                if (st + 1 < nst) {
+                    pipe_wait<TA>(st + 1, nst);
+                    stage_frags<TA>(sb1, h, wm, wn, l32, f);
+                    if (st + 3 < nst) stage_issue<TA>(args.A, args.B, sb0, wave, lane, m0, n0, k_lo + (st + 3) * BK);
+                    stage_mfma<TA>(f, acc);
                 }
-                const float* As = lds[buf][0];
-                const float* Bs = lds[buf][1];
-#pragma unroll
-                for (int s = 0; s < CK / 2; ++s) {
-                    const int kr = s + (CK / 2) * h;
-                    const float a0 = As[kr * CS + wm * 64 + l32], a1 = As[kr * CS + wm * 64 + 32 + l32];
-                    const float b0 = Bs[kr * CS + wn * 64 + l32], b1 = Bs[kr * CS + wn * 64 + 32 + l32];
-                    acc[0][0] = mfma32(a0, b0, acc[0][0]);
-                    acc[0][1] = mfma32(a0, b1, acc[0][1]);
-                    acc[1][0] = mfma32(a1, b0, acc[1][0]);
-                    acc[1][1] = mfma32(a1, b1, acc[1][1]);
+                if (st + 2 < nst) {
+                    pipe_wait<TA>(st + 2, nst);
+                    stage_frags<TA>(sb2, h, wm, wn, l32, f);
+                    if (st + 4 < nst) stage_issue<TA>(args.A, args.B, sb1, wave, lane, m0, n0, k_lo + (st + 4) * BK);
+                    stage_mfma<TA>(f, acc);
                 }
-                if (more) {
-                    la.store(lds[buf ^ 1][0], t);
-                    lb.store(lds[buf ^ 1][1], t);
-                }
-                __syncthreads();
-                buf ^= 1;
             }
         }
-        epi.tile(acc, m0, n0, ks, wm, wn, lane, gram, sq);
+        args.epi.tile(acc, m0, n0, ks, wm, wn, lane, gram, sq);
     }
 
     if constexpr (EPI::kGram) {
         // rows 64..127 of the tile (wm = 1) join rows 0..63, then one write per block
-        float* red = &lds[0][0][0];
+        __syncthreads();
+        float* red = reinterpret_cast<float*>(&sb0);
         if (wm == 1) {
 #pragma unroll
             for (int jj = 0; jj < 2; ++jj)
@@ -375,6 +358,7 @@ __global__ __launch_bounds__(256) void calib_gemm_kernel(LA la, LB lb, const EPI
         for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off);
         if (lane == 0) sq_lds[wave] = sq;
         __syncthreads();
+        const EPI& epi = args.epi;
         if (wm == 0) {
             const int64_t nb = epi.d / 32;
 #pragma unroll
@@ -393,28 +377,112 @@ __global__ __launch_bounds__(256) void calib_gemm_kernel(LA la, LB lb, const EPI
     }
 }
 
-// ------------------------------------------------------------ small kernels
-
-// sum of squares of v[0 .. n) into partial[blockIdx.x] (grid-stride, fp64).
-__global__ __launch_bounds__(256) void sumsq_kernel(const float* v, int64_t n, double* partial) {
+// One pass over the residual res [R, o] (fp32): its bf16 terms hi = bf16(r),
+// lo = bf16(r - hi) both as [R, op] (K = o contiguous, zero for columns
+// o .. op) and transposed as [o, Rp] (K = rows contiguous, zero for rows
+// R .. Rp), and the sum of its squares per workgroup (fp64) into
+// partial[blockIdx.y * gridDim.x + blockIdx.x].  Grid: 64-row x 64-column tiles.
+__global__ __launch_bounds__(256) void residual_prep_kernel(const float* res, int64_t rows, int64_t cols, int64_t op,
+                                                            int64_t Rp, uint16_t* nh, uint16_t* nl, uint16_t* th,
+                                                            uint16_t* tl, double* partial) {
+    __shared__ float tile[64][65];
     __shared__ double red[4];
-    double s = 0.0;
-    const int64_t n4 = n / 4;
-    const float4* v4 = reinterpret_cast<const float4*>(v);
-    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n4; i += int64_t(gridDim.x) * 256) {
-        const float4 x = v4[i];
-        s += double(x.x) * x.x + double(x.y) * x.y + double(x.z) * x.z + double(x.w) * x.w;
-    }
-    if (blockIdx.x == 0 && threadIdx.x < n - 4 * n4) {
-        const double x = v[4 * n4 + threadIdx.x];
-        s += x * x;
+    const int t = threadIdx.x;
+    const int64_t r0 = int64_t(blockIdx.x) * 64, c0 = int64_t(blockIdx.y) * 64;
+    double sq = 0.0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int rl = t / 16 + 16 * i, cl = 4 * (t % 16);
+        const int64_t r = r0 + rl, cc = c0 + cl;
+        float e[4] = {0.f, 0.f, 0.f, 0.f};
+        if (r < rows) {
+            const float* p = res + r * cols + cc;
+            if (cols % 4 == 0 && cc + 3 < cols) {
+                const float4 x = *reinterpret_cast<const float4*>(p);
+                e[0] = x.x;
+                e[1] = x.y;
+                e[2] = x.z;
+                e[3] = x.w;
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (cc + j < cols) e[j] = p[j];
+            }
+        }
+        uint32_t hb[4], lb[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            tile[rl][cl + j] = e[j];
+            sq += double(e[j]) * double(e[j]);
+            hb[j] = bf16_rne(e[j]);
+            lb[j] = bf16_rne(e[j] - __uint_as_float(hb[j] << 16));
+        }
+        // natural layout [R, op]: 4 columns (8 bytes) per thread; zero beyond o, up to op
+        if (r < rows && cc < op) {
+            *reinterpret_cast<uint2*>(nh + r * op + cc) = make_uint2(hb[0] | (hb[1] << 16), hb[2] | (hb[3] << 16));
+            *reinterpret_cast<uint2*>(nl + r * op + cc) = make_uint2(lb[0] | (lb[1] << 16), lb[2] | (lb[3] << 16));
+        }
     }
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+    for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off);
+    if ((t & 63) == 0) red[t >> 6] = sq;
     __syncthreads();
-    if (threadIdx.x == 0) partial[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
+    if (t == 0) partial[int64_t(blockIdx.y) * gridDim.x + blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
+    const int cl = t / 4, seg = t % 4;
+    const int64_t cc = c0 + cl, rr = r0 + 16 * seg;
+    if (cc >= cols || rr >= Rp) return;
+    uint32_t h[8], l[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float x0 = tile[16 * seg + 2 * j][cl], x1 = tile[16 * seg + 2 * j + 1][cl];
+        const uint32_t h0 = bf16_rne(x0), h1 = bf16_rne(x1);
+        const uint32_t l0 = bf16_rne(x0 - __uint_as_float(h0 << 16)), l1 = bf16_rne(x1 - __uint_as_float(h1 << 16));
+        h[j] = h0 | (h1 << 16);
+        l[j] = l0 | (l1 << 16);
+    }
+    uint4* ph = reinterpret_cast<uint4*>(th + cc * Rp + rr);
+    uint4* pl = reinterpret_cast<uint4*>(tl + cc * Rp + rr);
+    ph[0] = make_uint4(h[0], h[1], h[2], h[3]);
+    ph[1] = make_uint4(h[4], h[5], h[6], h[7]);
+    pl[0] = make_uint4(l[0], l[1], l[2], l[3]);
+    pl[1] = make_uint4(l[4], l[5], l[6], l[7]);
 }
+
+// out[c][r] = bf16 of the dequantized MXFP4 value (r, c) (exact), c < d,
+// r < ldo, zero for r >= rows: an MXFP4 matrix [rows, d] as its transpose.
+__global__ __launch_bounds__(256) void decode_t_kernel(const uint8_t* codes, const uint8_t* scales, int64_t rows,
+                                                       int64_t d, uint16_t* out, int64_t ldo) {
+    __shared__ uint16_t tile[64][66];
+    const int t = threadIdx.x;
+    const int64_t r0 = int64_t(blockIdx.x) * 64, c0 = int64_t(blockIdx.y) * 64;
+    {
+        const int rl = t / 4, cq = t % 4;
+        const int64_t r = r0 + rl, cc = c0 + 16 * cq;
+        uint2 cw = make_uint2(0, 0);
+        uint32_t s = 127;
+        if (r < rows && cc < d) {
+            cw = *reinterpret_cast<const uint2*>(codes + r * (d / 2) + cc / 2);
+            s = scales[r * (d / 32) + cc / 32];
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const uint32_t w = j < 8 ? cw.x : cw.y;
+            tile[rl][16 * cq + j] = uint16_t(__float_as_uint(mx_value(w >> (4 * (j % 8)), s)) >> 16);
+        }
+    }
+    __syncthreads();
+    const int cl = t / 4, seg = t % 4;
+    const int64_t cc = c0 + cl, rr = r0 + 16 * seg;
+    if (cc >= d || rr >= ldo) return;
+    uint32_t v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = uint32_t(tile[16 * seg + 2 * j][cl]) | (uint32_t(tile[16 * seg + 2 * j + 1][cl]) << 16);
+    uint4* p = reinterpret_cast<uint4*>(out + cc * ldo + rr);
+    p[0] = make_uint4(v[0], v[1], v[2], v[3]);
+    p[1] = make_uint4(v[4], v[5], v[6], v[7]);
+}
+
+// ------------------------------------------------------------ small kernels
 
 // out[f][e] = sum over chunks c and the blocks j of factor f of partial[c][j][e];
 // one factor per block j (nfac = nb) or one for all (nfac = 1).  Fixed order.
@@ -648,12 +716,6 @@ __global__ void set_lambdas_kernel(const double* losses, float* lambdas) {
     }
 }
 
-__global__ __launch_bounds__(256) void copy_kernel(const float4* src, float4* dst, int64_t n4, const float* s1,
-                                                   float* d1, int64_t tail) {
-    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n4; i += int64_t(gridDim.x) * 256) dst[i] = src[i];
-    if (blockIdx.x == 0 && threadIdx.x < tail) d1[threadIdx.x] = s1[threadIdx.x];
-}
-
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -672,12 +734,14 @@ CalibPlan calib_plan(int64_t R, int64_t o, int64_t d, int a, int64_t nfac) {
     pl.act_mt = cdiv(R, CT);
     pl.act_chunks = std::max<int64_t>(1, std::min(pl.act_mt, cdiv(kTargetWg, pl.ntn)));
     pl.w_mt = cdiv(o, CT);
-    const int64_t stages = std::max<int64_t>(1, cdiv(R, CK));
+    pl.Rp = cdiv(std::max<int64_t>(R, 1), BK) * BK;
+    pl.op = cdiv(o, BK) * BK;
+    const int64_t stages = pl.Rp / BK;
     pl.w_ks = std::max<int64_t>(1, std::min(cdiv(kTargetWg, pl.ntn * pl.w_mt), cdiv(stages, 8)));
-    pl.w_kchunk = cdiv(cdiv(std::max<int64_t>(R, 1), pl.w_ks), CK) * CK;
-    pl.w_ks = std::max<int64_t>(1, cdiv(std::max<int64_t>(R, 1), pl.w_kchunk));
+    pl.w_kchunk = cdiv(cdiv(pl.Rp, pl.w_ks), BK) * BK;
+    pl.w_ks = std::max<int64_t>(1, cdiv(pl.Rp, pl.w_kchunk));
     pl.w_chunks = pl.w_mt * pl.w_ks;
-    pl.nsum = kSumParts;
+    pl.nsum = cdiv(pl.Rp, 64) * cdiv(o, 64);
     size_t off = 0;
     auto take = [&](size_t bytes) {
         const size_t at = off;
@@ -692,6 +756,12 @@ CalibPlan calib_plan(int64_t R, int64_t o, int64_t d, int a, int64_t nfac) {
     pl.cW = take(size_t(o) * d / 2);
     pl.sW = take(size_t(o) * (d / 32));
     pl.res = take(size_t(R) * o * 4);
+    pl.rnh = take(size_t(R) * pl.op * 2);
+    pl.rnl = take(size_t(R) * pl.op * 2);
+    pl.rth = take(size_t(o) * pl.Rp * 2);
+    pl.rtl = take(size_t(o) * pl.Rp * 2);
+    pl.aht = take(size_t(d) * pl.Rp * 2);
+    pl.wht = take(size_t(d) * pl.op * 2);
     pl.fa = take(size_t(nfac) * a * a * 4);
     pl.fb = take(size_t(nfac) * b * b * 4);
     pl.gpa = take(size_t(pl.act_chunks) * pl.nb * 1024 * 4);
@@ -712,13 +782,12 @@ CalibPlan calib_plan(int64_t R, int64_t o, int64_t d, int a, int64_t nfac) {
 hipError_t launch_calib_reference(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o,
                                   float* Yneg, hipStream_t st) {
     if (R == 0 || o == 0) return hipSuccess;
-    const bool vec = d % 8 == 0;
-    LoadRowBF16 la{X, R, d, vec, {}};
-    LoadRowBF16 lb{W, o, d, vec, {}};
-    EpiStoreNeg epi{Yneg, R, o, o};
-    GemmGrid g{R, o, d, cdiv(R, CT), 1, cdiv(d, CK) * CK, cdiv(R, CT)};
-    dim3 grid(unsigned(cdiv(o, CT)), unsigned(g.chunks));
-    calib_gemm_kernel<<<grid, 256, 0, st>>>(la, lb, epi, g);
+    GemmArgs<1, EpiStoreNeg> args{{{reinterpret_cast<const uint8_t*>(X), R, d * 2}},
+                                  {reinterpret_cast<const uint8_t*>(W), o, d * 2},
+                                  {Yneg, R, o, o},
+                                  {R, o, d, cdiv(R, CT), 1, d, cdiv(R, CT)}};
+    dim3 grid(unsigned(cdiv(o, CT)), unsigned(args.g.chunks));
+    calib_gemm_kernel<1><<<grid, 256, 0, st>>>(args);
     return hipGetLastError();
 }
 
@@ -738,6 +807,12 @@ hipError_t launch_calib_backward(const CalibPlan& pl, const CalibStepArgs& s, hi
     const uint8_t* cW = ws + pl.cW;
     const uint8_t* sW = ws + pl.sW;
     float* res = reinterpret_cast<float*>(ws + pl.res);
+    uint16_t* rnh = reinterpret_cast<uint16_t*>(ws + pl.rnh);
+    uint16_t* rnl = reinterpret_cast<uint16_t*>(ws + pl.rnl);
+    uint16_t* rth = reinterpret_cast<uint16_t*>(ws + pl.rth);
+    uint16_t* rtl = reinterpret_cast<uint16_t*>(ws + pl.rtl);
+    uint16_t* aht = reinterpret_cast<uint16_t*>(ws + pl.aht);
+    uint16_t* wht = reinterpret_cast<uint16_t*>(ws + pl.wht);
     float* gpa = reinterpret_cast<float*>(ws + pl.gpa);
     float* gpw = reinterpret_cast<float*>(ws + pl.gpw);
     double* sqa = reinterpret_cast<double*>(ws + pl.sqa);
@@ -747,25 +822,31 @@ hipError_t launch_calib_backward(const CalibPlan& pl, const CalibStepArgs& s, hi
     float* gw = reinterpret_cast<float*>(ws + pl.gw);
     const int64_t R = pl.R, o = pl.o, d = pl.d;
 
-    sumsq_kernel<<<kSumParts, 256, 0, st>>>(res, R * o, sr);
     const float c1 = float(2.0 / (double(R) * double(o)));
+    // K-contiguous operands: What^T [d, op], Ahat^T [d, Rp], res as bf16 hi / lo [R, op] and [o, Rp]
+    decode_t_kernel<<<dim3(unsigned(cdiv(pl.op, 64)), unsigned(cdiv(d, 64))), 256, 0, st>>>(cW, sW, o, d, wht, pl.op);
+    decode_t_kernel<<<dim3(unsigned(cdiv(pl.Rp, 64)), unsigned(cdiv(d, 64))), 256, 0, st>>>(cA, sA, R, d, aht, pl.Rp);
+    residual_prep_kernel<<<dim3(unsigned(cdiv(pl.Rp, 64)), unsigned(cdiv(o, 64))), 256, 0, st>>>(
+        res, R, o, pl.op, pl.Rp, rnh, rnl, rth, rtl, sr);
     // activation side: P = res . What  (M = R, N = d, K = o)
     {
-        LoadRowF32 la{res, R, o, o % 4 == 0, {}};
-        LoadMx lb{cW, sW, d, 0, 0};
-        EpiGram epi{s.X, yA, cA, sA, R, d, c1, s.lambdas, 0, float(2.0 / (double(R) * double(d))), gpa, sqa};
-        GemmGrid g{R, d, o, pl.act_mt, 1, cdiv(o, CK) * CK, pl.act_chunks};
+        GemmArgs<2, EpiGram> args{
+            {{reinterpret_cast<const uint8_t*>(rnh), R, pl.op * 2}, {reinterpret_cast<const uint8_t*>(rnl), R, pl.op * 2}},
+            {reinterpret_cast<const uint8_t*>(wht), d, pl.op * 2},
+            {s.X, yA, cA, sA, R, d, c1, s.lambdas, 0, float(2.0 / (double(R) * double(d))), gpa, sqa},
+            {R, d, pl.op, pl.act_mt, 1, pl.op, pl.act_chunks}};
         dim3 grid(unsigned(pl.ntn), unsigned(pl.act_chunks));
-        calib_gemm_kernel<<<grid, 256, 0, st>>>(la, lb, epi, g);
+        calib_gemm_kernel<2><<<grid, 256, 0, st>>>(args);
     }
     // weight side: P = res^T . Ahat  (M = o, N = d, K = R)
     {
-        LoadColF32 la{res, o, o, o % 4 == 0, {}};
-        LoadMx lb{cA, sA, d, 0, 0};
-        EpiGram epi{s.W, yW, cW, sW, o, d, c1, s.lambdas, 1, float(2.0 / (double(o) * double(d))), gpw, sqw};
-        GemmGrid g{o, d, R, pl.w_mt, pl.w_ks, pl.w_kchunk, pl.w_chunks};
+        GemmArgs<2, EpiGram> args{
+            {{reinterpret_cast<const uint8_t*>(rth), o, pl.Rp * 2}, {reinterpret_cast<const uint8_t*>(rtl), o, pl.Rp * 2}},
+            {reinterpret_cast<const uint8_t*>(aht), d, pl.Rp * 2},
+            {s.W, yW, cW, sW, o, d, c1, s.lambdas, 1, float(2.0 / (double(o) * double(d))), gpw, sqw},
+            {o, d, pl.Rp, pl.w_mt, pl.w_ks, pl.w_kchunk, pl.w_chunks}};
         dim3 grid(unsigned(pl.ntn), unsigned(pl.w_chunks));
-        calib_gemm_kernel<<<grid, 256, 0, st>>>(la, lb, epi, g);
+        calib_gemm_kernel<2><<<grid, 256, 0, st>>>(args);
     }
     gram_reduce_kernel<<<dim3(unsigned(pl.nfac), 4), 256, 0, st>>>(gpa, pl.act_chunks, pl.nb, pl.nfac, ga);
     gram_reduce_kernel<<<dim3(unsigned(pl.nfac), 4), 256, 0, st>>>(gpw, pl.w_chunks, pl.nb, pl.nfac, gw);
@@ -780,7 +861,7 @@ hipError_t launch_calib_backward(const CalibPlan& pl, const CalibStepArgs& s, hi
     la.adam_t = s.adam_t;
     la.lr = s.lr;
     la.sr = sr;
-    la.nsr = kSumParts;
+    la.nsr = pl.nsum;
     la.sqa = sqa;
     la.nsqa = pl.act_chunks * pl.ntn;
     la.sqw = sqw;
@@ -801,14 +882,6 @@ hipError_t launch_calib_init(float* adam_m, float* adam_v, int64_t n, float* lam
 
 hipError_t launch_calib_set_lambdas(const double* losses, float* lambdas, hipStream_t st) {
     set_lambdas_kernel<<<1, 64, 0, st>>>(losses, lambdas);
-    return hipGetLastError();
-}
-
-hipError_t launch_calib_copy(const float* src, float* dst, int64_t n, hipStream_t st) {
-    const int64_t n4 = n / 4;
-    const unsigned grid = unsigned(std::max<int64_t>(1, std::min<int64_t>(cdiv(n4, 256), 4096)));
-    copy_kernel<<<grid, 256, 0, st>>>(reinterpret_cast<const float4*>(src), reinterpret_cast<float4*>(dst), n4,
-                                      src + 4 * n4, dst + 4 * n4, n - 4 * n4);
     return hipGetLastError();
 }
 

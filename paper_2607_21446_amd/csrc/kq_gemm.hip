@@ -111,7 +111,8 @@ __global__ __launch_bounds__(256) void mxfp4_gemm_kernel(const GemmParams g) {
                     const int64_t row = m0 + 32 * i + 8 * q + 4 * h + e;
                     if (row >= g.M) continue;
                     float* dst = g.C + row * g.ldc_out + col;
-                    *dst = g.accumulate ? *dst + acc[i][j][4 * q + e] : acc[i][j][4 * q + e];
+                    const float base = g.bias ? g.bias[row * g.ldc_out + col] : g.accumulate ? *dst : 0.0f;
+                    *dst = (g.bias || g.accumulate) ? base + acc[i][j][4 * q + e] : acc[i][j][4 * q + e];
                 }
         }
 }
@@ -248,6 +249,7 @@ __global__ __launch_bounds__(256) void mxfp4_gemm_tiled_kernel(const GemmParams 
         const int64_t m = mb0 + wm * (32 * TM) + 32 * j + r;
         if (m >= g.M) continue;
         float* crow = g.C + m * g.ldc_out;
+        const float* brow = g.bias ? g.bias + m * g.ldc_out : g.accumulate ? crow : nullptr;
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -255,17 +257,16 @@ __global__ __launch_bounds__(256) void mxfp4_gemm_tiled_kernel(const GemmParams 
                 const int64_t n = nb0 + wn * 64 + 32 * i + 8 * q + 4 * h;
                 float4 v = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
                 if (g.vec_ok && n + 3 < g.N) {
-                    float4* dst = reinterpret_cast<float4*>(crow + n);
-                    if (g.accumulate) {
-                        const float4 o = *dst;
+                    if (brow) {
+                        const float4 o = *reinterpret_cast<const float4*>(brow + n);
                         v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
                     }
-                    *dst = v;
+                    *reinterpret_cast<float4*>(crow + n) = v;
                 } else {
-                    if (n + 0 < g.N) crow[n + 0] = g.accumulate ? crow[n + 0] + v.x : v.x;
-                    if (n + 1 < g.N) crow[n + 1] = g.accumulate ? crow[n + 1] + v.y : v.y;
-                    if (n + 2 < g.N) crow[n + 2] = g.accumulate ? crow[n + 2] + v.z : v.z;
-                    if (n + 3 < g.N) crow[n + 3] = g.accumulate ? crow[n + 3] + v.w : v.w;
+                    if (n + 0 < g.N) crow[n + 0] = brow ? brow[n + 0] + v.x : v.x;
+                    if (n + 1 < g.N) crow[n + 1] = brow ? brow[n + 1] + v.y : v.y;
+                    if (n + 2 < g.N) crow[n + 2] = brow ? brow[n + 2] + v.z : v.z;
+                    if (n + 3 < g.N) crow[n + 3] = brow ? brow[n + 3] + v.w : v.w;
                 }
             }
     }
@@ -422,6 +423,7 @@ __global__ __launch_bounds__(256) void mxfp4_gemm_pipe_kernel(const GemmParams g
         const int64_t m = mb0 + wm * 64 + 32 * j + r;
         if (m >= g.M) continue;
         float* crow = g.C + m * g.ldc_out;
+        const float* brow = g.bias ? g.bias + m * g.ldc_out : g.accumulate ? crow : nullptr;
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -429,17 +431,16 @@ __global__ __launch_bounds__(256) void mxfp4_gemm_pipe_kernel(const GemmParams g
                 const int64_t n = nb0 + wn * 64 + 32 * i + 8 * q + 4 * h;
                 float4 v = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
                 if (g.vec_ok && n + 3 < g.N) {
-                    float4* dst = reinterpret_cast<float4*>(crow + n);
-                    if (g.accumulate) {
-                        const float4 o = *dst;
+                    if (brow) {
+                        const float4 o = *reinterpret_cast<const float4*>(brow + n);
                         v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
                     }
-                    *dst = v;
+                    *reinterpret_cast<float4*>(crow + n) = v;
                 } else {
-                    if (n + 0 < g.N) crow[n + 0] = g.accumulate ? crow[n + 0] + v.x : v.x;
-                    if (n + 1 < g.N) crow[n + 1] = g.accumulate ? crow[n + 1] + v.y : v.y;
-                    if (n + 2 < g.N) crow[n + 2] = g.accumulate ? crow[n + 2] + v.z : v.z;
-                    if (n + 3 < g.N) crow[n + 3] = g.accumulate ? crow[n + 3] + v.w : v.w;
+                    if (n + 0 < g.N) crow[n + 0] = brow ? brow[n + 0] + v.x : v.x;
+                    if (n + 1 < g.N) crow[n + 1] = brow ? brow[n + 1] + v.y : v.y;
+                    if (n + 2 < g.N) crow[n + 2] = brow ? brow[n + 2] + v.z : v.z;
+                    if (n + 3 < g.N) crow[n + 3] = brow ? brow[n + 3] + v.w : v.w;
                 }
             }
     }

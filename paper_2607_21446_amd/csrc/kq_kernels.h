@@ -53,6 +53,7 @@ struct GemmParams {
     float* C;                 // [M, ldc_out]
     int64_t ldc_out;
     int accumulate;           // 1: C += product, 0: C = product
+    const float* bias = nullptr;  // if set: C = bias + product (bias [M, ldc_out], vec rule as C)
     int vec_ok;               // C 16-byte aligned and ldc_out a multiple of 4
     int scales_aligned;       // both scale arrays 4-byte aligned
     int tile_m = 2;           // instruction tiles per wave along M in the tiled kernel (2 or 4)

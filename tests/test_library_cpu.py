@@ -213,6 +213,7 @@ def test_calibration_rejects():
     ws = lambda R=64, o=32, d=64, a=4, nfac=1: L.kq_calib_workspace_size(R, o, d, a, nfac, ctypes.byref(n))
     assert ws() == SUCCESS and n.value > 0
     assert ws(R=0) == INVALID and ws(o=0) == INVALID and ws(d=48) == INVALID
+    assert ws(o=65535 * 64 + 1) == INVALID and ws(d=65535 * 64 + 32, nfac=1) == INVALID
     assert ws(a=3) == UNSUPPORTED and ws(nfac=3) == UNSUPPORTED and ws(nfac=2) == SUCCESS
     assert L.kq_calib_workspace_size(64, 32, 64, 4, 1, None) == NULLP
     assert L.kq_calib_reference(FAKE, 4, 64, FAKE, 4, None, None) == NULLP
