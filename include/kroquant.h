@@ -33,7 +33,8 @@
  *    KQ_SMOOTH_PATH and KQ_SMOOTH_WAVES select alternative kernel shapes of
  *    kq_quantize_packed and kq_smoothquant_quantize; KQ_GEMM_TILE_M (2 or 4)
  *    selects the register-staged kq_mxfp4_gemm kernel instead of the
- *    LDS-pipelined one.
+ *    LDS-pipelined ones, 8 forces their 256 x 256 tile (by default used once
+ *    the product has at least 96 such tiles, else 128 x 128).
  *  - Inputs must be finite; NaN or Inf inputs give unspecified codes.
  *  - Arguments are validated before any HIP call.  On failure the call
  *    returns the status and kq_last_error_detail() describes the argument

@@ -303,12 +303,13 @@ static kq::GemmParams gemm_params(const uint8_t* a_codes, const uint8_t* a_scale
     g.bias = bias;
     g.vec_ok = aligned(C, 16) && ldc % 4 == 0 && (!bias || aligned(bias, 16));
     g.scales_aligned = aligned(a_scales, 4) && aligned(b_scales, 4);
-    // KQ_GEMM_TILE_M (optional, read once): 0 = LDS-pipelined kernel (default), 2 or 4 = register-staged
-    // kernel with that many instruction tiles per wave along M (tuning only)
+    // KQ_GEMM_TILE_M (optional, read once): 0 = LDS-pipelined kernels (default: 256 x 256 tiles when there
+    // are at least 96 of them, else 128 x 128), 8 = always 256 x 256, 2 or 4 = register-staged kernel with
+    // that many instruction tiles per wave along M (tuning only)
     static const int tile_m = [] {
         const char* e = std::getenv("KQ_GEMM_TILE_M");
         const int v = e ? std::atoi(e) : 0;
-        return (v == 2 || v == 4) ? v : 0;
+        return (v == 2 || v == 4 || v == 8) ? v : 0;
     }();
     g.tile_m = tile_m;
     return g;

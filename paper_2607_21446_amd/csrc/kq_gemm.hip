@@ -446,8 +446,167 @@ __global__ __launch_bounds__(256) void mxfp4_gemm_pipe_kernel(const GemmParams g
     }
 }
 
+// Large-tile pipelined variant (same conditions as the one above): 512
+// threads own a 256 (N) x 256 (M) tile, 8 waves as 2 (N) x 4 (M) of 128 x 64
+// (4 x 2 instruction tiles, 128 accumulator registers), K 128 per stage in
+// three LDS stage buffers of 34 KB.  Twice the matrix-core work per operand
+// byte of the 128 x 128 tile and per barrier; each wave still issues 5 loads
+// per stage: W and X codes of rows 32 w .. 32 w + 31 (two 16-row loads each)
+// and one 64-row scale group (waves 0-3: W, waves 4-7: X).
+struct BigBuf {
+    uint4 wc[4 * 256];
+    uint4 xc[4 * 256];
+    uint32_t ws[256];
+    uint32_t xs[256];
+};
+
+__shared__ BigBuf g_big0, g_big1, g_big2;
+
+constexpr int64_t kBigTileMin = 96;  // 256 x 256 tiles needed before that kernel is chosen
+
+template <int B>
+__device__ __forceinline__ BigBuf& big_buf() {
+    if constexpr (B == 0) return g_big0;
+    else if constexpr (B == 1) return g_big1;
+    else return g_big2;
+}
+
+__device__ __forceinline__ void big_issue(const GemmParams& g, BigBuf& b, int wave, int lane, int64_t nb0, int64_t mb0,
+                                          int64_t row_bytes, int64_t nkb, int64_t st) {
+    const int q = lane >> 2;
+    const int blk = (lane & 3) ^ ((q >> 2) & 3);
+    const int64_t kbyte = (4 * st + blk) * 16;
+#pragma unroll
+    for (int gr = 0; gr < 2; ++gr) {
+        const int grp = 2 * wave + gr;
+        const int row = 16 * grp + q;
+        const int64_t n = min(nb0 + row, g.N - 1);
+        const int64_t m = min(mb0 + row, g.M - 1);
+        lds_load16(g.b_codes + n * row_bytes + kbyte, &b.wc[64 * grp]);
+        lds_load16(g.a_codes + m * row_bytes + kbyte, &b.xc[64 * grp]);
+    }
+    if (wave < 4) {
+        const int64_t n = min(nb0 + 64 * wave + lane, g.N - 1);
+        lds_load4(g.b_scales + n * nkb + 4 * st, &b.ws[64 * wave]);
+    } else {
+        const int64_t m = min(mb0 + 64 * (wave - 4) + lane, g.M - 1);
+        lds_load4(g.a_scales + m * nkb + 4 * st, &b.xs[64 * (wave - 4)]);
+    }
+}
+
+// A wave's fragments of one stage: both 64-wide K steps of its 4 W and 2 X tiles and their scales.
+struct BigFrags {
+    uint4 fw[2][4], fx[2][2];
+    uint32_t scw[4], scx[2];
+};
+
+__device__ __forceinline__ void big_frags(const BigBuf& b, const PipeCtx& c, BigFrags& f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f.scw[i] = __builtin_amdgcn_perm(0u, b.ws[c.wn * 128 + 32 * i + c.r], c.psel);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) f.scx[j] = __builtin_amdgcn_perm(0u, b.xs[c.wm * 64 + 32 * j + c.r], c.psel);
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) f.fw[s][i] = b.wc[pipe_slot(c.wn * 128 + 32 * i + c.r, 2 * s + c.h)];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) f.fx[s][j] = b.xc[pipe_slot(c.wm * 64 + 32 * j + c.r, 2 * s + c.h)];
+    }
+}
+
+template <int STEP>
+__device__ __forceinline__ void big_step(const BigFrags& f, f32x16g (&acc)[4][2]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(operand(Frag{f.fw[STEP][i], 0u}),
+                                                                         operand(Frag{f.fx[STEP][j], 0u}), acc[i][j], 4,
+                                                                         4, STEP, (int)f.scw[i], STEP, (int)f.scx[j]);
+}
+
+// All LDS reads of stage st come before stage st + 2 is issued, so the
+// vmcnt(0) the compiler still places before LDS reads in one of the three
+// unrolled iterations waits only for stage st + 1, already in flight.
+template <int CUR, int NXT>
+__device__ __forceinline__ void big_iter(const GemmParams& g, const PipeCtx& c, int64_t st, f32x16g (&acc)[4][2]) {
+    if (st + 1 < c.nst)
+        __builtin_amdgcn_s_waitcnt((kPipeLoadsPerWave & 15) | (7 << 4) | (15 << 8));  // vmcnt(5)
+    else
+        __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    BigFrags f;
+    big_frags(big_buf<CUR>(), c, f);
+    if (st + 2 < c.nst) big_issue(g, big_buf<NXT>(), c.wave, c.lane, c.nb0, c.mb0, c.row_bytes, c.nkb, st + 2);
+    big_step<0>(f, acc);
+    big_step<1>(f, acc);
+}
+
+__global__ __launch_bounds__(512) void mxfp4_gemm_big_kernel(const GemmParams g) {
+    PipeCtx c;
+    const int t = threadIdx.x;
+    c.wave = t >> 6;
+    c.lane = t & 63;
+    c.r = c.lane & 31;
+    c.h = c.lane >> 5;
+    c.wn = c.wave >> 2;
+    c.wm = c.wave & 3;
+    c.nb0 = (int64_t)blockIdx.x * 256;
+    c.mb0 = (int64_t)blockIdx.y * 256;
+    c.nkb = g.K / 32;
+    c.row_bytes = g.K / 2;
+    c.nst = g.K / 128;
+    c.psel = c.h ? 0x0c0c0301u : 0x0c0c0200u;
+    f32x16g acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16g{};
+    big_issue(g, g_big0, c.wave, c.lane, c.nb0, c.mb0, c.row_bytes, c.nkb, 0);
+    if (c.nst > 1) big_issue(g, g_big1, c.wave, c.lane, c.nb0, c.mb0, c.row_bytes, c.nkb, 1);
+    for (int64_t st = 0; st < c.nst; st += 3) {
+        big_iter<0, 2>(g, c, st, acc);
+        if (st + 1 < c.nst) big_iter<1, 0>(g, c, st + 1, acc);
+        if (st + 2 < c.nst) big_iter<2, 1>(g, c, st + 2, acc);
+    }
+    const int r = c.r, h = c.h, wn = c.wn, wm = c.wm;
+    // acc[i][j][4q + e] = C[mb0 + wm 64 + 32 j + r][nb0 + wn 128 + 32 i + 8 q + 4 h + e]
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int64_t m = c.mb0 + wm * 64 + 32 * j + r;
+        if (m >= g.M) continue;
+        float* crow = g.C + m * g.ldc_out;
+        const float* brow = g.bias ? g.bias + m * g.ldc_out : g.accumulate ? crow : nullptr;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int64_t n = c.nb0 + wn * 128 + 32 * i + 8 * q + 4 * h;
+                float4 v = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+                if (g.vec_ok && n + 3 < g.N) {
+                    if (brow) {
+                        const float4 o = *reinterpret_cast<const float4*>(brow + n);
+                        v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
+                    }
+                    *reinterpret_cast<float4*>(crow + n) = v;
+                } else {
+                    if (n + 0 < g.N) crow[n + 0] = brow ? brow[n + 0] + v.x : v.x;
+                    if (n + 1 < g.N) crow[n + 1] = brow ? brow[n + 1] + v.y : v.y;
+                    if (n + 2 < g.N) crow[n + 2] = brow ? brow[n + 2] + v.z : v.z;
+                    if (n + 3 < g.N) crow[n + 3] = brow ? brow[n + 3] + v.w : v.w;
+                }
+            }
+    }
+}
+
 hipError_t launch_mxfp4_gemm(const GemmParams& g, hipStream_t st) {
-    if (g.K % kGemmTileK == 0 && g.scales_aligned && g.tile_m == 0) {
+    // the 256 x 256 tile once there are enough of them to spread over the chip, else 128 x 128
+    const int64_t big_tiles = ((g.N + 255) / 256) * ((g.M + 255) / 256);
+    const bool big = g.tile_m == 8 || (g.tile_m == 0 && big_tiles >= kBigTileMin);
+    if (g.K % kGemmTileK == 0 && g.scales_aligned && big) {
+        const dim3 grid((unsigned)((g.N + 255) / 256), (unsigned)((g.M + 255) / 256));
+        hipLaunchKernelGGL(mxfp4_gemm_big_kernel, grid, dim3(512), 0, st, g);
+    } else if (g.K % kGemmTileK == 0 && g.scales_aligned && g.tile_m == 0) {
         const dim3 grid((unsigned)((g.N + 127) / 128), (unsigned)((g.M + 127) / 128));
         hipLaunchKernelGGL(mxfp4_gemm_pipe_kernel, grid, dim3(256), 0, st, g);
     } else if (g.K % kGemmTileK == 0 && g.scales_aligned) {
