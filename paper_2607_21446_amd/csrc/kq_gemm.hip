@@ -542,33 +542,7 @@ __device__ __forceinline__ void big_iter(const GemmParams& g, const PipeCtx& c, 
     big_step<1>(f, acc);
 }
 
-__global__ __launch_bounds__(512) void mxfp4_gemm_big_kernel(const GemmParams g) {
-    PipeCtx c;
-    const int t = threadIdx.x;
-    c.wave = t >> 6;
-    c.lane = t & 63;
-    c.r = c.lane & 31;
-    c.h = c.lane >> 5;
-    c.wn = c.wave >> 2;
-    c.wm = c.wave & 3;
-    c.nb0 = (int64_t)blockIdx.x * 256;
-    c.mb0 = (int64_t)blockIdx.y * 256;
-    c.nkb = g.K / 32;
-    c.row_bytes = g.K / 2;
-    c.nst = g.K / 128;
-    c.psel = c.h ? 0x0c0c0301u : 0x0c0c0200u;
-    f32x16g acc[4][2];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16g{};
-    big_issue(g, g_big0, c.wave, c.lane, c.nb0, c.mb0, c.row_bytes, c.nkb, 0);
-    if (c.nst > 1) big_issue(g, g_big1, c.wave, c.lane, c.nb0, c.mb0, c.row_bytes, c.nkb, 1);
-    for (int64_t st = 0; st < c.nst; st += 3) {
-        big_iter<0, 2>(g, c, st, acc);
-        if (st + 1 < c.nst) big_iter<1, 0>(g, c, st + 1, acc);
-        if (st + 2 < c.nst) big_iter<2, 1>(g, c, st + 2, acc);
-    }
+__device__ __forceinline__ void big_store(const GemmParams& g, const PipeCtx& c, const f32x16g (&acc)[4][2]) {
     const int r = c.r, h = c.h, wn = c.wn, wm = c.wm;
     // acc[i][j][4q + e] = C[mb0 + wm 64 + 32 j + r][nb0 + wn 128 + 32 i + 8 q + 4 h + e]
 #pragma unroll
@@ -597,6 +571,36 @@ __global__ __launch_bounds__(512) void mxfp4_gemm_big_kernel(const GemmParams g)
                 }
             }
     }
+}
+
+__global__ __launch_bounds__(512) void mxfp4_gemm_big_kernel(const GemmParams g) {
+    PipeCtx c;
+    const int t = threadIdx.x;
+    c.wave = __builtin_amdgcn_readfirstlane(t >> 6);  // wave-uniform: LDS bases and row offsets stay scalar
+    c.lane = t & 63;
+    c.r = c.lane & 31;
+    c.h = c.lane >> 5;
+    c.wn = c.wave >> 2;
+    c.wm = c.wave & 3;
+    c.nb0 = (int64_t)blockIdx.x * 256;
+    c.mb0 = (int64_t)blockIdx.y * 256;
+    c.nkb = g.K / 32;
+    c.row_bytes = g.K / 2;
+    c.nst = g.K / 128;
+    c.psel = c.h ? 0x0c0c0301u : 0x0c0c0200u;
+    f32x16g acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16g{};
+    big_issue(g, g_big0, c.wave, c.lane, c.nb0, c.mb0, c.row_bytes, c.nkb, 0);
+    if (c.nst > 1) big_issue(g, g_big1, c.wave, c.lane, c.nb0, c.mb0, c.row_bytes, c.nkb, 1);
+    for (int64_t st = 0; st < c.nst; st += 3) {
+        big_iter<0, 2>(g, c, st, acc);
+        if (st + 1 < c.nst) big_iter<1, 0>(g, c, st + 1, acc);
+        if (st + 2 < c.nst) big_iter<2, 1>(g, c, st + 2, acc);
+    }
+    big_store(g, c, acc);
 }
 
 hipError_t launch_mxfp4_gemm(const GemmParams& g, hipStream_t st) {
