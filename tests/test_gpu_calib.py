@@ -141,3 +141,53 @@ def test_calibrate_loop():
     assert rows[-1, 0] == pytest.approx(r["L_out"], rel=1e-4)
     assert rows[-1, 3] == pytest.approx(r["L"], rel=1e-4)
     print("gpu rows", rows[:, 3], "\noracle rows", rows_or[:, 3], "\nmax |dlu|", np.abs(lu_gpu - lu_or).max())
+
+
+def test_calibration_graph_replays_match_eager():
+    """kq_calib_step (no update) and a whole 3-step kq_calibrate captured into
+    HIP graphs and replayed three times, with other work and synchronizations
+    between the replays and the parameters reset before each: every replay
+    reproduces the eager losses, gradient, parameters and loss rows bit for bit
+    (the calls allocate, clear and synchronize nothing; all sums run in a fixed
+    order)."""
+    R, o, d, a = 300, 160, 256, 4
+    nfac = d // 32
+    X, W = synth.calib_layer(R, o, d, seed=31)
+    lu0 = synth.lu_params(nfac, seed=32)
+    Xd, Wd = dev_bf16(X), dev_bf16(W)
+    Yneg = kq.calib_reference(Xd, Wd)
+    ws = kq.calib_workspace(R, o, d, a, nfac)
+    lam = dev_f32(np.array(LAM))
+    lud = dev_f32(lu0)
+    grad = torch.empty((nfac, 5, 3), dtype=torch.float32, device="cuda")
+    losses = torch.empty(4, dtype=torch.float64, device="cuda")
+    kq.calib_step(Xd, Wd, Yneg, lud, lam, a=a, workspace=ws, grad=grad, losses=losses)
+    e_loss, e_grad = host(losses).copy(), host(grad).copy()
+    lu_c = dev_f32(lu0)
+    _, e_rows = kq.calibrate(Xd, Wd, lu=lu_c, a=a, steps=3, Yneg=Yneg, workspace=ws)
+    e_rows, e_lu = host(e_rows).copy(), host(lu_c).copy()
+
+    g1 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g1):
+        kq.calib_step(Xd, Wd, Yneg, lud, lam, a=a, workspace=ws, grad=grad, losses=losses)
+    lu_g = dev_f32(lu0)
+    rows_g = torch.empty((5, 4), dtype=torch.float64, device="cuda")
+    g2 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g2):
+        _, r = kq.calibrate(Xd, Wd, lu=lu_g, a=a, steps=3, Yneg=Yneg, workspace=ws)
+        rows_g.copy_(r)
+    other = dev_bf16(synth.activations(256, 1024, "normal", seed=33))
+    lu0_d = dev_f32(lu0)
+    for rep in range(3):
+        grad.fill_(7.0)
+        losses.fill_(7.0)
+        rows_g.fill_(7.0)
+        lu_g.copy_(lu0_d)
+        kq.mxfp4(other)
+        torch.cuda.synchronize()
+        g1.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(host(losses), e_loss) and np.array_equal(host(grad), e_grad), rep
+        g2.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(host(rows_g), e_rows) and np.array_equal(host(lu_g), e_lu), rep
