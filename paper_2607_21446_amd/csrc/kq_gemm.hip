@@ -573,6 +573,25 @@ __device__ __forceinline__ void big_store(const GemmParams& g, const PipeCtx& c,
     }
 }
 
+// Tile of workgroup (blockIdx.x, blockIdx.y) of a gx x gy grid.  Workgroups
+// are dealt to the 8 XCDs round-robin by linear id, so XCD k runs ids
+// k, k + 8, ...; those get consecutive logical ids (a bijection for any
+// count), and logical ids walk the tiles in groups of 4 M rows (N fastest
+// within a group, M fastest within a column), so each XCD's L2 sees a compact
+// block of about 4 x (T / 32) tiles instead of every M row.
+__device__ __forceinline__ void xcd_tile(int64_t gx, int64_t gy, int64_t& tn, int64_t& tm) {
+    const int64_t T = gx * gy;
+    const int64_t i = (int64_t)blockIdx.y * gx + blockIdx.x;
+    const int64_t k = i % 8, j = i / 8;
+    const int64_t L = k * (T / 8) + (k < T % 8 ? k : T % 8) + j;
+    constexpr int64_t GM = 4;
+    const int64_t gsize = GM * gx;
+    const int64_t first_m = (L / gsize) * GM;
+    const int64_t gm = gy - first_m < GM ? gy - first_m : GM;
+    tm = first_m + (L % gsize) % gm;
+    tn = (L % gsize) / gm;
+}
+
 __global__ __launch_bounds__(512) void mxfp4_gemm_big_kernel(const GemmParams g) {
     PipeCtx c;
     const int t = threadIdx.x;
@@ -582,8 +601,10 @@ __global__ __launch_bounds__(512) void mxfp4_gemm_big_kernel(const GemmParams g)
     c.h = c.lane >> 5;
     c.wn = c.wave >> 2;
     c.wm = c.wave & 3;
-    c.nb0 = (int64_t)blockIdx.x * 256;
-    c.mb0 = (int64_t)blockIdx.y * 256;
+    int64_t tn, tm;
+    xcd_tile(gridDim.x, gridDim.y, tn, tm);
+    c.nb0 = tn * 256;
+    c.mb0 = tm * 256;
     c.nkb = g.K / 32;
     c.row_bytes = g.K / 2;
     c.nst = g.K / 128;
