@@ -875,63 +875,33 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
     }
 }
 
-// Matrix-core KroQuant with K read from the pack, one 64-block unit per wave
-// (no loop): few live registers, so every wave of a large grid is resident
-// at once and all input loads are in flight from the start.  FLAT: unit =
-// blockIdx.x;  COLUMN: column block j = blockIdx.x % nb, rows 64 * (blockIdx.x / nb).
-//
-// Binade-edge test.  With e the error of this path and of the fixed order
-// (|e| <= 116 u sum_k |K_nk||x_k| <= 116 u ||K||_inf max|x|, u = 2^-24) and
-// max|x| <= ||K^-1||_inf max|Kx| <= ||K^-1||_inf (amax + |e|), the two amax
-// differ by at most 116 u cond (1 - 104 u cond)^-1 amax <= 2^-17 cond amax =
-// rho amax whenever cond = cond_inf(K) <= 2^13.  amax = (1 + f) 2^E with
-// f = mantissa / 2^23, so amax - 2^E <= rho amax implies f <= 2 rho and
-// 2^(E+1) - amax <= rho amax implies 1 - f <= 2 rho: a block is re-evaluated in
-// the fixed order when its amax mantissa lies within T = ceil(2^24 rho) of 0 or
-// of 2^23 (T from the pack; T = 2^22 flags every block, used above cond 2^13),
-// or when amax < 2^-123, so its E8M0 scale equals the fixed-order one.
-template <Mapping MAP, int NA, int NB, bool ILV>
-__global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
-    __shared__ uint4 lds[256];
+// The body for one unit: FULL = all 64 blocks present (no per-tile bounds
+// tests in the straight-line code), WY = the fp32 transformed values are
+// stored too.  Codes and scales are always written.
+template <Mapping MAP, int NA, int NB, bool ILV, bool WY, bool FULL>
+__device__ __forceinline__ void unit_body(const Params& p, uint4* lds, int64_t jcol, int64_t first, int nvalid_rt,
+                                          uint32_t bstride) {
     const int lane = threadIdx.x;
     const int h = lane >> 5, jl = lane & 31;
-    int64_t jcol = 0, u = blockIdx.x, first;
-    int nvalid;
-    uint32_t bstride;
-    if (MAP == Mapping::Flat) {
-        first = u * 64;
-        nvalid = (int)min<int64_t>(64, p.nblocks - first);
-        bstride = 1;
-    } else {
-        jcol = u % p.nb;
-        const int64_t row0 = (u / p.nb) * 64;
-        first = row0 * p.nb + jcol;
-        nvalid = (int)min<int64_t>(64, p.M - row0);
-        bstride = (uint32_t)p.nb;
-    }
+    const int nvalid = FULL ? 64 : nvalid_rt;
     // chunk 64c + lane of the unit (block (64c + lane) / 4, chunk (64c + lane) % 4
     // of that block) goes to LDS slot 64c + wslot (lds_slot is additive in c here)
     const uint4* src = reinterpret_cast<const uint4*>(p.X) + first * 4;
     const int wslot = lds_slot(lane >> 2, lane & 3);
-    {
-        uint4 v[4];
-        if (nvalid == 64) {
+    uint4 v[4];
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const uint32_t ci = 64 * c + lane;
-                v[c] = load_nt(src + (MAP == Mapping::Flat ? ci : (ci >> 2) * bstride * 4 + (ci & 3)));
-            }
+    for (int c = 0; c < 4; ++c) {
+        const uint32_t ci = 64 * c + lane;
+        const uint32_t off = MAP == Mapping::Flat ? ci : (ci >> 2) * bstride * 4 + (ci & 3);
+        if (FULL) {
+            v[c] = load_nt(src + off);
         } else {
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const uint32_t ci = 64 * c + lane;
-                v[c] = make_uint4(0u, 0u, 0u, 0u);
-                if ((int)(ci >> 2) < nvalid) v[c] = load_nt(src + ((ci >> 2) * bstride * 4 + (ci & 3)));
-            }
+            v[c] = make_uint4(0u, 0u, 0u, 0u);
+            if ((int)(ci >> 2) < nvalid) v[c] = load_nt(src + off);
         }
-#pragma unroll
-        for (int c = 0; c < 4; ++c) lds[wslot + 64 * c] = v[c];
     }
+    // the input loads leave first; the K slices (L2-resident) follow them
+    __builtin_amdgcn_sched_barrier(0);
     const int64_t f = (p.nfac == 1) ? 0 : jcol;
     // K slice i (i = 2 term + k-step) of this lane at byte 1024 i + 16 lane of the
     // pack: one uniform base 2 KiB in, so every offset fits the load's immediate
@@ -956,30 +926,45 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
     // output bases of the unit (wave-uniform) and this lane's block offsets
     uint8_t* const codes_u = p.codes + first * 16;
     uint8_t* const scales_u = p.scales + first;
-    float* const y_u = p.y + first * 32;
+    float* const y_u = WY ? p.y + first * 32 : nullptr;
+    // every chunk goes to LDS as soon as it arrives
+#pragma unroll
+    for (int c = 0; c < 4; ++c) lds[wslot + 64 * c] = v[c];
     // lane (jl, h) reads chunks h and 2 + h of block 32 t + jl: slots 128 t + rslot
     // and 128 t + (rslot ^ 2)
     const int rslot = 4 * jl + (h ^ ((jl >> 2) & 3));
     wave_lds_sync();
+    uint4 raw[2][2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        raw[t][0] = lds[128 * t + rslot];
+        raw[t][1] = lds[128 * t + (rslot ^ 2)];
+    }
     uint64_t edges = 0;  // blocks of the unit on a binade edge (bit = block index)
     // the three terms, smallest first, of tile t: acc[n][block] += K[n][k-step] . x[block][k-step]
-    auto product = [&](const uint4 (&raw)[2]) {
+    auto product = [&](const uint4 (&r)[2]) {
         f32x16 acc = {};
 #pragma unroll
         for (int s = 0; s < 2; ++s)
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.lo[s], __builtin_bit_cast(bf16x8, raw[s]), acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.lo[s], __builtin_bit_cast(bf16x8, r[s]), acc, 0, 0, 0);
 #pragma unroll
         for (int s = 0; s < 2; ++s)
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.mid[s], __builtin_bit_cast(bf16x8, raw[s]), acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.mid[s], __builtin_bit_cast(bf16x8, r[s]), acc, 0, 0, 0);
 #pragma unroll
         for (int s = 0; s < 2; ++s)
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.hi[s], __builtin_bit_cast(bf16x8, raw[s]), acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.hi[s], __builtin_bit_cast(bf16x8, r[s]), acc, 0, 0, 0);
         return acc;
     };
-    // amax, binade-edge flag, scale, codes and stores of tile t
-    auto epilogue = [&](int t, const f32x16& acc, const uint4 (&raw)[2]) {
+    // amax, binade-edge flag, scale and codes of tile t (its y is stored at
+    // once); the code and scale stores of both tiles come after both products
+    struct TileOut {
+        uint2 codes;
+        uint32_t sb;
+        bool store;
+    };
+    auto finish = [&](int t, const f32x16& acc, const uint4 (&r)[2]) {
         const int bt = 32 * t + jl;
-        const bool valid = bt < nvalid;
+        const bool valid = FULL || bt < nvalid;
         // lane holds y[16h + i] of block bt in acc[i]
         float am = 0.0f;
 #pragma unroll
@@ -988,53 +973,95 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
         bool near = valid && (((amb + edge_t) & 0x7FFFFFu) <= 2u * edge_t || amb < (4u << 23));
         if (amb == 0u && zero_ok) {
             // all outputs +-0: exact when the inputs are all +0 (bit patterns 0)
-            const uint32_t any = raw[0].x | raw[0].y | raw[0].z | raw[0].w | raw[1].x | raw[1].y | raw[1].z | raw[1].w;
+            const uint32_t any = r[0].x | r[0].y | r[0].z | r[0].w | r[1].x | r[1].y | r[1].z | r[1].w;
             if ((any | other_half(any)) == 0u) near = false;
         }
-        const uint32_t sb = max(amb >> 23, 2u) - 2u;
-        const float sc = __uint_as_float(sb << 23);
-        const uint2 out = make_uint2(codes8(acc, 0, sc, amb), codes8(acc, 8, sc, amb));
-        const uint32_t ob = (uint32_t)bt * bstride;  // this lane's block, relative to `first`
-        if (valid && !near) {
-            if (p.codes) {
-                *reinterpret_cast<uint2*>(codes_u + (ob * 16u + 8u * h)) = out;
-                if (h == 0) scales_u[ob] = (uint8_t)sb;
-            }
-            if (p.y) {
-                float* yb = y_u + (ob * 32u + 16u * h);
+        TileOut o;
+        o.sb = max(amb >> 23, 2u) - 2u;
+        const float sc = __uint_as_float(o.sb << 23);
+        o.codes = make_uint2(codes8(acc, 0, sc, amb), codes8(acc, 8, sc, amb));
+        o.store = valid && !near;
+        if (WY && o.store) {
+            float* yb = y_u + ((uint32_t)bt * bstride * 32u + 16u * h);
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    *reinterpret_cast<float4*>(yb + 4 * q) =
-                        make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
-            }
+            for (int q = 0; q < 4; ++q)
+                *reinterpret_cast<float4*>(yb + 4 * q) =
+                    make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
         }
         edges |= (__builtin_amdgcn_ballot_w64(near) & 0xFFFFFFFFull) << (32 * t);
+        return o;
+    };
+    auto store = [&](int t, const TileOut& o) {
+        const uint32_t ob = (uint32_t)(32 * t + jl) * bstride;  // this lane's block, relative to `first`
+        if (o.store) {
+            *reinterpret_cast<uint2*>(codes_u + (ob * 16u + 8u * h)) = o.codes;
+            if (h == 0) scales_u[ob] = (uint8_t)o.sb;
+        }
     };
     if (ILV && nvalid > 32) {
         // both tiles' products first (two accumulators): the second chain runs
         // on the matrix cores while the first tile's epilogue is on the VALU
-        uint4 raw[2][2];
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-            raw[t][0] = lds[128 * t + rslot];
-            raw[t][1] = lds[128 * t + (rslot ^ 2)];
-        }
         const f32x16 acc0 = product(raw[0]);
         const f32x16 acc1 = product(raw[1]);
-        epilogue(0, acc0, raw[0]);
-        epilogue(1, acc1, raw[1]);
+        const TileOut o0 = finish(0, acc0, raw[0]);
+        const TileOut o1 = finish(1, acc1, raw[1]);
+        store(0, o0);
+        store(1, o1);
+    } else if (FULL) {
+        const TileOut o0 = finish(0, product(raw[0]), raw[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        const TileOut o1 = finish(1, product(raw[1]), raw[1]);
+        __builtin_amdgcn_sched_barrier(0);
+        store(0, o0);
+        store(1, o1);
     } else {
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-            if (32 * t >= nvalid) break;
-            uint4 raw[2];
-            raw[0] = lds[128 * t + rslot];
-            raw[1] = lds[128 * t + (rslot ^ 2)];
-            epilogue(t, product(raw), raw);
-        }
+        store(0, finish(0, product(raw[0]), raw[0]));
+        if (nvalid > 32) store(1, finish(1, product(raw[1]), raw[1]));
     }
     // blocks whose amax is on a binade edge: the fixed evaluation order decides
     exact_flagged<NA, NB>(edges, lds, first, bstride, p.A + f * (NA * NA), p.B + f * (NB * NB), p);
+}
+
+// Matrix-core KroQuant with K read from the pack, one 64-block unit per wave
+// (no loop): few live registers, so every wave of a large grid is resident
+// at once and all input loads are in flight from the start.  FLAT: unit =
+// blockIdx.x;  COLUMN: column block j = blockIdx.x % nb, rows 64 * (blockIdx.x / nb).
+// Per wave: the four input loads are issued first, then the K slices; all
+// four chunks go through LDS; both 32-block tiles are multiplied and encoded
+// back to back and their code and scale stores issued last.
+//
+// Binade-edge test.  With e the error of this path and of the fixed order
+// (|e| <= 116 u sum_k |K_nk||x_k| <= 116 u ||K||_inf max|x|, u = 2^-24) and
+// max|x| <= ||K^-1||_inf max|Kx| <= ||K^-1||_inf (amax + |e|), the two amax
+// differ by at most 116 u cond (1 - 104 u cond)^-1 amax <= 2^-17 cond amax =
+// rho amax whenever cond = cond_inf(K) <= 2^13.  amax = (1 + f) 2^E with
+// f = mantissa / 2^23, so amax - 2^E <= rho amax implies f <= 2 rho and
+// 2^(E+1) - amax <= rho amax implies 1 - f <= 2 rho: a block is re-evaluated in
+// the fixed order when its amax mantissa lies within T = ceil(2^24 rho) of 0 or
+// of 2^23 (T from the pack; T = 2^22 flags every block, used above cond 2^13),
+// or when amax < 2^-123, so its E8M0 scale equals the fixed-order one.
+template <Mapping MAP, int NA, int NB, bool ILV, bool WY>
+__global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
+    __shared__ uint4 lds[256];
+    const int64_t u = blockIdx.x;
+    int64_t jcol = 0, first;
+    int nvalid;
+    uint32_t bstride;
+    if (MAP == Mapping::Flat) {
+        first = u * 64;
+        nvalid = (int)min<int64_t>(64, p.nblocks - first);
+        bstride = 1;
+    } else {
+        jcol = u % p.nb;
+        const int64_t row0 = (u / p.nb) * 64;
+        first = row0 * p.nb + jcol;
+        nvalid = (int)min<int64_t>(64, p.M - row0);
+        bstride = (uint32_t)p.nb;
+    }
+    if (nvalid == 64)
+        unit_body<MAP, NA, NB, ILV, WY, true>(p, lds, jcol, first, 64, bstride);
+    else
+        unit_body<MAP, NA, NB, ILV, WY, false>(p, lds, jcol, first, nvalid, bstride);
 }
 
 // Materialise and split K = A (x) B for every factor pair, in the lane layout
@@ -1286,6 +1313,19 @@ static hipError_t launch_mfma_u(Params p, Mapping map, hipStream_t st, const Lau
     return hipGetLastError();
 }
 
+template <Mapping MAP, int NA, int NB>
+static hipError_t launch_unit(const Params& p, int64_t units, bool ilv, hipStream_t st) {
+    const dim3 g((unsigned)units), b(64);
+    if (ilv) {
+        if (p.y) hipLaunchKernelGGL((kron_mfma_unit_kernel<MAP, NA, NB, true, true>), g, b, 0, st, p);
+        else hipLaunchKernelGGL((kron_mfma_unit_kernel<MAP, NA, NB, true, false>), g, b, 0, st, p);
+    } else {
+        if (p.y) hipLaunchKernelGGL((kron_mfma_unit_kernel<MAP, NA, NB, false, true>), g, b, 0, st, p);
+        else hipLaunchKernelGGL((kron_mfma_unit_kernel<MAP, NA, NB, false, false>), g, b, 0, st, p);
+    }
+    return hipGetLastError();
+}
+
 template <int NA, int NB>
 static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
     if (p.kpack) {
@@ -1294,18 +1334,8 @@ static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st, cons
                 (map == Mapping::Flat) ? (p.nblocks + 63) / 64 : ((p.M + 63) / 64) * p.nb;
             // small grids (few waves per SIMD) hide less latency: interleave the two tiles
             const bool ilv = units <= cfg.interleave_max_units;
-            if (map == Mapping::Flat) {
-                if (ilv)
-                    hipLaunchKernelGGL((kron_mfma_unit_kernel<Mapping::Flat, NA, NB, true>), dim3((unsigned)units), dim3(64), 0, st, p);
-                else
-                    hipLaunchKernelGGL((kron_mfma_unit_kernel<Mapping::Flat, NA, NB, false>), dim3((unsigned)units), dim3(64), 0, st, p);
-            } else {
-                if (ilv)
-                    hipLaunchKernelGGL((kron_mfma_unit_kernel<Mapping::Column, NA, NB, true>), dim3((unsigned)units), dim3(64), 0, st, p);
-                else
-                    hipLaunchKernelGGL((kron_mfma_unit_kernel<Mapping::Column, NA, NB, false>), dim3((unsigned)units), dim3(64), 0, st, p);
-            }
-            return hipGetLastError();
+            if (map == Mapping::Flat) return launch_unit<Mapping::Flat, NA, NB>(p, units, ilv, st);
+            return launch_unit<Mapping::Column, NA, NB>(p, units, ilv, st);
         }
         if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, true>(p, map, st, cfg);
         return launch_mfma_u<NA, NB, 1, true>(p, map, st, cfg);
