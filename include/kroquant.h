@@ -219,6 +219,21 @@ kq_status kq_mxfp4_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* co
                             uint8_t* scales, void* stream);
 
 /*
+ * kq_stream_floor -- a measurement aid, not part of the method: the memory
+ * traffic of the quantizers above with no arithmetic, for timing the floor
+ * their launch shape and bytes alone set (2 bytes read, 17/32 byte written
+ * per element, one wave per 64 blocks, the same nontemporal loads).  For
+ * every 32-element block k of X it writes out16[16 k .. 16 k + 15] = the XOR
+ * of the block's four 16-byte chunks and out1[k] = the low byte of
+ * (word 0 XOR word 1) of that XOR (little-endian words).  X as for
+ * kq_mxfp4_quantize (device bf16 [M, d], d a positive multiple of 32, 16-byte
+ * aligned); out16 device [M, d/2] (16-byte aligned), out1 device [M, d/32].
+ * Errors as kq_mxfp4_quantize; M = 0 is a no-op.  Enqueued on `stream`; no
+ * allocation, no synchronization.
+ */
+kq_status kq_stream_floor(const uint16_t* X, int64_t M, int64_t d, uint8_t* out16, uint8_t* out1, void* stream);
+
+/*
  * kq_e2m1_encode -- the element-encode step alone, for checking the device
  * conversion: codes[i] = code(v[2i]) | code(v[2i+1]) << 4 at E8M0 byte s
  * (0..254), with the rounding rule above.  v device fp32 [n], n even;

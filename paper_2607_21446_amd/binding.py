@@ -22,6 +22,7 @@ STATUS = {
 EXPORTED = (
     "kq_quantize", "kq_quantize_exact", "kq_quantize_packed", "kq_pack_factors", "kq_quantize_lu",
     "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_fwht_quantize", "kq_mxfp4_quantize", "kq_mxfp4_gemm",
+    "kq_stream_floor",
     "kq_e2m1_encode", "kq_weight_transform", "kq_factors_inverse_transpose", "kq_lu_to_factors",
     "kq_calib_workspace_size", "kq_calib_reference", "kq_calib_step", "kq_calibrate",
     "kq_status_string", "kq_last_error_detail", "kq_version",
@@ -54,6 +55,7 @@ def lib() -> ctypes.CDLL:
     L.kq_fwht_quantize.argtypes = [P, I64, I64, P, P, P, P]
     L.kq_mxfp4_gemm.argtypes = [P, P, I64, P, P, I64, I64, P, I64, I, P]
     L.kq_mxfp4_quantize.argtypes = [P, I64, I64, P, P, P]
+    L.kq_stream_floor.argtypes = [P, I64, I64, P, P, P]
     L.kq_e2m1_encode.argtypes = [P, I64, I, P, P]
     L.kq_weight_transform.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P]
     L.kq_factors_inverse_transpose.argtypes = [P, P, I, I, I64, P, P]
@@ -252,6 +254,15 @@ def mxfp4(X, codes=None, scales=None, stream=None):
     _check(lib().kq_mxfp4_quantize(_ptr(X), M, d, _ptr(codes), _ptr(scales), _stream(stream)),
            "kq_mxfp4_quantize")
     return codes, scales
+
+
+def stream_floor(X, out16=None, out1=None, stream=None):
+    """kq_stream_floor: the quantizers' traffic with no arithmetic (a timing aid)."""
+    _need(X, torch.bfloat16, "X")
+    out16, out1, _ = _outputs(X, out16, out1, None, False)
+    M, d = X.shape
+    _check(lib().kq_stream_floor(_ptr(X), M, d, _ptr(out16), _ptr(out1), _stream(stream)), "kq_stream_floor")
+    return out16, out1
 
 
 def e2m1_encode(v, s, codes=None, stream=None):

@@ -286,6 +286,16 @@ kq_status kq_fwht_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* cod
     return from_hip(kq::launch_fwht(p, (hipStream_t)stream), "kq_fwht_quantize");
 }
 
+kq_status kq_stream_floor(const uint16_t* X, int64_t M, int64_t d, uint8_t* out16, uint8_t* out1, void* stream) {
+    kq_status st = check_common(X, M, d, out16, out1, nullptr, true);
+    if (st != KQ_SUCCESS) return st;
+    if (M == 0) return ok();
+    kq::Params p = make_params(X, M, d, out16, out1, nullptr);
+    if (p.nblocks / 64 >= (int64_t)1 << 31)
+        return fail(KQ_ERROR_INVALID_VALUE, "M * d = %lld * %lld is too large for one launch", (long long)M, (long long)d);
+    return from_hip(kq::launch_stream_floor(p, (hipStream_t)stream), "kq_stream_floor");
+}
+
 static kq::GemmParams gemm_params(const uint8_t* a_codes, const uint8_t* a_scales, int64_t M, const uint8_t* b_codes,
                                   const uint8_t* b_scales, int64_t N, int64_t K, float* C, int64_t ldc, int accumulate,
                                   const float* bias) {

@@ -64,5 +64,6 @@ hipError_t launch_mxfp4_gemm(const GemmParams& g, hipStream_t st);
 hipError_t launch_pack(int a, const float* A, const float* B, int64_t nfac, uint8_t* kpack, hipStream_t st);
 hipError_t launch_e2m1(const float* v, int64_t npairs, uint32_t s, uint8_t* codes, hipStream_t st);
 hipError_t launch_fwht(const Params& p, hipStream_t st);  // d a power of two, 32 .. 16384
+hipError_t launch_stream_floor(const Params& p, hipStream_t st);  // traffic of the quantizers, no arithmetic
 
 }  // namespace kq

@@ -1167,6 +1167,49 @@ __global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ A, c
     }
 }
 
+// The quantizers' memory traffic with no arithmetic: one wave per 64-block
+// unit reads its 4 KiB with the same four nontemporal 1 KiB loads and writes
+// 16 bytes and one byte per block (the XOR of the block's four 16-byte
+// chunks and the low byte of that XOR's first two words), so the time of this
+// kernel is what the launch shape and the bytes alone cost.
+__global__ __launch_bounds__(64) void stream_floor_kernel(const Params p) {
+    const int lane = threadIdx.x;
+    const int64_t first = (int64_t)blockIdx.x * 64;
+    const int nvalid = (int)min<int64_t>(64, p.nblocks - first);
+    const uint4* src = reinterpret_cast<const uint4*>(p.X) + first * 4;
+    uint4 v[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const int ci = 64 * c + lane;
+        v[c] = make_uint4(0u, 0u, 0u, 0u);
+        if ((ci >> 2) < nvalid) v[c] = load_nt(src + ci);
+    }
+    // lane l holds chunk l % 4 of block 16 c + l / 4 of load c; fold the four
+    // chunks of each block into the lane that owns it after the fold: the XOR
+    // over lanes 4 k .. 4 k + 3 (DPP quad reductions) lands in lane 4 k
+    uint4 r[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        uint32_t w[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            w[i] ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w[i], 0xB1, 0xF, 0xF, false);  // lane ^ 1
+            w[i] ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w[i], 0x4E, 0xF, 0xF, false);  // lane ^ 2
+        }
+        r[c] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+    if ((lane & 3) == 0) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int b = 16 * c + (lane >> 2);
+            if (b < nvalid) {
+                *reinterpret_cast<uint4*>(p.codes + (first + b) * 16) = r[c];
+                p.scales[first + b] = (uint8_t)(r[c].x ^ r[c].y);
+            }
+        }
+    }
+}
+
 // element encode alone (checks of the device conversion)
 __global__ __launch_bounds__(kThreads) void e2m1_kernel(const float* __restrict__ v, int64_t npairs,
                                                        uint32_t s, uint8_t* __restrict__ codes) {
@@ -1439,6 +1482,12 @@ hipError_t launch_fwht(const Params& p, hipStream_t st) {
         case 16384: return launch_fwht_n<14>(p, st);
         default: return hipErrorInvalidValue;
     }
+}
+
+hipError_t launch_stream_floor(const Params& p, hipStream_t st) {
+    const int64_t units = (p.nblocks + 63) / 64;
+    hipLaunchKernelGGL(stream_floor_kernel, dim3((unsigned)units), dim3(64), 0, st, p);
+    return hipGetLastError();
 }
 
 hipError_t launch_e2m1(const float* v, int64_t npairs, uint32_t s, uint8_t* codes, hipStream_t st) {

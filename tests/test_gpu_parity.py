@@ -144,6 +144,19 @@ def test_comparators_parity(M, d):
     assert_exact((host(c), host(s), None), (cr, sr, None), "mxfp4")
 
 
+@pytest.mark.parametrize("M,d", [(1, 32), (3, 64), (257, 1152), (130, 5600)])
+def test_stream_floor_outputs(M, d):
+    """kq_stream_floor (the traffic-only timing aid) writes, per block, the XOR
+    of its four 16-byte chunks and the low byte of that XOR's words 0 ^ 1;
+    ragged unit counts included."""
+    X = synth.activations(M, d, "normal", seed=M * d, chan_frac=0.0)
+    o16, o1 = kq.stream_floor(dev_bf16(X))
+    w = np.ascontiguousarray(X).view(np.uint32).reshape(M, d // 32, 4, 4)
+    fold = w[:, :, 0] ^ w[:, :, 1] ^ w[:, :, 2] ^ w[:, :, 3]
+    assert np.array_equal(host(o16).view(np.uint32).reshape(M, d // 32, 4), fold)
+    assert np.array_equal(host(o1), ((fold[:, :, 0] ^ fold[:, :, 1]) & 0xFF).astype(np.uint8))
+
+
 def test_tiny_config_all_paths():
     w = synth.workload("tiny_256x1152")
     want = oracle.quantize(w.X, w.A, w.B, want_y=True)

@@ -131,6 +131,10 @@ def test_comparators_reject():
     assert L.kq_smoothquant_quantize(FAKE, 4, 40, FAKE, FAKE, FAKE, None, None) == INVALID
     assert L.kq_hadamard32_quantize(FAKE, 4, 64, None, FAKE, None, None) == NULLP
     assert L.kq_mxfp4_quantize(FAKE + 2, 4, 64, FAKE, FAKE, None) == MISALIGNED
+    assert L.kq_stream_floor(FAKE + 2, 4, 64, FAKE, FAKE, None) == MISALIGNED
+    assert L.kq_stream_floor(FAKE, 4, 48, FAKE, FAKE, None) == INVALID
+    assert L.kq_stream_floor(FAKE, 4, 64, None, FAKE, None) == NULLP
+    assert L.kq_stream_floor(FAKE, 0, 64, FAKE, FAKE, None) == 0
     assert L.kq_e2m1_encode(FAKE, 3, 127, FAKE, None) == INVALID
     assert L.kq_e2m1_encode(FAKE, 4, 255, FAKE, None) == INVALID
     assert L.kq_e2m1_encode(FAKE, 4, -1, FAKE, None) == INVALID
