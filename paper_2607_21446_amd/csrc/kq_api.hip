@@ -89,6 +89,7 @@ kq::LaunchConfig default_config() {
             if (v >= 1 && v <= (1 << 30)) c.max_waves = v;
         }
         if (const char* e = std::getenv("KQ_PACKED_PERSISTENT")) c.packed_one_unit = std::atoi(e) == 0;
+        if (const char* e = std::getenv("KQ_ONTHEFLY_PERSISTENT")) c.build_unit = std::atoi(e) == 0;
         if (const char* e = std::getenv("KQ_SMOOTH_PATH")) {
             const int v = std::atoi(e);
             if (v >= 0 && v <= 3) c.smooth_path = v;

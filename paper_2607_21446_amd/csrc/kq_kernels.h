@@ -36,6 +36,7 @@ struct LaunchConfig {
     int64_t max_waves = 3072;               // workgroups (one wave each) of the on-the-fly matrix-core kernel
     int units_per_wave = 1;                 // 64-block units it loads per step (1 or 2)
     bool packed_one_unit = true;            // packed K: one unit per wave, no loop
+    bool build_unit = true;                 // K from the factors: built per 4-wave workgroup, one unit per wave
     int64_t interleave_max_units = 4096;    // packed K: interleave both tiles up to this many units
     int smooth_path = 3;                    // SmoothQuant layout: 0 chunk, 1 per-lane, 2 column, 3 stationary
     int64_t smooth_waves = 2048;            // target workgroups of the column-stationary SmoothQuant

@@ -590,7 +590,7 @@ __global__ __launch_bounds__(64) void smooth_stationary_kernel(const Params p) {
 template <int NA, int NB>
 __device__ __forceinline__ void exact_blocks_coop(const uint4* unit_lds, int blk0, int blk1, const float* Af,
                                                   const float* Bf, const Params& p, int64_t out0, int64_t out1) {
-    const int h = threadIdx.x >> 5;
+    const int h = (threadIdx.x >> 5) & 1;  // half of this wave (workgroups may hold several waves)
     const int n = threadIdx.x & 31;
     const int o = n / NB, i = n % NB;
     const int blk = h ? blk1 : blk0;
@@ -643,10 +643,8 @@ __device__ __forceinline__ void exact_flagged(uint64_t edges, const uint4* unit_
 // so A (x) B = (G_1 (x) ... (x) G_5)^T; every product left to right, one fp32
 // rounding per multiply, g11 = fma(c, b, -(1/a)).  The wave writes A then B
 // (NA*NA + NB*NB floats) to `out`; the parameters come in as scalar loads.
-template <int NA, int NB>
-__device__ __forceinline__ void decode_lu_factors(const float* lu, int lane, float* out) {
-    constexpr int na = NA == 1 ? 0 : NA == 2 ? 1 : NA == 4 ? 2 : 3;
-    float g[5][4];
+// The 2x2 factors G_k = [[g0, g1], [g2, g3]] from the parameters (wave-uniform, scalar loads).
+__device__ __forceinline__ void lu_g(const float* lu, float (&g)[5][4]) {
 #pragma unroll
     for (int k = 0; k < 5; ++k) {
         const float pa = ld_uniform(lu, 3 * k), pb = ld_uniform(lu, 3 * k + 1), pc = ld_uniform(lu, 3 * k + 2);
@@ -655,23 +653,33 @@ __device__ __forceinline__ void decode_lu_factors(const float* lu, int lane, flo
         g[k][2] = pc * pa;
         g[k][3] = __builtin_fmaf(pc, pb, -(1.0f / pa));
     }
-    for (int idx = lane; idx < NA * NA + NB * NB; idx += 64) {
-        const bool in_a = idx < NA * NA;
-        const int rowi = in_a ? idx / NA : (idx - NA * NA) / NB;  // o or i
-        const int coli = in_a ? idx % NA : (idx - NA * NA) % NB;  // p or q
-        float v = 1.0f;
-        bool first = true;
+}
+
+// Entry idx of A then B (idx < NA*NA + NB*NB), branch-free: factors outside
+// the entry's group multiply as exactly 1, so the product is the left-to-right
+// product of the entry's own G entries.
+template <int NA, int NB>
+__device__ __forceinline__ float lu_entry(const float (&g)[5][4], int idx) {
+    constexpr int na = NA == 1 ? 0 : NA == 2 ? 1 : NA == 4 ? 2 : 3;
+    const bool in_a = idx < NA * NA;
+    const int rowi = in_a ? idx / NA : (idx - NA * NA) / NB;  // o or i
+    const int coli = in_a ? idx % NA : (idx - NA * NA) % NB;  // p or q
+    float v = 1.0f;
 #pragma unroll
-        for (int k = 0; k < 5; ++k) {
-            if ((k < na) != in_a) continue;
-            const int sh = in_a ? na - 1 - k : 4 - k;
-            const int e = 2 * ((coli >> sh) & 1) + ((rowi >> sh) & 1);  // G_k[bit of col][bit of row]
-            const float ge = e == 0 ? g[k][0] : e == 1 ? g[k][1] : e == 2 ? g[k][2] : g[k][3];
-            v = first ? ge : v * ge;
-            first = false;
-        }
-        out[idx] = v;
+    for (int k = 0; k < 5; ++k) {
+        const int sh = k < na ? na - 1 - k : 4 - k;
+        const int e = 2 * ((coli >> sh) & 1) + ((rowi >> sh) & 1);  // G_k[bit of col][bit of row]
+        const float ge = e == 0 ? g[k][0] : e == 1 ? g[k][1] : e == 2 ? g[k][2] : g[k][3];
+        v *= ((k < na) == in_a) ? ge : 1.0f;
     }
+    return v;
+}
+
+template <int NA, int NB>
+__device__ __forceinline__ void decode_lu_factors(const float* lu, int lane, float* out) {
+    float g[5][4];
+    lu_g(lu, g);
+    for (int idx = lane; idx < NA * NA + NB * NB; idx += 64) out[idx] = lu_entry<NA, NB>(g, idx);
 }
 
 // Matrix-core KroQuant.  A wave handles U consecutive units per step (all
@@ -875,61 +883,78 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
     }
 }
 
-// The body for one unit: FULL = all 64 blocks present (no per-tile bounds
-// tests in the straight-line code), WY = the fp32 transformed values are
-// stored too.  Codes and scales are always written.
-template <Mapping MAP, int NA, int NB, bool ILV, bool WY, bool FULL>
-__device__ __forceinline__ void unit_body(const Params& p, uint4* lds, int64_t jcol, int64_t first, int nvalid_rt,
-                                          uint32_t bstride) {
-    const int lane = threadIdx.x;
+// Input loads of one 64-block unit (four nontemporal 1 KiB loads, chunk
+// 64 c + lane in v[c]); FULL = all 64 blocks present.  A partial unit
+// (0 <= nvalid < 64) issues the same four loads, each lane at a clamped
+// in-bounds address, and zeroes the chunks of missing blocks, so every path
+// has exactly four loads in flight (later waits can then count them).
+template <Mapping MAP, bool FULL>
+__device__ __forceinline__ void load_unit(const Params& p, int64_t first, int nvalid, uint32_t bstride, uint4 (&v)[4]) {
+    const int lane = threadIdx.x & 63;
+    const uint4* src = reinterpret_cast<const uint4*>(p.X) + (FULL || nvalid > 0 ? first * 4 : 0);
+    const uint32_t last = FULL ? 63u : (uint32_t)max(nvalid, 1) - 1u;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const uint32_t ci = 64 * c + lane;
+        const uint32_t b = FULL ? (ci >> 2) : min(ci >> 2, last);
+        const uint32_t off = MAP == Mapping::Flat ? (FULL ? ci : 4 * b + (ci & 3)) : b * bstride * 4 + (ci & 3);
+        const uint4 t = load_nt(src + off);
+        v[c] = (FULL || (int)(ci >> 2) < nvalid) ? t : make_uint4(0u, 0u, 0u, 0u);
+    }
+}
+
+// The same four loads for a unit of any size, with no branch and no select:
+// lanes of missing blocks read the unit's last present block (or block 0 of
+// X when the unit is empty); unit_compute zeroes them when it stages the
+// chunks.  Straight-line, so that a later wait for an older load can count
+// these four as still in flight.
+template <Mapping MAP>
+__device__ __forceinline__ void load_unit_clamped(const Params& p, int64_t first, int nvalid, uint32_t bstride,
+                                                  uint4 (&v)[4]) {
+    const int lane = threadIdx.x & 63;
+    const uint4* src = reinterpret_cast<const uint4*>(p.X) + (nvalid > 0 ? first * 4 : 0);
+    const uint32_t last = (uint32_t)max(nvalid, 1) - 1u;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const uint32_t ci = 64 * c + lane;
+        const uint32_t b = min(ci >> 2, last);
+        const uint32_t off = MAP == Mapping::Flat ? 4 * b + (ci & 3) : b * bstride * 4 + (ci & 3);
+        v[c] = load_nt(src + off);
+    }
+}
+
+// How a unit decides which blocks lie on a binade edge (see the kernels below).
+struct EdgeTest {
+    uint32_t edge_t;  // PACKED: mantissa window T from the pack
+    float kbound;     // otherwise: 2^-17 ||K||_inf (per-block window kbound * max|x|)
+};
+
+// The compute of one unit once its chunks are in v and the K slices in ks:
+// both 32-block tiles through LDS, multiplied, encoded and stored (codes and
+// scales last), binade-edge blocks re-evaluated in the fixed order.  FULL =
+// all 64 blocks present (no per-tile bounds tests in the straight-line
+// code); WY / WY16 = the fp32 / bf16 transformed values are stored too;
+// PACKED selects the edge test.  lds = this wave's 256-slot staging area;
+// Af, Bf = the factors (for the fixed-order fallback).
+template <Mapping MAP, int NA, int NB, bool ILV, bool WY, bool WY16, bool FULL, bool PACKED>
+__device__ __forceinline__ void unit_compute(const Params& p, uint4* lds, int64_t first, int nvalid_rt,
+                                             uint32_t bstride, const uint4 (&v)[4], const KSlices& ks, bool zero_ok,
+                                             EdgeTest et, const float* Af, const float* Bf) {
+    const int lane = threadIdx.x & 63;
     const int h = lane >> 5, jl = lane & 31;
     const int nvalid = FULL ? 64 : nvalid_rt;
     // chunk 64c + lane of the unit (block (64c + lane) / 4, chunk (64c + lane) % 4
     // of that block) goes to LDS slot 64c + wslot (lds_slot is additive in c here)
-    const uint4* src = reinterpret_cast<const uint4*>(p.X) + first * 4;
     const int wslot = lds_slot(lane >> 2, lane & 3);
-    uint4 v[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        const uint32_t ci = 64 * c + lane;
-        const uint32_t off = MAP == Mapping::Flat ? ci : (ci >> 2) * bstride * 4 + (ci & 3);
-        if (FULL) {
-            v[c] = load_nt(src + off);
-        } else {
-            v[c] = make_uint4(0u, 0u, 0u, 0u);
-            if ((int)(ci >> 2) < nvalid) v[c] = load_nt(src + off);
-        }
-    }
-    // the input loads leave first; the K slices (L2-resident) follow them
-    __builtin_amdgcn_sched_barrier(0);
-    const int64_t f = (p.nfac == 1) ? 0 : jcol;
-    // K slice i (i = 2 term + k-step) of this lane at byte 1024 i + 16 lane of the
-    // pack: one uniform base 2 KiB in, so every offset fits the load's immediate
-    const uint8_t* const pk0 = p.kpack + f * kPackBytes;
-    const uint8_t* const pkm = pk0 + 2048;
-    const uint32_t lo16 = 16u * (uint32_t)lane;
-    auto kslice = [&](int i) {
-        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(pkm + lo16 + (1024 * i - 2048)));
-    };
-    KSlices ks;
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-        ks.hi[s] = kslice(0 * 2 + s);
-        ks.mid[s] = kslice(1 * 2 + s);
-        ks.lo[s] = kslice(2 * 2 + s);
-    }
-    const float* hdr = reinterpret_cast<const float*>(pk0 + 6 * 64 * 16);
-    // nonzero when no row of A and no row of B has every sign bit set: then an
-    // all-(+0) input block gives +0 for every output in the fixed order
-    const bool zero_ok = __float_as_uint(ld_uniform(hdr, 2)) != 0u;
-    const uint32_t edge_t = __float_as_uint(ld_uniform(hdr, 3));
     // output bases of the unit (wave-uniform) and this lane's block offsets
     uint8_t* const codes_u = p.codes + first * 16;
     uint8_t* const scales_u = p.scales + first;
     float* const y_u = WY ? p.y + first * 32 : nullptr;
-    // every chunk goes to LDS as soon as it arrives
+    uint16_t* const y16_u = WY16 ? p.y16 + first * 32 : nullptr;
+    // every chunk goes to LDS as soon as it arrives (those of missing blocks as zeros)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) lds[wslot + 64 * c] = v[c];
+    for (int c = 0; c < 4; ++c)
+        lds[wslot + 64 * c] = (FULL || (64 * c + lane) / 4 < nvalid) ? v[c] : make_uint4(0u, 0u, 0u, 0u);
     // lane (jl, h) reads chunks h and 2 + h of block 32 t + jl: slots 128 t + rslot
     // and 128 t + (rslot ^ 2)
     const int rslot = 4 * jl + (h ^ ((jl >> 2) & 3));
@@ -965,12 +990,21 @@ __device__ __forceinline__ void unit_body(const Params& p, uint4* lds, int64_t j
     auto finish = [&](int t, const f32x16& acc, const uint4 (&r)[2]) {
         const int bt = 32 * t + jl;
         const bool valid = FULL || bt < nvalid;
-        // lane holds y[16h + i] of block bt in acc[i]
+        // lane holds y[16h + i] of block bt in acc[i]; values >= 0 compare as their bit patterns
         float am = 0.0f;
 #pragma unroll
         for (int i = 0; i < 16; ++i) am = fmaxf(am, fabsf(acc[i]));
         const uint32_t amb = max_with_other_half(__float_as_uint(am));
-        bool near = valid && (((amb + edge_t) & 0x7FFFFFu) <= 2u * edge_t || amb < (4u << 23));
+        bool near;
+        if (PACKED) {
+            near = valid && (((amb + et.edge_t) & 0x7FFFFFu) <= 2u * et.edge_t || amb < (4u << 23));
+        } else {
+            // window kbound * max|x| around both powers of two that bracket amax
+            const float bnd = et.kbound * __uint_as_float(max_with_other_half(__float_as_uint(max_abs_bf16(r))));
+            const uint32_t e = amb >> 23;
+            const float a = __uint_as_float(amb);
+            near = valid && (e <= 3u || a - __uint_as_float(e << 23) <= bnd || __uint_as_float((e + 1u) << 23) - a <= bnd);
+        }
         if (amb == 0u && zero_ok) {
             // all outputs +-0: exact when the inputs are all +0 (bit patterns 0)
             const uint32_t any = r[0].x | r[0].y | r[0].z | r[0].w | r[1].x | r[1].y | r[1].z | r[1].w;
@@ -987,6 +1021,13 @@ __device__ __forceinline__ void unit_body(const Params& p, uint4* lds, int64_t j
             for (int q = 0; q < 4; ++q)
                 *reinterpret_cast<float4*>(yb + 4 * q) =
                     make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
+        }
+        if (WY16 && o.store) {
+            uint4* yb = reinterpret_cast<uint4*>(y16_u + ((uint32_t)bt * bstride * 32u + 16u * h));
+#pragma unroll
+            for (int q = 0; q < 2; ++q)
+                yb[q] = make_uint4(bf16_pair(acc[8 * q], acc[8 * q + 1]), bf16_pair(acc[8 * q + 2], acc[8 * q + 3]),
+                                   bf16_pair(acc[8 * q + 4], acc[8 * q + 5]), bf16_pair(acc[8 * q + 6], acc[8 * q + 7]));
         }
         edges |= (__builtin_amdgcn_ballot_w64(near) & 0xFFFFFFFFull) << (32 * t);
         return o;
@@ -1007,19 +1048,60 @@ __device__ __forceinline__ void unit_body(const Params& p, uint4* lds, int64_t j
         const TileOut o1 = finish(1, acc1, raw[1]);
         store(0, o0);
         store(1, o1);
-    } else if (FULL) {
+    } else {
+        // straight-line for full and partial units alike: a partial unit's
+        // missing blocks hold zeros and are neither stored nor flagged
         const TileOut o0 = finish(0, product(raw[0]), raw[0]);
         __builtin_amdgcn_sched_barrier(0);
         const TileOut o1 = finish(1, product(raw[1]), raw[1]);
         __builtin_amdgcn_sched_barrier(0);
         store(0, o0);
         store(1, o1);
-    } else {
-        store(0, finish(0, product(raw[0]), raw[0]));
-        if (nvalid > 32) store(1, finish(1, product(raw[1]), raw[1]));
     }
     // blocks whose amax is on a binade edge: the fixed evaluation order decides
-    exact_flagged<NA, NB>(edges, lds, first, bstride, p.A + f * (NA * NA), p.B + f * (NB * NB), p);
+    exact_flagged<NA, NB>(edges, lds, first, bstride, Af, Bf, p);
+}
+
+// K slices and edge data of factor pair f from the pack (kq_pack_factors),
+// issued after the unit's input loads.
+__device__ __forceinline__ void packed_k(const Params& p, int64_t f, KSlices& ks, bool& zero_ok, EdgeTest& et) {
+    const int lane = threadIdx.x & 63;
+    // K slice i (i = 2 term + k-step) of this lane at byte 1024 i + 16 lane of the
+    // pack: one uniform base 2 KiB in, so every offset fits the load's immediate
+    const uint8_t* const pk0 = p.kpack + f * kPackBytes;
+    const uint8_t* const pkm = pk0 + 2048;
+    const uint32_t lo16 = 16u * (uint32_t)lane;
+    auto kslice = [&](int i) {
+        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(pkm + lo16 + (1024 * i - 2048)));
+    };
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        ks.hi[s] = kslice(0 * 2 + s);
+        ks.mid[s] = kslice(1 * 2 + s);
+        ks.lo[s] = kslice(2 * 2 + s);
+    }
+    const float* hdr = reinterpret_cast<const float*>(pk0 + 6 * 64 * 16);
+    // nonzero when no row of A and no row of B has every sign bit set: then an
+    // all-(+0) input block gives +0 for every output in the fixed order
+    zero_ok = __float_as_uint(ld_uniform(hdr, 2)) != 0u;
+    et.edge_t = __float_as_uint(ld_uniform(hdr, 3));
+    et.kbound = 0.0f;
+}
+
+template <Mapping MAP, int NA, int NB, bool ILV, bool WY, bool FULL>
+__device__ __forceinline__ void packed_unit(const Params& p, uint4* lds, int64_t jcol, int64_t first, int nvalid,
+                                            uint32_t bstride) {
+    uint4 v[4];
+    load_unit<MAP, FULL>(p, first, nvalid, bstride, v);
+    // the input loads leave first; the K slices (L2-resident) follow them
+    __builtin_amdgcn_sched_barrier(0);
+    const int64_t f = (p.nfac == 1) ? 0 : jcol;
+    KSlices ks;
+    bool zero_ok;
+    EdgeTest et;
+    packed_k(p, f, ks, zero_ok, et);
+    unit_compute<MAP, NA, NB, ILV, WY, false, FULL, true>(p, lds, first, nvalid, bstride, v, ks, zero_ok, et,
+                                                          p.A + f * (NA * NA), p.B + f * (NB * NB));
 }
 
 // Matrix-core KroQuant with K read from the pack, one 64-block unit per wave
@@ -1059,9 +1141,155 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
         bstride = (uint32_t)p.nb;
     }
     if (nvalid == 64)
-        unit_body<MAP, NA, NB, ILV, WY, true>(p, lds, jcol, first, 64, bstride);
+        packed_unit<MAP, NA, NB, ILV, WY, true>(p, lds, jcol, first, 64, bstride);
     else
-        unit_body<MAP, NA, NB, ILV, WY, false>(p, lds, jcol, first, nvalid, bstride);
+        packed_unit<MAP, NA, NB, ILV, WY, false>(p, lds, jcol, first, nvalid, bstride);
+}
+
+// Matrix-core KroQuant with K built on chip from the factors (kq_quantize)
+// or from the 15 LU parameters of G_1..G_5 (kq_quantize_lu): four waves per
+// workgroup, one 64-block unit each, all four sharing one factor pair.  Every
+// wave issues its input loads first; while they are in flight the workgroup
+// stages A and B in LDS (or decodes them, LU), builds the split K once (wave w
+// builds k-step w / 2, entries 4 (w % 2) .. 4 (w % 2) + 3 of every lane's
+// slice), and wave 0 computes ||A||_inf ||B||_inf and the all-(+0) flag; LDS
+// fences and bare barriers separate the phases so that no wait covers the
+// input loads.  Then each wave runs the unit as in the packed kernel, with
+// the binade-edge window 2^-17 ||K||_inf max|x| per block (||K||_inf =
+// ||A||_inf ||B||_inf, computed in fp32 and widened by 2^-16 relative).
+// FLAT: workgroup g = units 4 g .. 4 g + 3.  COLUMN: workgroup g = column
+// block j = g % nb, row units 4 (g / nb) .. + 3.  Trailing waves with no rows
+// take part in the build and return.
+template <Mapping MAP, int NA, int NB, bool LU, bool WY, bool WY16>
+__global__ __launch_bounds__(256) void kron_build_unit_kernel(const Params p) {
+    constexpr int NF = NA * NA + NB * NB;
+    __shared__ uint4 lds_x[4][256];   // per-wave input staging
+    __shared__ uint4 lds_k[3][2][64];  // split K: [term hi, mid, lo][k-step][lane]
+    __shared__ float fac[NF];          // A then B
+    __shared__ float hdr[2];           // ||K||_inf bound, all-(+0) flag
+    // the wave index as a uniform value, so that branches on the unit are scalar
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    int64_t jcol = 0, first;
+    int nvalid;
+    uint32_t bstride;
+    if (MAP == Mapping::Flat) {
+        first = ((int64_t)blockIdx.x * 4 + w) * 64;
+        nvalid = (int)max<int64_t>(0, min<int64_t>(64, p.nblocks - first));
+        bstride = 1;
+    } else {
+        jcol = blockIdx.x % p.nb;
+        const int64_t row0 = ((int64_t)(blockIdx.x / p.nb) * 4 + w) * 64;
+        first = row0 * p.nb + jcol;
+        nvalid = (int)max<int64_t>(0, min<int64_t>(64, p.M - row0));
+        bstride = (uint32_t)p.nb;
+    }
+    const int64_t f = (p.nfac == 1) ? 0 : jcol;
+    // the factor entries (NF <= 1040 < 256 * 5) are loaded before the input:
+    // loads retire in order, so waiting for them does not wait for the input
+    constexpr int FPT = (NF + 255) / 256;
+    float fv[LU ? 1 : FPT];
+    if (!LU) {
+#pragma unroll
+        for (int q = 0; q < FPT; ++q) {
+            // unconditional (clamped index), so no branch hides the load from the wait counting
+            const int i = min(threadIdx.x + 256 * q, (unsigned)NF - 1);
+            const float* src = i < NA * NA ? p.A + f * (NA * NA) + i : p.B + f * (NB * NB) + (i - NA * NA);
+            fv[q] = __builtin_nontemporal_load(src);
+        }
+    }
+    uint4 v[4];
+    load_unit_clamped<MAP>(p, first, nvalid, bstride, v);
+    __builtin_amdgcn_sched_barrier(0);
+    // phase 1: factors into LDS (LU: every thread decodes at most one entry)
+    if (LU) {
+        float g[5][4];
+        lu_g(p.lu + f * 15, g);
+#pragma unroll
+        for (int q = 0; q < FPT; ++q) {
+            const int i = threadIdx.x + 256 * q;
+            if (i < NF) fac[i] = lu_entry<NA, NB>(g, i);
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < FPT; ++q) {
+            const int i = threadIdx.x + 256 * q;
+            if (i < NF) fac[i] = fv[q];
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+    // phase 2: this wave's share of the split K; wave 0 also the norms and flag
+    {
+        const float* Af = fac;
+        const float* Bf = fac + NA * NA;
+        const int n = perm_row(lane & 31), hh = lane >> 5;
+        const int s = w >> 1, c0 = 4 * (w & 1);
+        bf16x2 hi[2], mid[2], lo[2];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int k = 16 * s + 8 * hh + c0 + c;
+            const float kv = Af[(n / NB) * NA + k / NB] * Bf[(n % NB) * NB + k % NB];
+            const __bf16 t1 = (__bf16)kv;
+            const float r1 = kv - (float)t1;  // exact
+            const __bf16 t2 = (__bf16)r1;
+            const float r2 = r1 - (float)t2;  // exact
+            hi[c >> 1][c & 1] = t1;
+            mid[c >> 1][c & 1] = t2;
+            lo[c >> 1][c & 1] = (__bf16)r2;
+        }
+        auto put = [&](int term, const bf16x2 (&q)[2]) {
+            uint2* dst = reinterpret_cast<uint2*>(&lds_k[term][s][lane]) + (w & 1);
+            *dst = make_uint2(__builtin_bit_cast(uint32_t, q[0]), __builtin_bit_cast(uint32_t, q[1]));
+        };
+        put(0, hi);
+        put(1, mid);
+        put(2, lo);
+        if (w == 0) {
+            // lane i < NA: row i of A; NA <= lane < NA + NB: row lane - NA of B
+            const bool in_a = lane < NA, in_b = lane >= NA && lane < NA + NB;
+            const int len = in_a ? NA : NB;
+            const float* row = in_a ? Af + lane * NA : Bf + (lane - NA) * NB;
+            float rs = 0.0f;
+            bool allneg = in_a || in_b;
+            if (in_a || in_b) {
+                for (int j = 0; j < len; ++j) {
+                    rs += fabsf(row[j]);
+                    allneg = allneg && (__float_as_uint(row[j]) >> 31);
+                }
+            }
+            float ra = in_a ? rs : 0.0f, rb = in_b ? rs : 0.0f;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) {
+                ra = fmaxf(ra, __shfl_xor(ra, off));
+                rb = fmaxf(rb, __shfl_xor(rb, off));
+            }
+            const bool zero_ok = __builtin_amdgcn_ballot_w64(allneg) == 0;
+            if (lane == 0) {
+                hdr[0] = ra * rb * 0x1.0001p-17f;
+                hdr[1] = zero_ok ? 1.0f : 0.0f;
+            }
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+    if (nvalid == 0) return;
+    // phase 3: this lane's K slices, then the unit (one straight-line body for
+    // full and partial units: fewer live registers than two specialised copies)
+    KSlices ks;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        ks.hi[s] = __builtin_bit_cast(bf16x8, lds_k[0][s][lane]);
+        ks.mid[s] = __builtin_bit_cast(bf16x8, lds_k[1][s][lane]);
+        ks.lo[s] = __builtin_bit_cast(bf16x8, lds_k[2][s][lane]);
+    }
+    EdgeTest et;
+    et.edge_t = 0u;
+    et.kbound = hdr[0];
+    const bool zero_ok = hdr[1] != 0.0f;
+    unit_compute<MAP, NA, NB, false, WY, WY16, false, false>(p, lds_x[w], first, nvalid, bstride, v, ks, zero_ok, et,
+                                                             fac, fac + NA * NA);
 }
 
 // Materialise and split K = A (x) B for every factor pair, in the lane layout
@@ -1369,12 +1597,32 @@ static hipError_t launch_unit(const Params& p, int64_t units, bool ilv, hipStrea
     return hipGetLastError();
 }
 
+// The on-chip-K unit kernel: four units per workgroup (one factor pair each).
+template <int NA, int NB, bool LU>
+static hipError_t launch_build(const Params& p, Mapping map, hipStream_t st) {
+    const int64_t g = (map == Mapping::Flat) ? ((p.nblocks + 63) / 64 + 3) / 4 : (((p.M + 63) / 64 + 3) / 4) * p.nb;
+    const dim3 grid((unsigned)g), b(256);
+    const bool wy = p.y != nullptr, wy16 = LU && p.y16 != nullptr;
+#define KQ_BUILD(MAP, WY, WY16) hipLaunchKernelGGL((kron_build_unit_kernel<MAP, NA, NB, LU, WY, WY16>), grid, b, 0, st, p)
+    if (map == Mapping::Flat) {
+        if (wy16) { if (wy) KQ_BUILD(Mapping::Flat, true, LU); else KQ_BUILD(Mapping::Flat, false, LU); }
+        else { if (wy) KQ_BUILD(Mapping::Flat, true, false); else KQ_BUILD(Mapping::Flat, false, false); }
+    } else {
+        if (wy16) { if (wy) KQ_BUILD(Mapping::Column, true, LU); else KQ_BUILD(Mapping::Column, false, LU); }
+        else { if (wy) KQ_BUILD(Mapping::Column, true, false); else KQ_BUILD(Mapping::Column, false, false); }
+    }
+#undef KQ_BUILD
+    return hipGetLastError();
+}
+
+// grids of more workgroups than this take the grid-stride kernels
+constexpr int64_t kMaxUnitGrid = (int64_t(1) << 31) - 1;
+
 template <int NA, int NB>
 static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
+    const int64_t units = (map == Mapping::Flat) ? (p.nblocks + 63) / 64 : ((p.M + 63) / 64) * p.nb;
     if (p.kpack) {
-        if (cfg.packed_one_unit) {
-            const int64_t units =
-                (map == Mapping::Flat) ? (p.nblocks + 63) / 64 : ((p.M + 63) / 64) * p.nb;
+        if (cfg.packed_one_unit && units <= kMaxUnitGrid) {
             // small grids (few waves per SIMD) hide less latency: interleave the two tiles
             const bool ilv = units <= cfg.interleave_max_units;
             if (map == Mapping::Flat) return launch_unit<Mapping::Flat, NA, NB>(p, units, ilv, st);
@@ -1383,12 +1631,15 @@ static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st, cons
         if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, true>(p, map, st, cfg);
         return launch_mfma_u<NA, NB, 1, true>(p, map, st, cfg);
     }
+    if (cfg.build_unit && units <= kMaxUnitGrid) return launch_build<NA, NB, false>(p, map, st);
     if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, false>(p, map, st, cfg);
     return launch_mfma_u<NA, NB, 1, false>(p, map, st, cfg);
 }
 
 template <int NA, int NB>
 static hipError_t launch_lu(const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
+    const int64_t units = (map == Mapping::Flat) ? (p.nblocks + 63) / 64 : ((p.M + 63) / 64) * p.nb;
+    if (cfg.build_unit && units <= kMaxUnitGrid) return launch_build<NA, NB, true>(p, map, st);
     if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, false, true>(p, map, st, cfg);
     return launch_mfma_u<NA, NB, 1, false, true>(p, map, st, cfg);
 }
