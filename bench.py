@@ -83,6 +83,8 @@ def parse():
     ap.add_argument("--no-calib", action="store_true", help="skip the layer-wise calibration timing")
     ap.add_argument("--calib-samples", type=int, default=128,
                     help="calibration samples of 4608 tokens for the calibration timing")
+    ap.add_argument("--no-wide", action="store_true",
+                    help="skip the second FLUX shape, X [4608, 12288] (the MLP down-projection input)")
     ap.add_argument("--no-table2", action="store_true",
                     help="skip the power-of-two-d comparison (Q4, Scale, K1, K2, FWHT) at the paper's Table 2 shapes")
     return ap.parse_args()
@@ -309,6 +311,7 @@ def main():
     ms_floor_eager, _ = timed_eager(run_floor, args.steps, args.warmup)
     ms_warm, _ = timed(run_kq, args.steps, args.warmup, rotate=False)
     table2 = None if args.no_table2 else table2_shapes(kq, synth, dev, stream, sptr)
+    wide = None if args.no_wide else wide_shape(kq, synth, dev, stream, timed_graph_steps=args.steps)
     gemm = None if args.no_gemm else gemm_timing(kq, synth, dev, stream, sptr, Cs[0], Ss[0], M, d)
     calib = None if args.no_calib else calib_timing(kq, synth, dev, stream, sptr, args.calib_samples)
     dist = per_launch(run_kq)
@@ -367,11 +370,63 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
         "cpu_baseline": cpu,
+        "flux_4608x12288": wide,
         "table2_pow2_d": table2,
         "w4a4_gemm": gemm,
         "calibration": calib,
     }
     print(json.dumps(line), flush=True)
+
+
+def wide_shape(kq, synth, dev, stream, timed_graph_steps=1000, warmup=1000):
+    """The other FLUX.1-schnell activation shape, X bf16 [4608, 12288] (input of
+    the MLP down-projection; 143 MB per step): the hot path, SmoothQuant, plain
+    MXFP4 and the traffic-only kernel, each as K launches captured into a HIP
+    graph (MALL-cold rotation) replayed between HIP events."""
+    import torch
+    w = synth.workload("flux_4608x12288")
+    M, d = w.X.shape
+    nbytes = algorithmic_bytes(M, d)
+    nsets = max(2, int(np.ceil(2 * MALL_BYTES / nbytes)) + 1)
+    X0 = torch.from_numpy(w.X.view(np.int16)).view(torch.bfloat16).to(dev)
+    Xs = [X0.clone() for _ in range(nsets)]
+    Cs = [torch.empty((M, d // 2), dtype=torch.uint8, device=dev) for _ in range(nsets)]
+    Ss = [torch.empty((M, d // 32), dtype=torch.uint8, device=dev) for _ in range(nsets)]
+    A, B = torch.from_numpy(w.A).to(dev), torch.from_numpy(w.B).to(dev)
+    mult = torch.from_numpy(w.mult).to(dev)
+    kpack = kq.pack_factors(A, B)
+    fns = {
+        "kroquant": lambda i: kq.quantize_packed(Xs[i], A, B, kpack, codes=Cs[i], scales=Ss[i]),
+        "smoothquant": lambda i: kq.smoothquant(Xs[i], mult, codes=Cs[i], scales=Ss[i]),
+        "mxfp4": lambda i: kq.mxfp4(Xs[i], codes=Cs[i], scales=Ss[i]),
+        "stream_floor": lambda i: kq.stream_floor(Xs[i], out16=Cs[i], out1=Ss[i]),
+    }
+    steps = max(1, timed_graph_steps // 4)  # ~25 us per step: a quarter of the headline's step count
+    out = {"M": M, "d": d, "algorithmic_bytes": nbytes, "steps": steps,
+           "mall": f"cold: {nsets} rotating buffer sets, {nsets * nbytes / 1e6:.0f} MB"}
+    for name, fn in fns.items():
+        for i in range(warmup):
+            fn(i % nsets)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(steps):
+                fn(i % nsets)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / steps * 1e3
+        gbs = nbytes / us * 1e-3
+        out[name] = {"us": round(us, 3), "gbs": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
+        del g
+    out["kroquant_vs_smoothquant"] = round(out["smoothquant"]["us"] / out["kroquant"]["us"], 3)
+    del Xs, Cs, Ss, X0
+    torch.cuda.empty_cache()
+    return out
 
 
 TABLE2_SHAPES = [(4096, 1024), (4096, 4096), (4096, 16384), (512, 4096), (512, 16384)]
