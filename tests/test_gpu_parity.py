@@ -461,13 +461,15 @@ def _gemm_tolerance(ac, as_, bc, bs):
 
 @pytest.mark.parametrize("M,N,K", [(77, 200, 2240), (128, 128, 64), (33, 70, 1120), (300, 257, 3072), (1, 1, 32),
                                    (5, 3, 128), (64, 130, 256), (130, 64, 384), (200, 200, 512), (129, 127, 1280),
-                                   (3072, 2304, 128), (3000, 2200, 384)])
+                                   (3072, 2304, 128), (3000, 2200, 384), (2500, 2470, 1664)])
 def test_mxfp4_gemm_parity(M, N, K):
     """C = deq(A) deq(B)^T on the matrix cores against the oracle's fp64
     product, within the fp32 accumulation bound; ragged tiles, odd block
-    counts along K, and the accumulate mode.  The two largest shapes have at
-    least 96 tiles of 256 x 256 and so run the large-tile kernel (the last one
-    with ragged tiles in both directions)."""
+    counts along K, and the accumulate mode.  The three largest shapes have at
+    least 96 tiles of 256 x 256 and so run the large-tile kernel (the last two
+    with ragged tiles in both directions; the last one with 13 K stages, so
+    every stage buffer is refilled several times and the stage count is not a
+    multiple of the three buffers)."""
     ac, as_ = _rand_mx(M, K, seed=M + K)
     bc, bs = _rand_mx(N, K, seed=N + 2 * K)
     ref = oracle.mxfp4_gemm(ac, as_, bc, bs)
