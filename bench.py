@@ -83,6 +83,8 @@ def parse():
     ap.add_argument("--no-calib", action="store_true", help="skip the layer-wise calibration timing")
     ap.add_argument("--calib-samples", type=int, default=128,
                     help="calibration samples of 4608 tokens for the calibration timing")
+    ap.add_argument("--no-large", action="store_true",
+                    help="skip the large stress shape, X [18432, 12288] with 384 per-block factor pairs")
     ap.add_argument("--no-wide", action="store_true",
                     help="skip the second FLUX shape, X [4608, 12288] (the MLP down-projection input)")
     ap.add_argument("--no-table2", action="store_true",
@@ -312,6 +314,7 @@ def main():
     ms_warm, _ = timed(run_kq, args.steps, args.warmup, rotate=False)
     table2 = None if args.no_table2 else table2_shapes(kq, synth, dev, stream, sptr)
     wide = None if args.no_wide else wide_shape(kq, synth, dev, stream, timed_graph_steps=args.steps)
+    large = None if args.no_large else large_per_block(kq, synth, dev, stream)
     gemm = None if args.no_gemm else gemm_timing(kq, synth, dev, stream, sptr, Cs[0], Ss[0], M, d)
     calib = None if args.no_calib else calib_timing(kq, synth, dev, stream, sptr, args.calib_samples)
     dist = per_launch(run_kq)
@@ -371,6 +374,7 @@ def main():
                      "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
         "cpu_baseline": cpu,
         "flux_4608x12288": wide,
+        "large_18432x12288_per_block": large,
         "table2_pow2_d": table2,
         "w4a4_gemm": gemm,
         "calibration": calib,
@@ -425,6 +429,61 @@ def wide_shape(kq, synth, dev, stream, timed_graph_steps=1000, warmup=1000):
         del g
     out["kroquant_vs_smoothquant"] = round(out["smoothquant"]["us"] / out["kroquant"]["us"], 3)
     del Xs, Cs, Ss, X0
+    torch.cuda.empty_cache()
+    return out
+
+
+def large_per_block(kq, synth, dev, stream, steps=50, warmup=20):
+    """The large stress shape: FLUX batch 4, X bf16 [18432, 12288] (453 MB in,
+    573 MB per step), one factor pair per 32-column block (384 pairs), for
+    the (4, 8) and (2, 16) splits: the packed and on-the-fly KroQuant calls
+    and SmoothQuant, as `steps` launches over two rotating input sets (1.15 GB)
+    captured into a HIP graph and replayed between HIP events.  The input is
+    drawn on the device (the Student-t(3) recipe with torch's generator; the
+    host generator would take about a minute at this size); outputs at this
+    shape are checked against the oracle by the GPU tests on sampled rows."""
+    import torch
+    M, d = 18432, 12288
+    nb = d // 32
+    nbytes = algorithmic_bytes(M, d)
+    nsets = 2
+    Xs = [synth.activations_device(M, d, seed=100 + i, device=dev) for i in range(nsets)]
+    Cs = [torch.empty((M, d // 2), dtype=torch.uint8, device=dev) for _ in range(nsets)]
+    Ss = [torch.empty((M, nb), dtype=torch.uint8, device=dev) for _ in range(nsets)]
+    mult = torch.ones(d, dtype=torch.float32, device=dev)
+    out = {"M": M, "d": d, "nfac": nb, "algorithmic_bytes": nbytes, "steps": steps,
+           "mall": f"cold: {nsets} rotating input sets, {nsets * nbytes / 1e6:.0f} MB",
+           "inputs": "drawn on the device (Student-t(3), 0.5% channels x50)"}
+
+    def time_fn(fn):
+        for i in range(warmup):
+            fn(i % nsets)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(steps):
+                fn(i % nsets)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / steps * 1e3
+        del g
+        gbs = nbytes / us * 1e-3
+        return {"us": round(us, 2), "gbs": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
+
+    for a, b in ((4, 8), (2, 16)):
+        A, B = synth.factors(a, b, nb, seed=4)
+        Ad, Bd = torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev)
+        kpack = kq.pack_factors(Ad, Bd)
+        out[f"kroquant_packed_{a}x{b}"] = time_fn(
+            lambda i: kq.quantize_packed(Xs[i], Ad, Bd, kpack, codes=Cs[i], scales=Ss[i]))
+        out[f"kroquant_onthefly_{a}x{b}"] = time_fn(lambda i: kq.quantize(Xs[i], Ad, Bd, codes=Cs[i], scales=Ss[i]))
+    out["smoothquant"] = time_fn(lambda i: kq.smoothquant(Xs[i], mult, codes=Cs[i], scales=Ss[i]))
+    del Xs, Cs, Ss
     torch.cuda.empty_cache()
     return out
 

@@ -883,6 +883,17 @@ __global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
     }
 }
 
+// Workgroups go to the 8 XCDs round robin (workgroup i to XCD i % 8).  This
+// gives XCD x the contiguous workgroup range [x q + min(x, r), ...) of a grid
+// of G = 8 q + r (a bijection of [0, G)).  Used by the COLUMN mapping, where
+// neighbouring workgroups hold neighbouring 32-column blocks of the same
+// rows: their 64-byte input pieces share cache lines, and so do their code
+// and scale writes, which then all go through one L2.
+__device__ __forceinline__ int64_t xcd_order(int64_t i, int64_t G) {
+    const int64_t q = G >> 3, r = G & 7, x = i & 7;
+    return x * q + (x < r ? x : r) + (i >> 3);
+}
+
 // Input loads of one 64-block unit (four nontemporal 1 KiB loads, chunk
 // 64 c + lane in v[c]); FULL = all 64 blocks present.  A partial unit
 // (0 <= nvalid < 64) issues the same four loads, each lane at a clamped
@@ -1107,7 +1118,8 @@ __device__ __forceinline__ void packed_unit(const Params& p, uint4* lds, int64_t
 // Matrix-core KroQuant with K read from the pack, one 64-block unit per wave
 // (no loop): few live registers, so every wave of a large grid is resident
 // at once and all input loads are in flight from the start.  FLAT: unit =
-// blockIdx.x;  COLUMN: column block j = blockIdx.x % nb, rows 64 * (blockIdx.x / nb).
+// blockIdx.x;  COLUMN: with u = blockIdx.x in the XCD-contiguous order,
+// column block j = u % nb, rows 64 * (u / nb).
 // Per wave: the four input loads are issued first, then the K slices; all
 // four chunks go through LDS; both 32-block tiles are multiplied and encoded
 // back to back and their code and scale stores issued last.
@@ -1134,8 +1146,9 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
         nvalid = (int)min<int64_t>(64, p.nblocks - first);
         bstride = 1;
     } else {
-        jcol = u % p.nb;
-        const int64_t row0 = (u / p.nb) * 64;
+        const int64_t g = xcd_order(u, gridDim.x);
+        jcol = g % p.nb;
+        const int64_t row0 = (g / p.nb) * 64;
         first = row0 * p.nb + jcol;
         nvalid = (int)min<int64_t>(64, p.M - row0);
         bstride = (uint32_t)p.nb;
@@ -1157,9 +1170,9 @@ __global__ __launch_bounds__(64) void kron_mfma_unit_kernel(const Params p) {
 // input loads.  Then each wave runs the unit as in the packed kernel, with
 // the binade-edge window 2^-17 ||K||_inf max|x| per block (||K||_inf =
 // ||A||_inf ||B||_inf, computed in fp32 and widened by 2^-16 relative).
-// FLAT: workgroup g = units 4 g .. 4 g + 3.  COLUMN: workgroup g = column
-// block j = g % nb, row units 4 (g / nb) .. + 3.  Trailing waves with no rows
-// take part in the build and return.
+// FLAT: workgroup g = units 4 g .. 4 g + 3.  COLUMN: workgroup g (in the
+// XCD-contiguous order) = column block j = g % nb, row units 4 (g / nb) .. + 3.
+// Trailing waves with no rows take part in the build and return.
 template <Mapping MAP, int NA, int NB, bool LU, bool WY, bool WY16>
 __global__ __launch_bounds__(256) void kron_build_unit_kernel(const Params p) {
     constexpr int NF = NA * NA + NB * NB;
@@ -1177,8 +1190,9 @@ __global__ __launch_bounds__(256) void kron_build_unit_kernel(const Params p) {
         nvalid = (int)max<int64_t>(0, min<int64_t>(64, p.nblocks - first));
         bstride = 1;
     } else {
-        jcol = blockIdx.x % p.nb;
-        const int64_t row0 = ((int64_t)(blockIdx.x / p.nb) * 4 + w) * 64;
+        const int64_t gi = xcd_order(blockIdx.x, gridDim.x);
+        jcol = gi % p.nb;
+        const int64_t row0 = ((gi / p.nb) * 4 + w) * 64;
         first = row0 * p.nb + jcol;
         nvalid = (int)max<int64_t>(0, min<int64_t>(64, p.M - row0));
         bstride = (uint32_t)p.nb;
