@@ -79,7 +79,7 @@ kq::Params make_params(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, 
     return p;
 }
 
-// KQ_MAX_WAVES and KQ_UNITS_PER_WAVE (optional, read once): launch shape of
+// KQ_MAX_WAVES, KQ_UNITS_PER_WAVE and the switches below (optional, read once): launch shape of
 // the matrix-core kernel.  Tuning knobs only; outputs do not depend on them.
 kq::LaunchConfig default_config() {
     static const kq::LaunchConfig cfg = [] {
@@ -90,6 +90,11 @@ kq::LaunchConfig default_config() {
         }
         if (const char* e = std::getenv("KQ_PACKED_PERSISTENT")) c.packed_one_unit = std::atoi(e) == 0;
         if (const char* e = std::getenv("KQ_ONTHEFLY_PERSISTENT")) c.build_unit = std::atoi(e) == 0;
+        if (const char* e = std::getenv("KQ_COLUMN_TILE")) c.column_tile = std::atoi(e) != 0;
+        if (const char* e = std::getenv("KQ_TILE_ROWS")) {
+            const int v = std::atoi(e);
+            if (v >= 0 && v <= 8) c.tile_row_blocks = v;
+        }
         if (const char* e = std::getenv("KQ_SMOOTH_PATH")) {
             const int v = std::atoi(e);
             if (v >= 0 && v <= 3) c.smooth_path = v;

@@ -37,6 +37,8 @@ struct LaunchConfig {
     int units_per_wave = 1;                 // 64-block units it loads per step (1 or 2)
     bool packed_one_unit = true;            // packed K: one unit per wave, no loop
     bool build_unit = true;                 // K from the factors: built per 4-wave workgroup, one unit per wave
+    bool column_tile = true;                // per-block factors: 8-wave workgroups on strips of 8 column blocks
+    int tile_row_blocks = 0;                // 64-row steps per strip (0: chosen from the grid size)
     int64_t interleave_max_units = 4096;    // packed K: interleave both tiles up to this many units
     int smooth_path = 3;                    // SmoothQuant layout: 0 chunk, 1 per-lane, 2 column, 3 stationary
     int64_t smooth_waves = 2048;            // target workgroups of the column-stationary SmoothQuant

@@ -586,8 +586,9 @@ __global__ __launch_bounds__(64) void smooth_stationary_kernel(const Params p) {
 // chains of KronOp:
 //   Z[p][i] = B[i][0]*x[p*b] then fma(B[i][q], x[p*b+q], .), q = 1..b-1,
 //   Y[o][i] = A[o][0]*Z[0][i] then fma(A[o][p], Z[p][i], .), p = 1..a-1.
-// Called with all 64 lanes active; the blocks lie in this wave's LDS unit.
-template <int NA, int NB>
+// Called with all 64 lanes active; the blocks lie in this wave's LDS unit
+// (GX: the inputs are read from X at the output blocks, unit_lds unused).
+template <int NA, int NB, bool GX = false>
 __device__ __forceinline__ void exact_blocks_coop(const uint4* unit_lds, int blk0, int blk1, const float* Af,
                                                   const float* Bf, const Params& p, int64_t out0, int64_t out1) {
     const int h = (threadIdx.x >> 5) & 1;  // half of this wave (workgroups may hold several waves)
@@ -596,8 +597,14 @@ __device__ __forceinline__ void exact_blocks_coop(const uint4* unit_lds, int blk
     const int blk = h ? blk1 : blk0;
     const int64_t out_blk = h ? out1 : out0;
     float x[32];
+    if (GX) {
+        const uint4* const xs = reinterpret_cast<const uint4*>(p.X) + (blk < 0 ? out0 : out_blk) * 4;
 #pragma unroll
-    for (int m = 0; m < 4; ++m) unpack8(unit_lds[lds_slot(blk < 0 ? 0 : blk, m)], x + 8 * m);
+        for (int m = 0; m < 4; ++m) unpack8(xs[m], x + 8 * m);
+    } else {
+#pragma unroll
+        for (int m = 0; m < 4; ++m) unpack8(unit_lds[lds_slot(blk < 0 ? 0 : blk, m)], x + 8 * m);
+    }
     float acc = 0.0f;
 #pragma unroll
     for (int pr = 0; pr < NA; ++pr) {
@@ -620,7 +627,8 @@ __device__ __forceinline__ void exact_blocks_coop(const uint4* unit_lds, int blk
 }
 
 // all blocks flagged in `edges` (bit b = block b of the unit), two at a time
-template <int NA, int NB>
+// (GX: their inputs read from X instead of the unit in LDS)
+template <int NA, int NB, bool GX = false>
 __device__ __forceinline__ void exact_flagged(uint64_t edges, const uint4* unit_lds, int64_t first, uint32_t bstride,
                                               const float* Af, const float* Bf, const Params& p) {
     while (edges) {
@@ -631,8 +639,8 @@ __device__ __forceinline__ void exact_flagged(uint64_t edges, const uint4* unit_
             b1 = __builtin_ctzll(edges);
             edges &= edges - 1;
         }
-        exact_blocks_coop<NA, NB>(unit_lds, b0, b1, Af, Bf, p, first + (int64_t)b0 * bstride,
-                                  first + (int64_t)(b1 < 0 ? 0 : b1) * bstride);
+        exact_blocks_coop<NA, NB, GX>(unit_lds, b0, b1, Af, Bf, p, first + (int64_t)b0 * bstride,
+                                      first + (int64_t)(b1 < 0 ? 0 : b1) * bstride);
     }
 }
 
@@ -946,11 +954,22 @@ struct EdgeTest {
 // all 64 blocks present (no per-tile bounds tests in the straight-line
 // code); WY / WY16 = the fp32 / bf16 transformed values are stored too;
 // PACKED selects the edge test.  lds = this wave's 256-slot staging area;
-// Af, Bf = the factors (for the fixed-order fallback).
-template <Mapping MAP, int NA, int NB, bool ILV, bool WY, bool WY16, bool FULL, bool PACKED>
+// Af, Bf = the factors (for the fixed-order fallback).  TILE: the workgroup
+// has already staged the unit in lds (v is not used); the codes and scales of
+// the blocks to store go to ts.out (the 16 code bytes of block b at slot b,
+// its scale at byte 1024 + b) for the workgroup's row stores, which store the
+// blocks whose bit is set in *ts.mask; the binade-edge blocks go to *ts.edges
+// for the caller's fixed-order pass.
+struct TileSink {
+    uint4* out;
+    uint64_t* mask;
+    uint64_t* edges;
+};
+
+template <Mapping MAP, int NA, int NB, bool ILV, bool WY, bool WY16, bool FULL, bool PACKED, bool TILE = false>
 __device__ __forceinline__ void unit_compute(const Params& p, uint4* lds, int64_t first, int nvalid_rt,
                                              uint32_t bstride, const uint4 (&v)[4], const KSlices& ks, bool zero_ok,
-                                             EdgeTest et, const float* Af, const float* Bf) {
+                                             EdgeTest et, const float* Af, const float* Bf, TileSink ts = {}) {
     const int lane = threadIdx.x & 63;
     const int h = lane >> 5, jl = lane & 31;
     const int nvalid = FULL ? 64 : nvalid_rt;
@@ -963,13 +982,15 @@ __device__ __forceinline__ void unit_compute(const Params& p, uint4* lds, int64_
     float* const y_u = WY ? p.y + first * 32 : nullptr;
     uint16_t* const y16_u = WY16 ? p.y16 + first * 32 : nullptr;
     // every chunk goes to LDS as soon as it arrives (those of missing blocks as zeros)
+    if (!TILE) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c)
-        lds[wslot + 64 * c] = (FULL || (64 * c + lane) / 4 < nvalid) ? v[c] : make_uint4(0u, 0u, 0u, 0u);
+        for (int c = 0; c < 4; ++c)
+            lds[wslot + 64 * c] = (FULL || (64 * c + lane) / 4 < nvalid) ? v[c] : make_uint4(0u, 0u, 0u, 0u);
+    }
     // lane (jl, h) reads chunks h and 2 + h of block 32 t + jl: slots 128 t + rslot
     // and 128 t + (rslot ^ 2)
     const int rslot = 4 * jl + (h ^ ((jl >> 2) & 3));
-    wave_lds_sync();
+    if (!TILE) wave_lds_sync();
     uint4 raw[2][2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -1062,10 +1083,30 @@ __device__ __forceinline__ void unit_compute(const Params& p, uint4* lds, int64_
     } else {
         // straight-line for full and partial units alike: a partial unit's
         // missing blocks hold zeros and are neither stored nor flagged
+        // TILE: each tile's codes and scales go to ts.out as soon as they
+        // exist (all blocks; the mask decides which are stored), so that the
+        // first tile's accumulators are dead before the second product
+        uint8_t* const ob = reinterpret_cast<uint8_t*>(ts.out);
+        auto tile_write = [&](int t, const TileOut& o) {
+            const int b = 32 * t + jl;
+            *reinterpret_cast<uint2*>(ob + 16 * b + 8 * h) = o.codes;
+            if (h == 0) ob[1024 + b] = (uint8_t)o.sb;
+        };
         const TileOut o0 = finish(0, product(raw[0]), raw[0]);
+        if (TILE) tile_write(0, o0);
         __builtin_amdgcn_sched_barrier(0);
         const TileOut o1 = finish(1, product(raw[1]), raw[1]);
+        if (TILE) tile_write(1, o1);
         __builtin_amdgcn_sched_barrier(0);
+        if (TILE) {
+            const uint64_t m = (__builtin_amdgcn_ballot_w64(o0.store) & 0xFFFFFFFFull) |
+                               (__builtin_amdgcn_ballot_w64(o1.store) << 32);
+            if (lane == 0) {
+                *ts.mask = m;
+                *ts.edges = edges;
+            }
+            return;
+        }
         store(0, o0);
         store(1, o1);
     }
@@ -1304,6 +1345,145 @@ __global__ __launch_bounds__(256) void kron_build_unit_kernel(const Params p) {
     const bool zero_ok = hdr[1] != 0.0f;
     unit_compute<MAP, NA, NB, false, WY, WY16, false, false>(p, lds_x[w], first, nvalid, bstride, v, ks, zero_ok, et,
                                                              fac, fac + NA * NA);
+}
+
+// Per-block factors (a pair per 32-column block, COLUMN mapping): eight waves
+// per workgroup on a strip of 8 column blocks, 64 rows at a time, so that
+// each row of a step is 512 contiguous bytes of X, 128 of codes and 8 of
+// scales (one wave per 64-byte piece of 64 rows would touch a different cache
+// line per row in every load and store).  Wave w owns column block 8 j + w of
+// the strip and keeps its K in registers for all the strip's steps: read from
+// the pack, or built by each lane from its rows of A and B with the window
+// 2^-17 ||K||_inf max|x|.  A step: wave w loads rows 8 w .. 8 w + 7 (two rows
+// per 1 KiB load) and writes each 16-byte chunk to the LDS tile of the wave
+// that owns its column block, then issues the next step's loads; after a
+// barrier each wave runs the unit body on its column block and parks its
+// codes and scales in LDS; after a second barrier the workgroup stores them
+// along rows.  The binade-edge blocks of all steps are re-evaluated after the
+// last step, their inputs read again from X (no lane keeps that code's
+// registers live through the steps).  Grid: ceil(nrb / rg) ceil(nb / 8) workgroups (nrb = ceil(M /
+// 64) row blocks, rg per strip) in the XCD-contiguous order, strips of the
+// same rows next to each other.  Columns and rows beyond the matrix are read
+// clamped, staged as zeros and not stored.
+//
+// The wave tiles are 260 slots apart: the 64 extra bytes put the same chunk
+// of the same row in different banks of the eight tiles, so the staging
+// writes (a row's 32 chunks go to eight tiles) are free of bank conflicts.
+constexpr int kTileCols = 8;
+constexpr int kTileSlots = 260;
+constexpr int kCodeSlots = 68;  // 64 blocks x 16 code bytes, then 64 scale bytes
+constexpr int kTileMaxSteps = 8;
+
+template <int NA, int NB, bool PACKED, bool WY>
+__global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params p, int rg) {
+    __shared__ uint4 lds_x[kTileCols * kTileSlots];
+    __shared__ uint4 lds_c[kTileCols * kCodeSlots];
+    __shared__ uint64_t stmask[kTileCols];
+    __shared__ uint64_t sedges[kTileCols][kTileMaxSteps];
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int64_t ntc = (p.nb + kTileCols - 1) / kTileCols;
+    const int64_t nrb = (p.M + 63) / 64;
+    const int64_t g = xcd_order(blockIdx.x, gridDim.x);
+    const int64_t jt = g % ntc, rb0 = (g / ntc) * rg;
+    const int nsteps = (int)min<int64_t>(rg, nrb - rb0);
+    const int ncols = (int)min<int64_t>(kTileCols, p.nb - kTileCols * jt);
+    const bool active = w < ncols;
+    const int64_t jc = kTileCols * jt + (active ? w : 0);  // this wave's column block
+    const int64_t f = (p.nfac == 1) ? 0 : jc;
+    const float* const Af = p.A + f * (NA * NA);
+    const float* const Bf = p.B + f * (NB * NB);
+    // the factor entries first: loads retire in order, so waiting for them
+    // does not wait for the input
+    KFactors<NA, NB> kf;
+    if (!PACKED) load_k_factors<NA, NB>(Af, Bf, lane, kf);
+    // load c of a step: row 8 w + 2 c + lane / 32, 16-byte chunk lane % 32 of
+    // its 512 bytes; a wave-uniform base per step and 32-bit lane offsets
+    // (64 rows of X span less than 4 GiB: d < 2^25, checked by the launcher)
+    const int q = lane & 31;
+    const int qb = min(q >> 2, ncols - 1);
+    const uint32_t rowbytes = (uint32_t)(p.nb * 64);
+    const uint32_t qoff = (uint32_t)(qb * 64 + (q & 3) * 16);
+    const uint8_t* const xstrip = reinterpret_cast<const uint8_t*>(p.X) + kTileCols * jt * 64;
+    uint4 v[4];
+    auto issue = [&](int64_t row0) {
+        const int nrows = (int)min<int64_t>(64, p.M - row0);
+        const uint8_t* const xs = xstrip + row0 * p.nb * 64;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const uint32_t r = (uint32_t)min(8 * w + 2 * c + (lane >> 5), nrows - 1);
+            v[c] = load_nt(reinterpret_cast<const uint4*>(xs + (r * rowbytes + qoff)));
+        }
+    };
+    issue(rb0 * 64);
+    __builtin_amdgcn_sched_barrier(0);
+    KSlices ks;
+    bool zero_ok;
+    EdgeTest et;
+    if (PACKED) {
+        packed_k(p, f, ks, zero_ok, et);
+    } else {
+        et.edge_t = 0u;
+        et.kbound = build_k<NA, NB>(kf, ks) * 0x1.0001p-17f;
+        // no row of A and no row of B with every sign bit set: then an
+        // all-(+0) input block gives +0 for every output in the fixed order
+        bool neg_row = false;
+        if (lane < NA) {
+            bool all = true;
+#pragma unroll
+            for (int j = 0; j < NA; ++j) all = all && (__float_as_uint(Af[lane * NA + j]) >> 31);
+            neg_row = all;
+        }
+        if (lane < NB) {
+            bool all = true;
+#pragma unroll
+            for (int j = 0; j < NB; ++j) all = all && (__float_as_uint(Bf[lane * NB + j]) >> 31);
+            neg_row = neg_row || all;
+        }
+        zero_ok = __builtin_amdgcn_ballot_w64(neg_row) == 0;
+    }
+    for (int it = 0; it < nsteps; ++it) {
+        const int64_t row0 = (rb0 + it) * 64;
+        const int nrows = (int)min<int64_t>(64, p.M - row0);
+        // stage: chunk (q & 3) of column block q / 4 goes to that wave's tile
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int r = 8 * w + 2 * c + (lane >> 5);
+            const bool ok = r < nrows && (q >> 2) < ncols;
+            lds_x[kTileSlots * (q >> 2) + lds_slot(r, q & 3)] = ok ? v[c] : make_uint4(0u, 0u, 0u, 0u);
+        }
+        if (it + 1 < nsteps) issue(row0 + 64);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        if (active)
+            unit_compute<Mapping::Column, NA, NB, false, WY, false, false, PACKED, true>(
+                p, lds_x + kTileSlots * w, row0 * p.nb + jc, nrows, (uint32_t)p.nb, v, ks, zero_ok, et, Af, Bf,
+                TileSink{lds_c + kCodeSlots * w, &stmask[w], &sedges[w][it]});
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        // row stores: thread t takes row t / 8, column block t % 8 of the step
+        const int r = threadIdx.x >> 3, j = threadIdx.x & 7;
+        const uint32_t mword = reinterpret_cast<const uint32_t*>(stmask)[2 * j + (r >> 5)];
+        if (p.codes && r < nrows && j < ncols && ((mword >> (r & 31)) & 1u)) {
+            const uint4* const ct = lds_c + kCodeSlots * j;
+            const int64_t blk0 = row0 * p.nb + kTileCols * jt;  // wave-uniform
+            const uint32_t ob = (uint32_t)r * (uint32_t)p.nb + (uint32_t)j;
+            *reinterpret_cast<uint4*>(p.codes + blk0 * 16 + ob * 16u) = ct[r];
+            (p.scales + blk0)[ob] = reinterpret_cast<const uint8_t*>(ct)[1024 + r];
+        }
+    }
+    // blocks on a binade edge: the fixed evaluation order decides (this
+    // wave's own records, so no barrier is needed)
+    if (active) {
+        for (int it = 0; it < nsteps; ++it) {
+            // readfirstlane returns int: widen each half through uint32_t
+            const uint64_t se = sedges[w][it];
+            const uint64_t e = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)se) |
+                               ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(se >> 32)) << 32);
+            if (e) exact_flagged<NA, NB, true>(e, nullptr, (rb0 + it) * 64 * p.nb + jc, (uint32_t)p.nb, Af, Bf, p);
+        }
+    }
 }
 
 // Materialise and split K = A (x) B for every factor pair, in the lane layout
@@ -1611,6 +1791,27 @@ static hipError_t launch_unit(const Params& p, int64_t units, bool ilv, hipStrea
     return hipGetLastError();
 }
 
+// Per-block factors: the 8-column tile kernel (K from the pack or built per wave).
+template <int NA, int NB, bool PACKED>
+static hipError_t launch_tile(const Params& p, int rg, hipStream_t st) {
+    const int64_t nrb = (p.M + 63) / 64, ntc = (p.nb + kTileCols - 1) / kTileCols;
+    const dim3 g((unsigned)(((nrb + rg - 1) / rg) * ntc)), b(64 * kTileCols);
+    if (p.y) hipLaunchKernelGGL((kron_tile_kernel<NA, NB, PACKED, true>), g, b, 0, st, p, rg);
+    else hipLaunchKernelGGL((kron_tile_kernel<NA, NB, PACKED, false>), g, b, 0, st, p, rg);
+    return hipGetLastError();
+}
+
+// Row blocks per strip of the tile kernel (1 .. kTileMaxSteps): the
+// configured count, else as many as keep at least ~1728 workgroups when each
+// wave builds its K (about three rounds of the 512 that fit at once: more
+// steps amortise the build) and ~3456 when K comes from the pack (only its
+// load to amortise, so a shorter last round matters more).
+static int tile_rows(const Params& p, const LaunchConfig& cfg) {
+    const int64_t tiles = ((p.M + 63) / 64) * ((p.nb + kTileCols - 1) / kTileCols);
+    const int64_t rg = cfg.tile_row_blocks > 0 ? cfg.tile_row_blocks : tiles / (p.kpack ? 3456 : 1728);
+    return rg < 1 ? 1 : rg > kTileMaxSteps ? kTileMaxSteps : (int)rg;
+}
+
 // The on-chip-K unit kernel: four units per workgroup (one factor pair each).
 template <int NA, int NB, bool LU>
 static hipError_t launch_build(const Params& p, Mapping map, hipStream_t st) {
@@ -1635,6 +1836,11 @@ constexpr int64_t kMaxUnitGrid = (int64_t(1) << 31) - 1;
 template <int NA, int NB>
 static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
     const int64_t units = (map == Mapping::Flat) ? (p.nblocks + 63) / 64 : ((p.M + 63) / 64) * p.nb;
+    const int64_t tiles = ((p.M + 63) / 64) * ((p.nb + kTileCols - 1) / kTileCols);
+    if (map == Mapping::Column && cfg.column_tile && tiles <= kMaxUnitGrid && p.d < (int64_t(1) << 25)) {
+        if (p.kpack) return launch_tile<NA, NB, true>(p, tile_rows(p, cfg), st);
+        return launch_tile<NA, NB, false>(p, tile_rows(p, cfg), st);
+    }
     if (p.kpack) {
         if (cfg.packed_one_unit && units <= kMaxUnitGrid) {
             // small grids (few waves per SIMD) hide less latency: interleave the two tiles

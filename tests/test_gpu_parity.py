@@ -531,6 +531,34 @@ def test_full_size_workloads(name):
     assert_exact((host(c), host(s), None), (cr, sr, None), name + " hadamard")
 
 
+def test_per_block_strips_ragged():
+    """Per-block factors on a shape whose strips take two 64-row steps, whose
+    last strip has one step, last row block two rows and last column strip
+    four column blocks (M = 4610, d = 12160, 380 blocks per row): sampled rows
+    against the oracle, and the flat mapping (one shared pair) against the
+    column mapping (that pair repeated per block) bit for bit, y included,
+    which checks the per-step binade-edge records."""
+    M, d = 4610, 12160
+    X = synth.activations(M, d, "student_t3", seed=21, chan_frac=0.01, chan_factor=40)
+    A, B = synth.factors(4, 8, d // 32, seed=22)
+    rows = np.unique(np.concatenate([[0, 63, 64, 127, 128, 4543, 4544, 4607, 4608, M - 1],
+                                     np.random.default_rng(1).choice(M, 60, replace=False)]))
+    cr, sr, yr = oracle.quantize(np.ascontiguousarray(X[rows]), A, B, want_y=True)
+    Xd, Ad, Bd = dev_bf16(X), dev_f32(A), dev_f32(B)
+    c, s, y = kq.quantize(Xd, Ad, Bd, want_y=True)
+    assert_mx_close((host(c)[rows], host(s)[rows], host(y)[rows]), (cr, sr, yr), "on the fly")
+    c, s, y = kq.quantize_packed(Xd, Ad, Bd, kq.pack_factors(Ad, Bd), want_y=True)
+    assert_mx_close((host(c)[rows], host(s)[rows], host(y)[rows]), (cr, sr, yr), "packed")
+    A1, B1 = synth.factors(4, 8, 1, seed=23)
+    nb = d // 32
+    g1 = gpu_quantize(X, A1, B1, exact=False)
+    g2 = gpu_quantize(X, np.repeat(A1, nb, 0), np.repeat(B1, nb, 0), exact=False)
+    assert_exact(g1, g2, "on the fly, flat vs column")
+    g1 = gpu_quantize_packed(X, A1, B1)
+    g2 = gpu_quantize_packed(X, np.repeat(A1, nb, 0), np.repeat(B1, nb, 0))
+    assert_exact(g1, g2, "packed, flat vs column")
+
+
 @pytest.mark.parametrize("name", ["large_18432x12288", "large_18432x12288_2x16"])
 def test_large_per_block_sampled_rows(name):
     """Large per-block-factor workload at full size; the oracle recomputes a
