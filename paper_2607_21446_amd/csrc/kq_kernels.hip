@@ -1353,18 +1353,20 @@ __global__ __launch_bounds__(256) void kron_build_unit_kernel(const Params p) {
 // scales (one wave per 64-byte piece of 64 rows would touch a different cache
 // line per row in every load and store).  Wave w owns column block 8 j + w of
 // the strip and keeps its K in registers for all the strip's steps: read from
-// the pack, or built by each lane from its rows of A and B with the window
-// 2^-17 ||K||_inf max|x|.  A step: wave w loads rows 8 w .. 8 w + 7 (two rows
-// per 1 KiB load) and writes each 16-byte chunk to the LDS tile of the wave
-// that owns its column block, then issues the next step's loads; after a
-// barrier each wave runs the unit body on its column block and parks its
-// codes and scales in LDS; after a second barrier the workgroup stores them
-// along rows.  The binade-edge blocks of all steps are re-evaluated after the
-// last step, their inputs read again from X (no lane keeps that code's
-// registers live through the steps).  Grid: ceil(nrb / rg) ceil(nb / 8) workgroups (nrb = ceil(M /
-// 64) row blocks, rg per strip) in the XCD-contiguous order, strips of the
-// same rows next to each other.  Columns and rows beyond the matrix are read
-// clamped, staged as zeros and not stored.
+// the pack (PACKED), or built by each lane from its rows of A and B, which the
+// wave stages in LDS (loaded, or decoded from the 15 parameters of G_1..G_5
+// when LU), with the window 2^-17 ||K||_inf max|x|.  A step: wave w loads rows
+// 8 w .. 8 w + 7 (two rows per 1 KiB load) and writes each 16-byte chunk to
+// the LDS tile of the wave that owns its column block, then issues the next
+// step's loads; after a barrier each wave runs the unit body on its column
+// block and parks its codes and scales in LDS; after a second barrier the
+// workgroup stores them along rows.  The binade-edge blocks of all steps are
+// re-evaluated after the last step, their inputs read again from X (no lane
+// keeps that code's registers live through the steps).  Grid: ceil(nrb / rg)
+// ceil(nb / 8) workgroups (nrb = ceil(M / 64) row blocks, rg per strip) in
+// the XCD-contiguous order, strips of the same rows next to each other.
+// Columns and rows beyond the matrix are read clamped, staged as zeros and
+// not stored.
 //
 // The wave tiles are 260 slots apart: the 64 extra bytes put the same chunk
 // of the same row in different banks of the eight tiles, so the staging
@@ -1374,12 +1376,15 @@ constexpr int kTileSlots = 260;
 constexpr int kCodeSlots = 68;  // 64 blocks x 16 code bytes, then 64 scale bytes
 constexpr int kTileMaxSteps = 8;
 
-template <int NA, int NB, bool PACKED, bool WY>
+template <int NA, int NB, bool PACKED, bool LU, bool WY, bool WY16>
 __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params p, int rg) {
+    constexpr int NF = NA * NA + NB * NB;
+    constexpr int FPL = (NF + 63) / 64;  // factor entries per lane
     __shared__ uint4 lds_x[kTileCols * kTileSlots];
     __shared__ uint4 lds_c[kTileCols * kCodeSlots];
     __shared__ uint64_t stmask[kTileCols];
     __shared__ uint64_t sedges[kTileCols][kTileMaxSteps];
+    __shared__ float fac[PACKED ? 1 : kTileCols * NF];  // each wave's A then B
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int64_t ntc = (p.nb + kTileCols - 1) / kTileCols;
     const int64_t nrb = (p.M + 63) / 64;
@@ -1390,12 +1395,19 @@ __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params 
     const bool active = w < ncols;
     const int64_t jc = kTileCols * jt + (active ? w : 0);  // this wave's column block
     const int64_t f = (p.nfac == 1) ? 0 : jc;
-    const float* const Af = p.A + f * (NA * NA);
-    const float* const Bf = p.B + f * (NB * NB);
-    // the factor entries first: loads retire in order, so waiting for them
-    // does not wait for the input
-    KFactors<NA, NB> kf;
-    if (!PACKED) load_k_factors<NA, NB>(Af, Bf, lane, kf);
+    // K from the factors: this wave's A and B are staged in its LDS area,
+    // loaded first (coalesced; loads retire in order, so waiting for them does
+    // not wait for the input) or, LU, decoded there from the 15 parameters
+    float fv[PACKED || LU ? 1 : FPL];
+    if (!PACKED && !LU) {
+#pragma unroll
+        for (int q = 0; q < FPL; ++q) {
+            // unconditional (clamped index), so no branch hides the load from the wait counting
+            const int i = min(lane + 64 * q, NF - 1);
+            const float* src = i < NA * NA ? p.A + f * (NA * NA) + i : p.B + f * (NB * NB) + (i - NA * NA);
+            fv[q] = __builtin_nontemporal_load(src);
+        }
+    }
     // load c of a step: row 8 w + 2 c + lane / 32, 16-byte chunk lane % 32 of
     // its 512 bytes; a wave-uniform base per step and 32-bit lane offsets
     // (64 rows of X span less than 4 GiB: d < 2^25, checked by the launcher)
@@ -1419,9 +1431,32 @@ __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params 
     KSlices ks;
     bool zero_ok;
     EdgeTest et;
+    const float* Af = p.A + f * (NA * NA);
+    const float* Bf = p.B + f * (NB * NB);
     if (PACKED) {
         packed_k(p, f, ks, zero_ok, et);
     } else {
+        float* const facw = fac + (PACKED ? 0 : w * NF);
+        if (LU) {
+            float gm[5][4];
+            lu_g(p.lu + f * 15, gm);
+#pragma unroll
+            for (int q2 = 0; q2 < FPL; ++q2) {
+                const int i = lane + 64 * q2;
+                if (i < NF) facw[i] = lu_entry<NA, NB>(gm, i);
+            }
+        } else {
+#pragma unroll
+            for (int q2 = 0; q2 < FPL; ++q2) {
+                const int i = lane + 64 * q2;
+                if (i < NF) facw[i] = fv[q2];
+            }
+        }
+        wave_lds_sync();
+        Af = facw;
+        Bf = facw + NA * NA;
+        KFactors<NA, NB> kf;
+        load_k_factors<NA, NB>(Af, Bf, lane, kf);
         et.edge_t = 0u;
         et.kbound = build_k<NA, NB>(kf, ks) * 0x1.0001p-17f;
         // no row of A and no row of B with every sign bit set: then an
@@ -1456,7 +1491,7 @@ __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params 
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
         if (active)
-            unit_compute<Mapping::Column, NA, NB, false, WY, false, false, PACKED, true>(
+            unit_compute<Mapping::Column, NA, NB, false, WY, WY16, false, PACKED, true>(
                 p, lds_x + kTileSlots * w, row0 * p.nb + jc, nrows, (uint32_t)p.nb, v, ks, zero_ok, et, Af, Bf,
                 TileSink{lds_c + kCodeSlots * w, &stmask[w], &sedges[w][it]});
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
@@ -1792,12 +1827,15 @@ static hipError_t launch_unit(const Params& p, int64_t units, bool ilv, hipStrea
 }
 
 // Per-block factors: the 8-column tile kernel (K from the pack or built per wave).
-template <int NA, int NB, bool PACKED>
+template <int NA, int NB, bool PACKED, bool LU>
 static hipError_t launch_tile(const Params& p, int rg, hipStream_t st) {
     const int64_t nrb = (p.M + 63) / 64, ntc = (p.nb + kTileCols - 1) / kTileCols;
     const dim3 g((unsigned)(((nrb + rg - 1) / rg) * ntc)), b(64 * kTileCols);
-    if (p.y) hipLaunchKernelGGL((kron_tile_kernel<NA, NB, PACKED, true>), g, b, 0, st, p, rg);
-    else hipLaunchKernelGGL((kron_tile_kernel<NA, NB, PACKED, false>), g, b, 0, st, p, rg);
+    const bool wy = p.y != nullptr, wy16 = LU && p.y16 != nullptr;
+#define KQ_TILE(WY, WY16) hipLaunchKernelGGL((kron_tile_kernel<NA, NB, PACKED, LU, WY, WY16>), g, b, 0, st, p, rg)
+    if (wy16) { if (wy) KQ_TILE(true, LU); else KQ_TILE(false, LU); }
+    else { if (wy) KQ_TILE(true, false); else KQ_TILE(false, false); }
+#undef KQ_TILE
     return hipGetLastError();
 }
 
@@ -1838,8 +1876,8 @@ static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st, cons
     const int64_t units = (map == Mapping::Flat) ? (p.nblocks + 63) / 64 : ((p.M + 63) / 64) * p.nb;
     const int64_t tiles = ((p.M + 63) / 64) * ((p.nb + kTileCols - 1) / kTileCols);
     if (map == Mapping::Column && cfg.column_tile && tiles <= kMaxUnitGrid && p.d < (int64_t(1) << 25)) {
-        if (p.kpack) return launch_tile<NA, NB, true>(p, tile_rows(p, cfg), st);
-        return launch_tile<NA, NB, false>(p, tile_rows(p, cfg), st);
+        if (p.kpack) return launch_tile<NA, NB, true, false>(p, tile_rows(p, cfg), st);
+        return launch_tile<NA, NB, false, false>(p, tile_rows(p, cfg), st);
     }
     if (p.kpack) {
         if (cfg.packed_one_unit && units <= kMaxUnitGrid) {
@@ -1859,6 +1897,9 @@ static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st, cons
 template <int NA, int NB>
 static hipError_t launch_lu(const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
     const int64_t units = (map == Mapping::Flat) ? (p.nblocks + 63) / 64 : ((p.M + 63) / 64) * p.nb;
+    const int64_t tiles = ((p.M + 63) / 64) * ((p.nb + kTileCols - 1) / kTileCols);
+    if (map == Mapping::Column && cfg.column_tile && tiles <= kMaxUnitGrid && p.d < (int64_t(1) << 25))
+        return launch_tile<NA, NB, false, true>(p, tile_rows(p, cfg), st);
     if (cfg.build_unit && units <= kMaxUnitGrid) return launch_build<NA, NB, true>(p, map, st);
     if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, false, true>(p, map, st, cfg);
     return launch_mfma_u<NA, NB, 1, false, true>(p, map, st, cfg);

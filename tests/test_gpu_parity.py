@@ -559,6 +559,30 @@ def test_per_block_strips_ragged():
     assert_exact(g1, g2, "packed, flat vs column")
 
 
+@pytest.mark.parametrize("a", [4, 1])
+def test_per_block_lu_strips_ragged(a):
+    """The LU form (15 parameters per pair decoded on chip) on the ragged
+    multi-step shape: sampled rows against the oracle's decode + fixed-order
+    quantizer, y16 = bf16(y), and one shared parameter set (flat mapping)
+    against the same set repeated per block (column mapping) bit for bit."""
+    M, d = 4610, 12160
+    nb = d // 32
+    X = synth.activations(M, d, "student_t3", seed=31, chan_frac=0.01, chan_factor=40)
+    lu = synth.lu_params(nb, seed=32 + a)
+    rows = np.unique(np.concatenate([[0, 63, 64, 127, 128, 4607, 4608, M - 1],
+                                     np.random.default_rng(2).choice(M, 40, replace=False)]))
+    cr, sr, yr, _ = oracle.quantize_lu(np.ascontiguousarray(X[rows]), lu, a, want_y=True)
+    c, s, y, y16 = gpu_quantize_lu(X, lu, a)
+    assert_mx_close((c[rows], s[rows], y[rows]), (cr, sr, yr), f"lu a={a}")
+    assert np.array_equal(y16[rows], oracle.f32_to_bf16(y[rows])), "y16 is not bf16(y)"
+    lu1 = synth.lu_params(1, seed=33 + a)
+    g1 = gpu_quantize_lu(X, lu1, a)
+    g2 = gpu_quantize_lu(X, np.repeat(lu1, nb, 0), a)
+    for u, v, what in zip(g1, g2, ("codes", "scales", "y", "y16")):
+        assert np.array_equal(np.ascontiguousarray(u).view(np.uint8), np.ascontiguousarray(v).view(np.uint8)), \
+            f"lu a={a}: flat vs column {what}"
+
+
 @pytest.mark.parametrize("name", ["large_18432x12288", "large_18432x12288_2x16"])
 def test_large_per_block_sampled_rows(name):
     """Large per-block-factor workload at full size; the oracle recomputes a
