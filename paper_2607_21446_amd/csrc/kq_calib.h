@@ -11,7 +11,7 @@ namespace kq {
 struct CalibPlan {
     int64_t R = 0, o = 0, d = 0, nb = 0, nfac = 0;
     int a = 4;
-    int64_t ntn = 0;                      // 128-column tiles of the d axis
+    int64_t ntn = 0;                      // 256-column tiles of the d axis (backward GEMMs)
     int64_t act_mt = 0, act_chunks = 0;   // activation-side backward: row tiles, workgroup rows
     int64_t w_mt = 0, w_ks = 0, w_kchunk = 0, w_chunks = 0;  // weight side: row tiles, K splits
     int64_t nsum = 0;                     // partial sums of the residual's squares (one per 64 x 64 tile)

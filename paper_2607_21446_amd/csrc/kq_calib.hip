@@ -12,8 +12,9 @@
 // forward products come from the quantizers and the W4A4 GEMM of the
 // library; this file holds the backward pass:
 //   * calib_gemm_kernel: bf16 matrix-core GEMM (v_mfma_f32_32x32x16_bf16,
-//     128 x 128 workgroup tile, 32-deep K stages loaded straight into three
-//     LDS buffers, two in flight) on operands stored K-contiguous.  The dequantized MXFP4 operands are exact
+//     128 x 256 workgroup tile for the backward products, 128 x 128 for the
+//     reference product, 32-deep K stages loaded straight into three LDS
+//     buffers, two in flight) on operands stored K-contiguous.  The dequantized MXFP4 operands are exact
 //     in bf16; the fp32 residual enters as two bf16 terms (hi = bf16(r),
 //     lo = bf16(r - hi), |r - hi - lo| <= 2^-17 |r|), so every product term
 //     is exact and sums run in fp32.  Two epilogues: the reference product
@@ -41,10 +42,15 @@ namespace {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int CT = 128;          // C tile edge of a workgroup (rows and columns)
+constexpr int CT = 128;          // C tile rows of a workgroup
 constexpr int BK = 32;           // K per LDS stage (bf16 elements; 64-byte rows)
-constexpr int kTileBytes = CT * BK * 2;
 constexpr int kTargetWg = 2048;  // workgroups the backward GEMMs aim for
+// Workgroup shapes: 2 x WN waves of 64 x 64, a C tile of 128 x 64 WN.  The
+// backward GEMMs take WN = 4 (eight waves, 128 x 256: a stage's bytes then
+// carry 1.5 times the matrix-core work of the 128 x 128 tile, as A has two
+// terms), the reference product WN = 2.
+constexpr int kWnBackward = 4;
+constexpr int kWnReference = 2;
 
 __device__ __forceinline__ float bf16f(uint16_t v) { return __uint_as_float(uint32_t(v) << 16); }
 
@@ -94,30 +100,37 @@ __device__ __forceinline__ void lds_load16(const uint8_t* src, void* lds_base) {
                                      (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
 }
 
-template <int TA>
+template <int TA, int WN>
 struct StageBuf {
-    uint4 a[TA][512];  // 128 rows x 4 slots of 16 bytes, slot lds_off(r, c) / 16
-    uint4 b[512];
+    uint4 a[TA][512];   // 128 rows x 4 slots of 16 bytes, slot lds_off(r, c) / 16
+    uint4 b[256 * WN];  // 64 WN rows, the same layout
 };
 
-// this wave's loads of one stage: rows 32 w .. 32 w + 31 of every operand,
-// 2 (TA + 1) instructions
-template <int TA>
-__device__ __forceinline__ void stage_issue(const Opnd (&A)[TA], const Opnd& B, StageBuf<TA>& sb, int wave, int lane,
-                                            int64_t m0, int64_t n0, int64_t k0) {
+// Loads of one stage per wave (one instruction = 16 rows x 64 bytes):
+// groups of 16 A rows 4 / WN (wave) .. (each term), groups of 16 B rows
+// 2 wave, 2 wave + 1; TA 4 / WN + 2 instructions.
+template <int TA, int WN>
+constexpr int stage_loads() { return TA * (4 / WN) + 2; }
+
+template <int TA, int WN>
+__device__ __forceinline__ void stage_issue(const Opnd (&A)[TA], const Opnd& B, StageBuf<TA, WN>& sb, int wave,
+                                            int lane, int64_t m0, int64_t n0, int64_t k0) {
+    constexpr int GA = 4 / WN;
     const int q = lane >> 2;
     const int blk = (lane & 3) ^ ((q >> 2) & 3);
     const int64_t kb = k0 * 2 + 16 * blk;
 #pragma unroll
     for (int gr = 0; gr < 2; ++gr) {
-        const int grp = 2 * wave + gr;
-        const int row = 16 * grp + q;
+        if (gr < GA) {
+            const int grp = GA * wave + gr;
 #pragma unroll
-        for (int x = 0; x < TA; ++x) {
-            const int64_t m = min(m0 + row, A[x].rows - 1);
-            lds_load16(A[x].p + m * A[x].ld + kb, &sb.a[x][64 * grp]);
+            for (int x = 0; x < TA; ++x) {
+                const int64_t m = min(m0 + 16 * grp + q, A[x].rows - 1);
+                lds_load16(A[x].p + m * A[x].ld + kb, &sb.a[x][64 * grp]);
+            }
         }
-        const int64_t n = min(n0 + row, B.rows - 1);
+        const int grp = 2 * wave + gr;
+        const int64_t n = min(n0 + 16 * grp + q, B.rows - 1);
         lds_load16(B.p + n * B.ld + kb, &sb.b[64 * grp]);
     }
 }
@@ -129,8 +142,9 @@ struct Frags {
 
 // this wave's fragments of one stage (all LDS reads of the stage, before any
 // later stage is issued)
-template <int TA>
-__device__ __forceinline__ void stage_frags(const StageBuf<TA>& sb, int h, int wm, int wn, int l32, Frags<TA>& f) {
+template <int TA, int WN>
+__device__ __forceinline__ void stage_frags(const StageBuf<TA, WN>& sb, int h, int wm, int wn, int l32,
+                                            Frags<TA>& f) {
 #pragma unroll
     for (int s = 0; s < 2; ++s)
 #pragma unroll
@@ -159,9 +173,9 @@ __device__ __forceinline__ void stage_mfma(const Frags<TA>& f, f32x16 (&acc)[2][
 // buffer (st + 2) % 3, which every wave finished reading before the barrier)
 // each wave waits until only its loads of stage st + 1 are outstanding, then
 // a bare s_barrier (a fenced barrier would drain the loads in flight).
-template <int TA>
+template <int TA, int WN>
 __device__ __forceinline__ void pipe_wait(int64_t st, int64_t nst) {
-    constexpr int kLoads = 2 * (TA + 1);
+    constexpr int kLoads = stage_loads<TA, WN>();
     if (st + 1 < nst)
         __builtin_amdgcn_s_waitcnt((kLoads & 15) | (7 << 4) | (15 << 8));  // vmcnt(kLoads)
     else
@@ -276,6 +290,7 @@ struct EpiGram {
 struct GemmGrid {
     int64_t M, N, K;
     int64_t m_tiles, ks, kchunk, chunks;
+    int xcd;  // 1: the column tiles of one chunk on one XCD (see calib_gemm_kernel)
 };
 
 template <int TA, class EPI>
@@ -289,16 +304,27 @@ struct GemmArgs {
 // C tile = sum_k A[m][k] B[n][k] over the work items (m tile, K split) of
 // this workgroup, each handed to the epilogue; A has TA bf16 terms.  Three
 // stage buffers, two stages in flight.
-template <int TA, class EPI>
-__global__ __launch_bounds__(256) void calib_gemm_kernel(const GemmArgs<TA, EPI> args) {
-    __shared__ StageBuf<TA> sb0, sb1, sb2;
-    __shared__ double sq_lds[4];
+template <int TA, int WN, class EPI>
+__global__ __launch_bounds__(128 * WN) void calib_gemm_kernel(const GemmArgs<TA, EPI> args) {
+    __shared__ StageBuf<TA, WN> sb0, sb1, sb2;
+    __shared__ double sq_lds[2 * WN];
     const GemmGrid& g = args.g;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
     const int h = lane >> 5, l32 = lane & 31;
-    const int64_t tn = blockIdx.x, c = blockIdx.y;
-    const int64_t n0 = tn * CT;
+    // work (chunk c, column tile tn).  xcd: workgroup L of the dispatch order
+    // runs on XCD L % 8, and each XCD takes a contiguous range of the works
+    // (column tile fastest), so the column tiles of a chunk, which read the
+    // same A rows at the same pace, share one L2
+    int64_t tn = blockIdx.x, c = blockIdx.y;
+    if (g.xcd) {
+        const int64_t G = int64_t(gridDim.x) * gridDim.y, L = blockIdx.x + int64_t(gridDim.x) * blockIdx.y;
+        const int64_t q = G >> 3, r = G & 7, x = L & 7;
+        const int64_t wk = x * q + (x < r ? x : r) + (L >> 3);
+        tn = wk % gridDim.x;
+        c = wk / gridDim.x;
+    }
+    const int64_t n0 = tn * (64 * WN);
 
     f32x16 gram[2];
     gram[0] = f32x16{};
@@ -319,24 +345,24 @@ __global__ __launch_bounds__(256) void calib_gemm_kernel(const GemmArgs<TA, EPI>
             // every wave is done with the buffers (and its earlier memory operations) before they refill
             __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
             __syncthreads();
-            stage_issue<TA>(args.A, args.B, sb0, wave, lane, m0, n0, k_lo);
-            if (nst > 1) stage_issue<TA>(args.A, args.B, sb1, wave, lane, m0, n0, k_lo + BK);
+            stage_issue<TA, WN>(args.A, args.B, sb0, wave, lane, m0, n0, k_lo);
+            if (nst > 1) stage_issue<TA, WN>(args.A, args.B, sb1, wave, lane, m0, n0, k_lo + BK);
             Frags<TA> f;
             for (int64_t st = 0; st < nst; st += 3) {
-                pipe_wait<TA>(st, nst);
-                stage_frags<TA>(sb0, h, wm, wn, l32, f);
-                if (st + 2 < nst) stage_issue<TA>(args.A, args.B, sb2, wave, lane, m0, n0, k_lo + (st + 2) * BK);
+                pipe_wait<TA, WN>(st, nst);
+                stage_frags<TA, WN>(sb0, h, wm, wn, l32, f);
+                if (st + 2 < nst) stage_issue<TA, WN>(args.A, args.B, sb2, wave, lane, m0, n0, k_lo + (st + 2) * BK);
                 stage_mfma<TA>(f, acc);
                 if (st + 1 < nst) {
-                    pipe_wait<TA>(st + 1, nst);
-                    stage_frags<TA>(sb1, h, wm, wn, l32, f);
-                    if (st + 3 < nst) stage_issue<TA>(args.A, args.B, sb0, wave, lane, m0, n0, k_lo + (st + 3) * BK);
+                    pipe_wait<TA, WN>(st + 1, nst);
+                    stage_frags<TA, WN>(sb1, h, wm, wn, l32, f);
+                    if (st + 3 < nst) stage_issue<TA, WN>(args.A, args.B, sb0, wave, lane, m0, n0, k_lo + (st + 3) * BK);
                     stage_mfma<TA>(f, acc);
                 }
                 if (st + 2 < nst) {
-                    pipe_wait<TA>(st + 2, nst);
-                    stage_frags<TA>(sb2, h, wm, wn, l32, f);
-                    if (st + 4 < nst) stage_issue<TA>(args.A, args.B, sb1, wave, lane, m0, n0, k_lo + (st + 4) * BK);
+                    pipe_wait<TA, WN>(st + 2, nst);
+                    stage_frags<TA, WN>(sb2, h, wm, wn, l32, f);
+                    if (st + 4 < nst) stage_issue<TA, WN>(args.A, args.B, sb1, wave, lane, m0, n0, k_lo + (st + 4) * BK);
                     stage_mfma<TA>(f, acc);
                 }
             }
@@ -373,7 +399,12 @@ __global__ __launch_bounds__(256) void calib_gemm_kernel(const GemmArgs<TA, EPI>
                 }
             }
         }
-        if (t == 0) epi.sq_partial[c * gridDim.x + tn] = ((sq_lds[0] + sq_lds[1]) + sq_lds[2]) + sq_lds[3];
+        if (t == 0) {
+            double tot = sq_lds[0];
+#pragma unroll
+            for (int i = 1; i < 2 * WN; ++i) tot += sq_lds[i];
+            epi.sq_partial[c * gridDim.x + tn] = tot;
+        }
     }
 }
 
@@ -720,6 +751,7 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+
 }  // namespace
 
 CalibPlan calib_plan(int64_t R, int64_t o, int64_t d, int a, int64_t nfac) {
@@ -730,7 +762,7 @@ CalibPlan calib_plan(int64_t R, int64_t o, int64_t d, int a, int64_t nfac) {
     pl.nb = d / 32;
     pl.a = a;
     pl.nfac = nfac;
-    pl.ntn = cdiv(d, CT);
+    pl.ntn = cdiv(d, 64 * kWnBackward);
     pl.act_mt = cdiv(R, CT);
     pl.act_chunks = std::max<int64_t>(1, std::min(pl.act_mt, cdiv(kTargetWg, pl.ntn)));
     pl.w_mt = cdiv(o, CT);
@@ -785,9 +817,9 @@ hipError_t launch_calib_reference(const uint16_t* X, int64_t R, int64_t d, const
     GemmArgs<1, EpiStoreNeg> args{{{reinterpret_cast<const uint8_t*>(X), R, d * 2}},
                                   {reinterpret_cast<const uint8_t*>(W), o, d * 2},
                                   {Yneg, R, o, o},
-                                  {R, o, d, cdiv(R, CT), 1, d, cdiv(R, CT)}};
-    dim3 grid(unsigned(cdiv(o, CT)), unsigned(args.g.chunks));
-    calib_gemm_kernel<1><<<grid, 256, 0, st>>>(args);
+                                  {R, o, d, cdiv(R, CT), 1, d, cdiv(R, CT), 0}};
+    dim3 grid(unsigned(cdiv(o, 64 * kWnReference)), unsigned(args.g.chunks));
+    calib_gemm_kernel<1, kWnReference><<<grid, 128 * kWnReference, 0, st>>>(args);
     return hipGetLastError();
 }
 
@@ -834,9 +866,9 @@ hipError_t launch_calib_backward(const CalibPlan& pl, const CalibStepArgs& s, hi
             {{reinterpret_cast<const uint8_t*>(rnh), R, pl.op * 2}, {reinterpret_cast<const uint8_t*>(rnl), R, pl.op * 2}},
             {reinterpret_cast<const uint8_t*>(wht), d, pl.op * 2},
             {s.X, yA, cA, sA, R, d, c1, s.lambdas, 0, float(2.0 / (double(R) * double(d))), gpa, sqa},
-            {R, d, pl.op, pl.act_mt, 1, pl.op, pl.act_chunks}};
+            {R, d, pl.op, pl.act_mt, 1, pl.op, pl.act_chunks, 1}};
         dim3 grid(unsigned(pl.ntn), unsigned(pl.act_chunks));
-        calib_gemm_kernel<2><<<grid, 256, 0, st>>>(args);
+        calib_gemm_kernel<2, kWnBackward><<<grid, 128 * kWnBackward, 0, st>>>(args);
     }
     // weight side: P = res^T . Ahat  (M = o, N = d, K = R)
     {
@@ -844,9 +876,9 @@ hipError_t launch_calib_backward(const CalibPlan& pl, const CalibStepArgs& s, hi
             {{reinterpret_cast<const uint8_t*>(rth), o, pl.Rp * 2}, {reinterpret_cast<const uint8_t*>(rtl), o, pl.Rp * 2}},
             {reinterpret_cast<const uint8_t*>(aht), d, pl.Rp * 2},
             {s.W, yW, cW, sW, o, d, c1, s.lambdas, 1, float(2.0 / (double(o) * double(d))), gpw, sqw},
-            {o, d, pl.Rp, pl.w_mt, pl.w_ks, pl.w_kchunk, pl.w_chunks}};
+            {o, d, pl.Rp, pl.w_mt, pl.w_ks, pl.w_kchunk, pl.w_chunks, 1}};
         dim3 grid(unsigned(pl.ntn), unsigned(pl.w_chunks));
-        calib_gemm_kernel<2><<<grid, 256, 0, st>>>(args);
+        calib_gemm_kernel<2, kWnBackward><<<grid, 128 * kWnBackward, 0, st>>>(args);
     }
     gram_reduce_kernel<<<dim3(unsigned(pl.nfac), 4), 256, 0, st>>>(gpa, pl.act_chunks, pl.nb, pl.nfac, ga);
     gram_reduce_kernel<<<dim3(unsigned(pl.nfac), 4), 256, 0, st>>>(gpw, pl.w_chunks, pl.nb, pl.nfac, gw);
