@@ -72,7 +72,9 @@ typedef enum kq_status {
  *   A       device, fp32 [nfac, a, a] row-major; B device, fp32 [nfac, b, b]
  *   (a, b)  one of (4, 8), (2, 16), (8, 4), (1, 32)
  *   nfac    1 (one pair for every block) or d/32 (pair f = j for block j:
- *           T = diag(K^(1), ..., K^(d/32)), Sec. 3.1)
+ *           T = diag(K^(1), ..., K^(d/32)), Sec. 3.1); d/32 needs d < 2^25
+ *           (KQ_ERROR_UNSUPPORTED otherwise; the same holds for every call
+ *           that takes per-block factors)
  *   codes   device, uint8 [M, d/2];  scales device, uint8 [M, d/32]
  *   y_out   device, fp32 [M, d] or NULL: the transformed values that were
  *           quantized

@@ -182,6 +182,11 @@ kq_status check_factors(int a, int b, int64_t nfac, int64_t d) {
     if (nfac != 1 && nfac != d / 32)
         return fail(KQ_ERROR_UNSUPPORTED, "nfac = %lld must be 1 or d/32 = %lld", (long long)nfac,
                     (long long)(d / 32));
+    // per-block factors run the column-mapped kernels, whose offsets within
+    // a 64-row unit are 32-bit
+    if (nfac > 1 && d >= (int64_t(1) << 25))
+        return fail(KQ_ERROR_UNSUPPORTED, "per-block factors (nfac = d/32) need d < 2^25, got d = %lld",
+                    (long long)d);
     return ok();
 }
 

@@ -57,7 +57,7 @@ def _q(**kw):
     (dict(X=None), NULLP), (dict(A=None), NULLP), (dict(B=None), NULLP), (dict(codes=None), NULLP),
     (dict(scales=None), NULLP), (dict(X=FAKE + 8), MISALIGNED), (dict(codes=FAKE + 4), MISALIGNED),
     (dict(y=FAKE + 4), MISALIGNED), (dict(A=FAKE + 2), MISALIGNED),
-    (dict(M=1 << 40, d=1 << 30), INVALID),
+    (dict(M=1 << 40, d=1 << 30), INVALID), (dict(d=1 << 25, nfac=1 << 20), UNSUPPORTED),
 ])
 def test_quantize_rejects(kw, status):
     assert _q(**kw) == status
@@ -94,6 +94,7 @@ def test_quantize_lu_rejects():
                                       kw.get("y", None), kw.get("y16", None), None)
     assert q(a=3) == UNSUPPORTED and q(a=16) == UNSUPPORTED and q(a=0) == UNSUPPORTED
     assert q(nfac=3) == UNSUPPORTED
+    assert q(d=1 << 25, nfac=1 << 20) == UNSUPPORTED
     assert q(lu=None) == NULLP
     assert q(lu=FAKE + 2) == MISALIGNED
     assert q(y16=FAKE + 8) == MISALIGNED
