@@ -312,6 +312,17 @@ def main():
         comparators[name + "_gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
     ms_floor_eager, _ = timed_eager(run_floor, args.steps, args.warmup)
     ms_warm, _ = timed(run_kq, args.steps, args.warmup, rotate=False)
+    # the vendor's device-to-device copy moving the same HBM bytes as one step
+    # (half of them read, half written), with the same rotation
+    half = nbytes // 2
+    copy_src = [Xs[i].view(torch.uint8).reshape(-1)[:half] for i in range(nsets)]
+    copy_dst = [torch.empty(half, dtype=torch.uint8, device=dev) for _ in range(nsets)]
+
+    def run_copy(i):
+        copy_dst[i].copy_(copy_src[i])
+
+    ms_copy, _ = timed(run_copy, args.steps, args.warmup)
+    del copy_dst
     table2 = None if args.no_table2 else table2_shapes(kq, synth, dev, stream, sptr)
     wide = None if args.no_wide else wide_shape(kq, synth, dev, stream, timed_graph_steps=args.steps)
     large = None if args.no_large else large_per_block(kq, synth, dev, stream)
@@ -358,6 +369,10 @@ def main():
                           "frac_of_peak": round(comparators["stream_floor_gbs"] / HBM_PEAK_GBS, 4),
                           "hot_path_frac_of_floor": round(comparators["stream_floor_us"] / us_kq, 4),
                           "what": "kq_stream_floor: the same loads, stores and launch shape with no arithmetic"},
+        "vendor_copy": {"us": round(ms_copy * 1e3, 3), "gbs": round(2 * half / (ms_copy * 1e-3) / 1e9, 1),
+                        "frac_of_peak": round(2 * half / (ms_copy * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                        "what": "torch copy_ (device to device) of half the step's bytes: the same HBM traffic "
+                                "as one step, same graph replay and rotation"},
         "paper_context": "other hardware, context only: on an MI350 the paper reports its fused quantizer kernel "
                          "up to 14% faster than its SmoothQuant kernel (abstract; Table 4 lists up to 1.31x)",
         "path": "kq_quantize_packed: matrix cores (v_mfma_f32_32x32x16_bf16, 3-term bf16 split of the "
