@@ -721,9 +721,22 @@ def cpu_baseline(w, nbytes):
         if el >= 10.0 or el + times[-1] > 30.0:
             break
     t = float(np.median(times))
+    # the same oracle on one thread: three passes (median)
+    oracle.set_num_threads(1)
+    try:
+        t1 = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            oracle.quantize(w.X, w.A, w.B)
+            t1.append(time.perf_counter() - t0)
+    finally:
+        oracle.set_num_threads(threads)
+    t1m = float(np.median(t1))
     return {"value": round(nbytes / t / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"{len(times)} full passes of {w.name} (median {t:.3f} s per pass)",
-            "cpu_model": _cpu_model()}
+            "single_thread": {"value": round(nbytes / t1m / 1e9, 3), "unit": "GB/s",
+                              "sample": f"3 full passes of {w.name} on 1 thread (median {t1m:.3f} s per pass)"},
+            "host_cpus": os.cpu_count(), "cpu_model": _cpu_model()}
 
 
 def _cpu_model():
