@@ -106,9 +106,9 @@ struct StageBuf {
     uint4 b[256 * WN];  // 64 WN rows, the same layout
 };
 
-// Loads of one stage per wave (one instruction = 16 rows x 64 bytes):
-// groups of 16 A rows 4 / WN (wave) .. (each term), groups of 16 B rows
-// 2 wave, 2 wave + 1; TA 4 / WN + 2 instructions.
+// Loads of one stage per wave (one instruction = 16 rows x 64 bytes): of
+// each A term the GA = 4 / WN groups of 16 rows GA wave .. GA wave + GA - 1,
+// of B the groups 2 wave and 2 wave + 1; TA GA + 2 instructions in all.
 template <int TA, int WN>
 constexpr int stage_loads() { return TA * (4 / WN) + 2; }
 
