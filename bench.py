@@ -147,7 +147,7 @@ def main():
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this quantizer benchmark runs on exactly one GPU (--gpus 1); the quantizer "
-              "has no cross-GPU step and multi-GPU runs are not part of this build", file=sys.stderr)
+              "has no cross-GPU step, and runs on more than one GPU are not supported", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -1,0 +1,45 @@
+"""The benchmark's output contract on the GPU: one short `bench.py` run (the
+headline workload, few steps, the side measurements switched off) prints one
+JSON line whose fields, units and roofline arithmetic are consistent and whose
+parity check of the timed hot path passed."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+from conftest import ROOT
+
+pytestmark = pytest.mark.gpu
+
+
+def _bench(*args, timeout=240):
+    return subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], cwd=ROOT, capture_output=True,
+                          text=True, timeout=timeout)
+
+
+def test_bench_json_line():
+    r = _bench("--steps", "20", "--warmup", "20", "--no-calib", "--no-gemm", "--no-table2", "--no-large",
+               "--no-wide", "--no-cpu-baseline")
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [ln for ln in r.stdout.splitlines() if ln.startswith("{")]
+    assert len(lines) == 1, r.stdout[-2000:]
+    d = json.loads(lines[0])
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+                "scaling", "vs_baseline", "dtype", "data", "config", "roofline", "cpu_baseline"):
+        assert key in d, key
+    assert d["n_gpus"] == 1 and d["steps"] == 20 and d["warmup"] == 20
+    assert d["unit"] == "GB/s" and d["higher_is_better"] is True and d["data"] == "synthetic"
+    assert d["config"]["workload"] == "flux_4608x3072" and d["config"]["M"] == 4608 and d["config"]["d"] == 3072
+    assert d["value"] > 0
+    # value is the algorithmic bytes of one step over the measured time per step
+    nbytes = 4608 * 3072 * (2 + 0.5 + 1 / 32)
+    assert abs(d["value"] - nbytes / (d["ms_per_step"] * 1e-3) / 1e9) <= 1e-3 * d["value"] + 0.5
+    rf = d["roofline"]
+    assert rf["bound"] == "hbm" and rf["unit"] == "GB/s" and rf["peak"] == 8000.0
+    assert abs(rf["frac"] - rf["achieved"] / rf["peak"]) < 1e-3
+    assert rf["traffic"] is None or rf["traffic"] > nbytes * 0.99
+    assert d["parity"]["hot_path"].startswith("ok"), d["parity"]
+    assert d["parity"]["exact_path"] == "bit-exact"
+

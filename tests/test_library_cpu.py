@@ -235,3 +235,13 @@ def test_calibration_rejects():
                                       kw.get("losses", FAKE), FAKE, kw.get("wsb", need), None)
     assert cal(steps=-1) == INVALID and cal(losses=None) == NULLP and cal(losses=FAKE + 4) == MISALIGNED
     assert cal(wsb=0) == INVALID
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py exits with a message before touching a GPU when asked for more than one."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], cwd=ROOT,
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "exactly one GPU" in r.stderr
