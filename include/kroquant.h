@@ -25,17 +25,16 @@
  *    synchronize; they enqueue one kernel on `stream` (a hipStream_t; NULL =
  *    the null stream) and return.  A fault inside the kernel surfaces at the
  *    caller's next synchronization, as for any HIP launch.
- *  - Alignment: X, codes and y_out must be 16-byte aligned; scales need no
+ *  - Alignment: X, codes and y_out must be 16-byte aligned (every lane moves
+ *    16 contiguous bytes per access; a row of codes is d/2 bytes, a multiple
+ *    of 16, so an aligned base keeps every row aligned); scales need no
  *    alignment; the factors need 4 B and the SmoothQuant multipliers 16 B.
- *  - Environment (read once; tuning knobs that never change results):
- *    KQ_MAX_WAVES (cap on workgroups) and KQ_UNITS_PER_WAVE (1 or 2) set the
- *    launch shape of the on-the-fly matrix-core kernel; KQ_PACKED_PERSISTENT,
- *    KQ_SMOOTH_PATH and KQ_SMOOTH_WAVES select alternative kernel shapes of
- *    kq_quantize_packed and kq_smoothquant_quantize; KQ_GEMM_TILE_M (2 or 4)
- *    selects the register-staged kq_mxfp4_gemm kernel instead of the
- *    LDS-pipelined ones, 8 forces their 256 x 256 tile (by default used once
- *    the product has at least 96 such tiles, else 128 x 128).
  *  - Inputs must be finite; NaN or Inf inputs give unspecified codes.
+ *  - Size: the matrix-core calls (kq_quantize, kq_quantize_packed,
+ *    kq_quantize_lu) launch one workgroup per 64 blocks (shared factors) or
+ *    per 64 rows x 8 column blocks (per-block factors) and return
+ *    KQ_ERROR_UNSUPPORTED when that count exceeds 2^31 - 1 (beyond 2^42
+ *    elements of X, far more than one GPU holds).
  *  - Arguments are validated before any HIP call.  On failure the call
  *    returns the status and kq_last_error_detail() describes the argument
  *    (thread-local).  HIP launch/runtime errors return KQ_ERROR_HIP with the
@@ -263,9 +262,15 @@ kq_status kq_weight_transform(const uint16_t* W, int64_t o, int64_t d, const flo
                               uint8_t* codes, uint8_t* scales, void* stream);
 
 /*
- * kq_factors_inverse_transpose -- host helper: A_it[f] = fp32(inv(A[f])^T),
- * B_it[f] = fp32(inv(B[f])^T) with fp64 Gauss-Jordan and partial pivoting;
- * all arrays are HOST memory.  Same singularity rule as kq_weight_transform.
+ * kq_factors_inverse_transpose -- host helper for the weight side of eq. (1)
+ * (Sec. 3.1: W is multiplied by T^-T so that X T (W T^-T)^T = X W^T) with the
+ * inverse of a Kronecker product taken factor by factor,
+ * (A (x) B)^-T = A^-T (x) B^-T (Sec. 3.2): A_it[f] = fp32(inv(A[f])^T),
+ * B_it[f] = fp32(inv(B[f])^T) with fp64 Gauss-Jordan and partial pivoting.
+ *   A, B     HOST fp32 [nfac, a, a], [nfac, b, b] (forward factors)
+ *   A_it, B_it  HOST fp32, same shapes (caller-owned)
+ * (a, b) and nfac as for kq_quantize (any nfac >= 1).  Same singularity rule
+ * as kq_weight_transform (KQ_ERROR_SINGULAR, outputs then unspecified).
  */
 kq_status kq_factors_inverse_transpose(const float* A, const float* B, int a, int b,
                                        int64_t nfac, float* A_it, float* B_it);

@@ -368,3 +368,75 @@ def lu_to_factors(abc, a_dim):
         As.append(Ka.T)
         Bs.append(Kb.T)
     return np.array(As, dtype=np.float32), np.array(Bs, dtype=np.float32)
+
+
+# ---------------------------------------------------------------- tolerance rule
+# Decision points of the E2M1 encode on v = |y| / 2^(s - 127): the sign decision
+# at 0 and the midpoints between neighbouring magnitudes (Sec. 3.1 quantizer,
+# OCP MX v1.0 E2M1).
+E2M1_DECISION_POINTS = np.array([0.0, 0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0], dtype=np.float64)
+
+
+def mx_compare(codes, scales, codes_ref, scales_ref, y_ref=None, y=None, rel_tol=1e-5, max_flip_frac=1e-4):
+    """Compare an MXFP4 result with the oracle's under the tolerance of a path
+    whose fp32 accumulation order differs from the oracle's:
+
+    * E8M0 scales identical;
+    * codes identical except flips to the adjacent magnitude (|dmag| = 1) or a
+      sign-only flip of magnitude 0, at most ``max_flip_frac`` of all codes;
+    * with ``y_ref`` (the oracle's fp32 transformed values): every flip sits at
+      a rounding decision, |v_ref - t| <= rel_tol * 8 with v_ref = |y_ref| /
+      2^(s - 127) and t the nearest decision point (an fp32 result within
+      rel_tol of max(|y_ref|, amax_block / 32) moves v by at most that much,
+      since v < 8);
+    * with ``y`` as well: max |y - y_ref| / max(|y_ref|, amax_block / 32) <= rel_tol.
+
+    Works on the packed bytes and unpacks only the differing ones, so it is
+    cheap at full size.  Returns a dict with the counts and ``ok``."""
+    codes, codes_ref = np.asarray(codes, np.uint8), np.asarray(codes_ref, np.uint8)
+    scales, scales_ref = np.asarray(scales, np.uint8), np.asarray(scales_ref, np.uint8)
+    if codes.shape != codes_ref.shape or scales.shape != scales_ref.shape:
+        raise ValueError("result and reference shapes differ")
+    M = codes.shape[0]
+    nbytes_row = codes.shape[1]
+    rep = {"codes": int(codes.size * 2), "scale_mismatches": int(np.count_nonzero(scales != scales_ref))}
+    flat, flat_ref = codes.reshape(-1), codes_ref.reshape(-1)
+    byte_idx = np.flatnonzero(flat != flat_ref)
+    lo = (flat[byte_idx] & 0xF, flat_ref[byte_idx] & 0xF)
+    hi = (flat[byte_idx] >> 4, flat_ref[byte_idx] >> 4)
+    elem = np.concatenate([2 * byte_idx[lo[0] != lo[1]], 2 * byte_idx[hi[0] != hi[1]] + 1])
+    got = np.concatenate([lo[0][lo[0] != lo[1]], hi[0][hi[0] != hi[1]]]).astype(np.int64)
+    ref = np.concatenate([lo[1][lo[0] != lo[1]], hi[1][hi[0] != hi[1]]]).astype(np.int64)
+    dmag = np.abs((got & 7) - (ref & 7))
+    sign_only_zero = ((got & 7) == 0) & ((ref & 7) == 0)
+    rep["flips"] = int(elem.size)
+    rep["non_adjacent"] = int(np.count_nonzero(~((dmag == 1) | sign_only_zero)))
+    rep["flip_frac"] = rep["flips"] / max(rep["codes"], 1)
+    rep["off_tie"] = None
+    if y_ref is not None and elem.size:
+        y_ref_flat = np.asarray(y_ref, np.float32).reshape(-1)
+        r, k = elem // (2 * nbytes_row), elem % (2 * nbytes_row)
+        s = scales_ref[r, k // 32].astype(np.float64)
+        v = np.abs(y_ref_flat[elem].astype(np.float64)) * np.exp2(127.0 - s)
+        dist = np.min(np.abs(v[:, None] - E2M1_DECISION_POINTS[None, :]), axis=1)
+        rep["off_tie"] = int(np.count_nonzero(dist > rel_tol * 8.0))
+        rep["max_tie_distance"] = float(dist.max())
+    elif y_ref is not None:
+        rep["off_tie"] = 0
+    rep["y_max_err"] = None
+    if y is not None and y_ref is not None:
+        worst = 0.0
+        step = max(1, (1 << 22) // max(nbytes_row * 2, 1))
+        for r0 in range(0, M, step):
+            yr = np.asarray(y_ref[r0:r0 + step], np.float64)
+            yg = np.asarray(y[r0:r0 + step], np.float64)
+            amax = np.abs(yr).reshape(yr.shape[0], -1, 32).max(-1)
+            den = np.maximum(np.abs(yr), np.repeat(amax, 32, axis=1) / 32.0)
+            den = np.where(den > 0, den, 1.0)
+            if yr.size:
+                worst = max(worst, float(np.max(np.abs(yg - yr) / den)))
+        rep["y_max_err"] = worst
+    rep["ok"] = bool(rep["scale_mismatches"] == 0 and rep["non_adjacent"] == 0
+                     and rep["flip_frac"] <= max_flip_frac and (rep["off_tie"] in (None, 0))
+                     and (rep["y_max_err"] is None or rep["y_max_err"] <= rel_tol))
+    return rep

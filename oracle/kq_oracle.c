@@ -259,15 +259,16 @@ int kqo_e8m0_scales(const float* amax, int64_t n, uint8_t* out) {
  *     (u_i, u_{i+h}) <- (u_i + u_{i+h}, u_i - u_{i+h}),  h = 1, 2, 4, ..., d/2,
  * in fp32, then one multiply by the fp32 nearest to 1/sqrt(d); then MXFP4 of
  * every 32-element block of the transformed row.  For d = 32 this is exactly
- * the Hadamard-32 comparator. */
+ * the Hadamard-32 comparator.  Returns -1 (nothing written) unless d is a
+ * power of two from 32 to 2^16. */
 int kqo_fwht(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, uint8_t* scales, float* yout) {
-    if (M < 0 || d < BLK || (d & (d - 1)) != 0) return -1;
+    /* d a power of two from 32 up to the row buffer below (2^16 elements) */
+    if (M < 0 || d < BLK || d > (1 << 16) || (d & (d - 1)) != 0) return -1;
     if (!X || !codes || !scales) return -2;
     const float inv_sqrt_d = (float)(1.0 / sqrt((double)d));
 #pragma omp parallel for schedule(static)
     for (int64_t r = 0; r < M; ++r) {
         float u[1 << 16];
-        if (d > (1 << 16)) continue;
         for (int64_t k = 0; k < d; ++k) u[k] = bf16_to_f32(X[r * d + k]);
         for (int64_t h = 1; h < d; h <<= 1) {
             for (int64_t i = 0; i < d; ++i) {

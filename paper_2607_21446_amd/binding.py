@@ -105,27 +105,59 @@ def _need(t, dtype, name, device=True):
         raise ValueError(f"{name} must be contiguous")
 
 
+def _size(t, numel, name, device=None):
+    """A caller-supplied buffer must hold exactly the elements the call reads
+    or writes (an undersized one would be accessed out of bounds) and sit on
+    the device of the input."""
+    if t.numel() != numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, the call needs {numel}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the input on {device}")
+
+
+def _matrix(X, name="X"):
+    if X.dim() != 2:
+        raise ValueError(f"{name} must be a 2-D [rows, columns] tensor, got shape {tuple(X.shape)}")
+    return X.shape
+
+
 def _outputs(X, codes, scales, y, want_y):
-    M, d = X.shape
+    M, d = _matrix(X)
     if codes is None:
         codes = torch.empty((M, d // 2), dtype=torch.uint8, device=X.device)
     if scales is None:
         scales = torch.empty((M, d // 32), dtype=torch.uint8, device=X.device)
     if y is None and want_y:
         y = torch.empty((M, d), dtype=torch.float32, device=X.device)
-    _need(codes, torch.uint8, "codes")
-    _need(scales, torch.uint8, "scales")
+    # on X's device (the public calls require X to be a device tensor)
+    _need(codes, torch.uint8, "codes", device=False)
+    _need(scales, torch.uint8, "scales", device=False)
+    _size(codes, M * (d // 2), "codes", X.device)
+    _size(scales, M * (d // 32), "scales", X.device)
     if y is not None:
-        _need(y, torch.float32, "y")
+        _need(y, torch.float32, "y", device=False)
+        _size(y, M * d, "y", X.device)
     return codes, scales, y
+
+
+def _pairs(A, B, device=None):
+    """Factor pairs A [nfac, a, a], B [nfac, b, b]: returns (a, b, nfac)."""
+    a, b = A.shape[-1], B.shape[-1]
+    if A.dim() < 2 or A.shape[-2] != a or B.dim() < 2 or B.shape[-2] != b:
+        raise ValueError(f"A and B must be [nfac, a, a] and [nfac, b, b], got {tuple(A.shape)}, {tuple(B.shape)}")
+    nfac = A.numel() // (a * a)
+    if B.numel() != nfac * b * b:
+        raise ValueError(f"A holds {nfac} factors of {a}x{a}, B {B.numel() / (b * b):g} of {b}x{b}")
+    if device is not None and (A.device != device or B.device != device):
+        raise ValueError(f"A ({A.device}) and B ({B.device}) must be on the input's device {device}")
+    return a, b, nfac
 
 
 def _kron(fn, name, X, A, B, codes, scales, y, want_y, stream):
     _need(X, torch.bfloat16, "X")
     _need(A, torch.float32, "A")
     _need(B, torch.float32, "B")
-    a, b = A.shape[-1], B.shape[-1]
-    nfac = A.numel() // (a * a)
+    a, b, nfac = _pairs(A, B, X.device)
     codes, scales, y = _outputs(X, codes, scales, y, want_y)
     M, d = X.shape
     _check(fn(_ptr(X), M, d, _ptr(A), _ptr(B), a, b, nfac, _ptr(codes), _ptr(scales), _ptr(y),
@@ -154,11 +186,11 @@ def pack_factors(A, B, kpack=None, stream=None):
     (offline, once per layer).  Returns a uint8 device tensor."""
     _need(A, torch.float32, "A")
     _need(B, torch.float32, "B")
-    a, b = A.shape[-1], B.shape[-1]
-    nfac = A.numel() // (a * a)
+    a, b, nfac = _pairs(A, B, A.device)
     if kpack is None:
         kpack = torch.empty(nfac * PACK_BYTES_PER_FACTOR, dtype=torch.uint8, device=A.device)
     _need(kpack, torch.uint8, "kpack")
+    _size(kpack, nfac * PACK_BYTES_PER_FACTOR, "kpack", A.device)
     _check(lib().kq_pack_factors(_ptr(A), _ptr(B), a, b, nfac, _ptr(kpack), _stream(stream)), "kq_pack_factors")
     return kpack
 
@@ -169,8 +201,8 @@ def quantize_packed(X, A, B, kpack, codes=None, scales=None, y=None, want_y=Fals
     _need(A, torch.float32, "A")
     _need(B, torch.float32, "B")
     _need(kpack, torch.uint8, "kpack")
-    a, b = A.shape[-1], B.shape[-1]
-    nfac = A.numel() // (a * a)
+    a, b, nfac = _pairs(A, B, X.device)
+    _size(kpack, nfac * PACK_BYTES_PER_FACTOR, "kpack", X.device)
     codes, scales, y = _outputs(X, codes, scales, y, want_y)
     M, d = X.shape
     _check(lib().kq_quantize_packed(_ptr(X), M, d, _ptr(A), _ptr(B), a, b, nfac, _ptr(kpack), _ptr(codes),
@@ -185,15 +217,17 @@ def quantize_lu(X, lu, a=4, codes=None, scales=None, y=None, y16=None, want_y=Fa
     Returns (codes, scales, y or None, y16 or None); y16 is bf16 [M, d]."""
     _need(X, torch.bfloat16, "X")
     _need(lu, torch.float32, "lu")
-    if lu.numel() % 15:
+    if lu.numel() % 15 or lu.numel() == 0:
         raise ValueError("lu must hold 15 parameters per factor pair")
     nfac = lu.numel() // 15
+    _size(lu, nfac * 15, "lu", X.device)
     codes, scales, y = _outputs(X, codes, scales, y, want_y)
     M, d = X.shape
     if y16 is None and want_y16:
         y16 = torch.empty((M, d), dtype=torch.bfloat16, device=X.device)
     if y16 is not None:
         _need(y16, torch.bfloat16, "y16")
+        _size(y16, M * d, "y16", X.device)
     _check(lib().kq_quantize_lu(_ptr(X), M, d, _ptr(lu), a, nfac, _ptr(codes), _ptr(scales), _ptr(y), _ptr(y16),
                                 _stream(stream)), "kq_quantize_lu")
     return codes, scales, y, y16
@@ -205,6 +239,7 @@ def smoothquant(X, mult, codes=None, scales=None, y=None, want_y=False, stream=N
     _need(mult, torch.float32, "mult")
     codes, scales, y = _outputs(X, codes, scales, y, want_y)
     M, d = X.shape
+    _size(mult, d, "mult", X.device)
     _check(lib().kq_smoothquant_quantize(_ptr(X), M, d, _ptr(mult), _ptr(codes), _ptr(scales), _ptr(y),
                                          _stream(stream)), "kq_smoothquant_quantize")
     return codes, scales, y
@@ -235,12 +270,19 @@ def mxfp4_gemm(a_codes, a_scales, b_codes, b_scales, C=None, accumulate=False, s
     uint8 [rows, K/2], scales uint8 [rows, K/32]).  Returns C (fp32)."""
     for t, name in ((a_codes, "a_codes"), (a_scales, "a_scales"), (b_codes, "b_codes"), (b_scales, "b_scales")):
         _need(t, torch.uint8, name)
+    _matrix(a_codes, "a_codes")
+    _matrix(b_codes, "b_codes")
     M, N, K = a_codes.shape[0], b_codes.shape[0], 2 * a_codes.shape[1]
     if b_codes.shape[1] * 2 != K or a_scales.shape != (M, K // 32) or b_scales.shape != (N, K // 32):
         raise ValueError("operand shapes do not match")
+    dev = a_codes.device
+    if any(t.device != dev for t in (a_scales, b_codes, b_scales)):
+        raise ValueError("all operands must be on one device")
     if C is None:
-        C = torch.empty((M, N), dtype=torch.float32, device=a_codes.device)
+        C = torch.empty((M, N), dtype=torch.float32, device=dev)
     _need(C, torch.float32, "C")
+    if tuple(C.shape) != (M, N) or C.device != dev:
+        raise ValueError(f"C must be [{M}, {N}] on {dev}, got {tuple(C.shape)} on {C.device}")
     _check(lib().kq_mxfp4_gemm(_ptr(a_codes), _ptr(a_scales), M, _ptr(b_codes), _ptr(b_scales), N, K, _ptr(C),
                                C.stride(0), int(accumulate), _stream(stream)), "kq_mxfp4_gemm")
     return C
@@ -271,6 +313,8 @@ def e2m1_encode(v, s, codes=None, stream=None):
     n = v.numel()
     if codes is None:
         codes = torch.empty(n // 2, dtype=torch.uint8, device=v.device)
+    _need(codes, torch.uint8, "codes")
+    _size(codes, n // 2, "codes", v.device)
     _check(lib().kq_e2m1_encode(_ptr(v), n, int(s), _ptr(codes), _stream(stream)), "kq_e2m1_encode")
     return codes
 
@@ -281,11 +325,12 @@ def weight_transform(W, A_host, B_host, W_out=None, codes=None, scales=None, qua
     _need(W, torch.bfloat16, "W")
     A_host = A_host.detach().to("cpu", torch.float32).contiguous()
     B_host = B_host.detach().to("cpu", torch.float32).contiguous()
-    a, b = A_host.shape[-1], B_host.shape[-1]
-    nfac = A_host.numel() // (a * a)
-    o, d = W.shape
+    a, b, nfac = _pairs(A_host, B_host)
+    o, d = _matrix(W, "W")
     if W_out is None:
         W_out = torch.empty((o, d), dtype=torch.float32, device=W.device)
+    _need(W_out, torch.float32, "W_out")
+    _size(W_out, o * d, "W_out", W.device)
     if quantize:
         codes, scales, _ = _outputs(W, codes, scales, None, False)
     _check(lib().kq_weight_transform(_ptr(W), o, d, _ptr(A_host), _ptr(B_host), a, b, nfac, _ptr(W_out),
@@ -297,8 +342,7 @@ def factors_inverse_transpose(A, B):
     """Host helper kq_factors_inverse_transpose on CPU fp32 tensors."""
     A = A.detach().to("cpu", torch.float32).contiguous()
     B = B.detach().to("cpu", torch.float32).contiguous()
-    a, b = A.shape[-1], B.shape[-1]
-    nfac = A.numel() // (a * a)
+    a, b, nfac = _pairs(A, B)
     Ait, Bit = torch.empty_like(A), torch.empty_like(B)
     _check(lib().kq_factors_inverse_transpose(_ptr(A), _ptr(B), a, b, nfac, _ptr(Ait), _ptr(Bit)),
            "kq_factors_inverse_transpose")
@@ -308,6 +352,8 @@ def factors_inverse_transpose(A, B):
 def lu_to_factors(abc, a):
     """Host helper kq_lu_to_factors: abc CPU fp32 [nfac, 5, 3] -> (A, B)."""
     abc = abc.detach().to("cpu", torch.float32).contiguous()
+    if abc.numel() % 15 or abc.numel() == 0:
+        raise ValueError("abc must hold 15 parameters per factor pair")
     nfac = abc.numel() // 15
     b = 32 // a
     A = torch.empty((nfac, a, a), dtype=torch.float32)
@@ -347,15 +393,29 @@ def calib_reference(X, W, Yneg=None, stream=None):
     """kq_calib_reference: Yneg = -(X W^T), fp32 [R, o]."""
     _need(X, torch.bfloat16, "X")
     _need(W, torch.bfloat16, "W")
-    R, d = X.shape
-    o = W.shape[0]
-    if W.shape[1] != d:
-        raise ValueError("X and W must have the same number of columns")
+    R, d = _matrix(X)
+    o = _matrix(W, "W")[0]
+    if W.shape[1] != d or W.device != X.device:
+        raise ValueError("X and W must have the same number of columns and sit on one device")
     if Yneg is None:
         Yneg = torch.empty((R, o), dtype=torch.float32, device=X.device)
     _need(Yneg, torch.float32, "Yneg")
+    _size(Yneg, R * o, "Yneg", X.device)
     _check(lib().kq_calib_reference(_ptr(X), R, d, _ptr(W), o, _ptr(Yneg), _stream(stream)), "kq_calib_reference")
     return Yneg
+
+
+def _calib_shapes(X, W, Yneg, lu):
+    R, d = _matrix(X)
+    o = _matrix(W, "W")[0]
+    if W.shape[1] != d or W.device != X.device:
+        raise ValueError("X and W must have the same number of columns and sit on one device")
+    _need(Yneg, torch.float32, "Yneg")
+    _size(Yneg, R * o, "Yneg", X.device)
+    if lu.numel() % 15 or lu.numel() == 0:
+        raise ValueError("lu must hold 15 parameters per factor pair")
+    _size(lu, lu.numel(), "lu", X.device)
+    return R, d, o, lu.numel() // 15
 
 
 def calib_step(X, W, Yneg, lu, lambdas, a=4, workspace=None, adam=None, grad=None, losses=None, stream=None):
@@ -368,19 +428,26 @@ def calib_step(X, W, Yneg, lu, lambdas, a=4, workspace=None, adam=None, grad=Non
     _need(Yneg, torch.float32, "Yneg")
     _need(lu, torch.float32, "lu")
     _need(lambdas, torch.float32, "lambdas")
-    R, d = X.shape
-    o = W.shape[0]
-    nfac = lu.numel() // 15
+    R, d, o, nfac = _calib_shapes(X, W, Yneg, lu)
+    _size(lambdas, 2, "lambdas", X.device)
     if workspace is None:
         workspace = calib_workspace(R, o, d, a, nfac, X.device)
+    _need(workspace, torch.uint8, "workspace")
     if grad is None:
         grad = torch.empty((nfac, 5, 3), dtype=torch.float32, device=X.device)
     if losses is None:
         losses = torch.empty(4, dtype=torch.float64, device=X.device)
+    _need(grad, torch.float32, "grad")
+    _size(grad, nfac * 15, "grad", X.device)
+    _need(losses, torch.float64, "losses")
+    _size(losses, 4, "losses", X.device)
     m = v = None
     t, lr = 0, 0.0
     if adam is not None:
         m, v, t, lr = adam
+        for buf, name in ((m, "adam m"), (v, "adam v")):
+            _need(buf, torch.float32, name)
+            _size(buf, nfac * 15, name, X.device)
     _check(lib().kq_calib_step(_ptr(X), R, d, _ptr(W), o, _ptr(Yneg), _ptr(lu), a, nfac, _ptr(lambdas), _ptr(grad),
                                _ptr(losses), _ptr(m), _ptr(v), int(t), float(lr), _ptr(workspace),
                                workspace.numel(), _stream(stream)), "kq_calib_step")
@@ -394,16 +461,16 @@ def calibrate(X, W, lu=None, a=4, per_block=True, steps=100, lr=1e-2, Yneg=None,
     losses fp64 [steps + 2, 4])."""
     _need(X, torch.bfloat16, "X")
     _need(W, torch.bfloat16, "W")
-    R, d = X.shape
-    o = W.shape[0]
+    R, d = _matrix(X)
     if lu is None:
         lu = hadamard_lu(d // 32 if per_block else 1, X.device)
     _need(lu, torch.float32, "lu")
-    nfac = lu.numel() // 15
     if Yneg is None:
         Yneg = calib_reference(X, W, stream=stream)
+    R, d, o, nfac = _calib_shapes(X, W, Yneg, lu)
     if workspace is None:
         workspace = calib_workspace(R, o, d, a, nfac, X.device)
+    _need(workspace, torch.uint8, "workspace")
     losses = torch.empty((steps + 2, 4), dtype=torch.float64, device=X.device)
     _check(lib().kq_calibrate(_ptr(X), R, d, _ptr(W), o, _ptr(Yneg), _ptr(lu), a, nfac, int(steps), float(lr),
                               _ptr(losses), _ptr(workspace), workspace.numel(), _stream(stream)), "kq_calibrate")

@@ -79,39 +79,6 @@ kq::Params make_params(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, 
     return p;
 }
 
-// KQ_MAX_WAVES, KQ_UNITS_PER_WAVE and the switches below (optional, read once): launch shape of
-// the matrix-core kernel.  Tuning knobs only; outputs do not depend on them.
-kq::LaunchConfig default_config() {
-    static const kq::LaunchConfig cfg = [] {
-        kq::LaunchConfig c;
-        if (const char* e = std::getenv("KQ_MAX_WAVES")) {
-            const long long v = std::atoll(e);
-            if (v >= 1 && v <= (1 << 30)) c.max_waves = v;
-        }
-        if (const char* e = std::getenv("KQ_PACKED_PERSISTENT")) c.packed_one_unit = std::atoi(e) == 0;
-        if (const char* e = std::getenv("KQ_ONTHEFLY_PERSISTENT")) c.build_unit = std::atoi(e) == 0;
-        if (const char* e = std::getenv("KQ_COLUMN_TILE")) c.column_tile = std::atoi(e) != 0;
-        if (const char* e = std::getenv("KQ_TILE_ROWS")) {
-            const int v = std::atoi(e);
-            if (v >= 0 && v <= 8) c.tile_row_blocks = v;
-        }
-        if (const char* e = std::getenv("KQ_SMOOTH_PATH")) {
-            const int v = std::atoi(e);
-            if (v >= 0 && v <= 3) c.smooth_path = v;
-        }
-        if (const char* e = std::getenv("KQ_SMOOTH_WAVES")) {
-            const long long v = std::atoll(e);
-            if (v >= 1 && v <= (1 << 24)) c.smooth_waves = v;
-        }
-        if (const char* e = std::getenv("KQ_UNITS_PER_WAVE")) {
-            const int v = std::atoi(e);
-            if (v == 1 || v == 2) c.units_per_wave = v;
-        }
-        return c;
-    }();
-    return cfg;
-}
-
 // fp64 Gauss-Jordan inverse with partial pivoting of an n x n fp32 matrix.
 // Returns false if a pivot is below 1e-12 times the infinity norm of its row
 // or if the infinity-norm condition number exceeds 1e6.
@@ -190,6 +157,20 @@ kq_status check_factors(int a, int b, int64_t nfac, int64_t d) {
     return ok();
 }
 
+// The matrix-core kernels launch one workgroup per 64-block unit (shared
+// factors) or per 64-row x 8-column-block tile (per-block factors); both
+// counts must fit one launch (2^31 - 1 workgroups, i.e. more than 2^42
+// elements of X).
+kq_status check_grid(int64_t M, int64_t d, int64_t nfac) {
+    const int64_t nb = d / 32;
+    const int64_t groups = nfac == 1 ? (M / 64) * nb + ((M % 64) * nb + 63) / 64
+                                     : ((M + 63) / 64) * ((nb + 7) / 8);
+    if (groups > kq::kMaxUnitGrid)
+        return fail(KQ_ERROR_UNSUPPORTED, "M = %lld, d = %lld needs %lld workgroups, more than one launch holds",
+                    (long long)M, (long long)d, (long long)groups);
+    return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -204,13 +185,14 @@ static kq_status quantize_kron(kq::Kind kind, const char* name, const uint16_t* 
     if (!aligned(A, 4) || !aligned(B, 4)) return fail(KQ_ERROR_MISALIGNED, "A and B must be 4-byte aligned");
     if (kpack && !aligned(kpack, 16)) return fail(KQ_ERROR_MISALIGNED, "kpack must be 16-byte aligned");
     if (M == 0) return ok();
+    if (kind != kq::Kind::Kron && (st = check_grid(M, d, nfac)) != KQ_SUCCESS) return st;
     kq::Params p = make_params(X, M, d, codes, scales, y_out);
     p.A = A;
     p.B = B;
     p.nfac = nfac;
     p.kpack = static_cast<const uint8_t*>(kpack);
     const kq::Mapping map = (nfac == 1) ? kq::Mapping::Flat : kq::Mapping::Column;
-    return from_hip(kq::launch(kind, a, p, map, (hipStream_t)stream, default_config()), name);
+    return from_hip(kq::launch(kind, a, p, map, (hipStream_t)stream), name);
 }
 
 kq_status kq_quantize(const uint16_t* X, int64_t M, int64_t d, const float* A, const float* B, int a,
@@ -238,12 +220,13 @@ kq_status kq_quantize_lu(const uint16_t* X, int64_t M, int64_t d, const float* l
     if (!aligned(lu, 4)) return fail(KQ_ERROR_MISALIGNED, "lu must be 4-byte aligned");
     if (y16_out && !aligned(y16_out, 16)) return fail(KQ_ERROR_MISALIGNED, "y16_out must be 16-byte aligned");
     if (M == 0) return ok();
+    if ((st = check_grid(M, d, nfac)) != KQ_SUCCESS) return st;
     kq::Params p = make_params(X, M, d, codes, scales, y_out);
     p.nfac = nfac;
     p.lu = lu;
     p.y16 = y16_out;
     const kq::Mapping map = (nfac == 1) ? kq::Mapping::Flat : kq::Mapping::Column;
-    return from_hip(kq::launch(kq::Kind::KronLU, a, p, map, (hipStream_t)stream, default_config()), "kq_quantize_lu");
+    return from_hip(kq::launch(kq::Kind::KronLU, a, p, map, (hipStream_t)stream), "kq_quantize_lu");
 }
 
 kq_status kq_pack_factors(const float* A, const float* B, int a, int b, int64_t nfac, void* kpack, void* stream) {
@@ -272,7 +255,7 @@ kq_status kq_smoothquant_quantize(const uint16_t* X, int64_t M, int64_t d, const
     if (M == 0) return ok();
     kq::Params p = make_params(X, M, d, codes, scales, y_out);
     p.mult = mult;
-    return from_hip(kq::launch(kq::Kind::Smooth, 0, p, kq::Mapping::Flat, (hipStream_t)stream, default_config()),
+    return from_hip(kq::launch(kq::Kind::Smooth, 0, p, kq::Mapping::Flat, (hipStream_t)stream),
                     "kq_smoothquant_quantize");
 }
 
@@ -282,7 +265,7 @@ kq_status kq_hadamard32_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_
     if (st != KQ_SUCCESS) return st;
     if (M == 0) return ok();
     kq::Params p = make_params(X, M, d, codes, scales, y_out);
-    return from_hip(kq::launch(kq::Kind::Hadamard, 0, p, kq::Mapping::Flat, (hipStream_t)stream, default_config()),
+    return from_hip(kq::launch(kq::Kind::Hadamard, 0, p, kq::Mapping::Flat, (hipStream_t)stream),
                     "kq_hadamard32_quantize");
 }
 
@@ -324,15 +307,6 @@ static kq::GemmParams gemm_params(const uint8_t* a_codes, const uint8_t* a_scale
     g.bias = bias;
     g.vec_ok = aligned(C, 16) && ldc % 4 == 0 && (!bias || aligned(bias, 16));
     g.scales_aligned = aligned(a_scales, 4) && aligned(b_scales, 4);
-    // KQ_GEMM_TILE_M (optional, read once): 0 = LDS-pipelined kernels (default: 256 x 256 tiles when there
-    // are at least 96 of them, else 128 x 128), 8 = always 256 x 256, 2 or 4 = register-staged kernel with
-    // that many instruction tiles per wave along M (tuning only)
-    static const int tile_m = [] {
-        const char* e = std::getenv("KQ_GEMM_TILE_M");
-        const int v = e ? std::atoi(e) : 0;
-        return (v == 2 || v == 4 || v == 8) ? v : 0;
-    }();
-    g.tile_m = tile_m;
     return g;
 }
 
@@ -360,7 +334,7 @@ kq_status kq_mxfp4_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* co
     if (st != KQ_SUCCESS) return st;
     if (M == 0) return ok();
     kq::Params p = make_params(X, M, d, codes, scales, nullptr);
-    return from_hip(kq::launch(kq::Kind::Plain, 0, p, kq::Mapping::Flat, (hipStream_t)stream, default_config()),
+    return from_hip(kq::launch(kq::Kind::Plain, 0, p, kq::Mapping::Flat, (hipStream_t)stream),
                     "kq_mxfp4_quantize");
 }
 
@@ -409,7 +383,7 @@ kq_status kq_weight_transform(const uint16_t* W, int64_t o, int64_t d, const flo
         p.B = dev + Ait.size();
         p.nfac = nfac;
         const kq::Mapping map = (nfac == 1) ? kq::Mapping::Flat : kq::Mapping::Column;
-        e = kq::launch(kq::Kind::Kron, a, p, map, s, default_config());
+        e = kq::launch(kq::Kind::Kron, a, p, map, s);
     }
     // the host vectors and the device buffer must outlive the queued work
     const hipError_t es = hipStreamSynchronize(s);

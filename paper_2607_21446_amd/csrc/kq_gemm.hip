@@ -117,160 +117,8 @@ __global__ __launch_bounds__(256) void mxfp4_gemm_kernel(const GemmParams g) {
         }
 }
 
-// Tiled variant for K a multiple of 128 (the usual case; the kernel above
-// takes any K).  The matrix-core rows are the weights (N) and its columns the
-// activations (M), so each lane ends with four consecutive C columns of one C
-// row per accumulator row-group: 16-byte stores.  Workgroup tile 128 (N) x 256
-// (M), waves 2 x 2 of 64 x 128 (2 x 4 instruction tiles, eight accumulators).
-// K advances 128 at a time (four blocks, two instruction steps): the next
-// stage's codes are loaded into registers while the current stage is
-// multiplied out of LDS, then written to the other LDS buffer (one barrier
-// per stage).  LDS holds each operand block-major, [step][half][row][16 B],
-// so a wave's fragment read is 64 consecutive 16-byte slots.  A lane's scale
-// bytes for a stage are one aligned dword per row (four blocks), rearranged
-// with v_perm so that byte s is block 2 s + (lane / 32): the instruction's
-// opsel then picks step s.
-constexpr int kGemmTileN = 128, kGemmTileK = 128;
-
-// Staging of one stage: chunk c = row * 4 + block; W 512 chunks (2 per
-// thread), X 1024 (4 per thread).
-template <int TM>
-struct Stage {
-    uint4 w[2], x[TM];
-};
-
-template <int TM>
-__device__ __forceinline__ void load_stage(const GemmParams& g, int t, int64_t nb0, int64_t mb0, int64_t row_bytes,
-                                           int64_t st, Stage<TM>& sg) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int c = t + 256 * i;
-        const int64_t n = nb0 + (c >> 2);
-        sg.w[i] = make_uint4(0u, 0u, 0u, 0u);
-        if (n < g.N) sg.w[i] = *reinterpret_cast<const uint4*>(g.b_codes + n * row_bytes + (4 * st + (c & 3)) * 16);
-    }
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-        const int c = t + 256 * i;
-        const int64_t m = mb0 + (c >> 2);
-        sg.x[i] = make_uint4(0u, 0u, 0u, 0u);
-        if (m < g.M) sg.x[i] = *reinterpret_cast<const uint4*>(g.a_codes + m * row_bytes + (4 * st + (c & 3)) * 16);
-    }
-}
-
-template <int TM>
-__device__ __forceinline__ void store_stage(uint4* lw, uint4* lx, int t, const Stage<TM>& sg) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int c = t + 256 * i;
-        lw[(c & 3) * kGemmTileN + (c >> 2)] = sg.w[i];  // block b = 2 step + half
-    }
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-        const int c = t + 256 * i;
-        lx[(c & 3) * (64 * TM) + (c >> 2)] = sg.x[i];
-    }
-}
-
-// A lane's scale bytes of one stage for one row: byte s = block 2 s + half.
-__device__ __forceinline__ uint32_t stage_scales(const uint8_t* sc, int64_t row, int64_t nrows, int64_t nkb, int64_t st,
-                                                 uint32_t psel) {
-    uint32_t w = 0x7F7F7F7Fu;
-    if (row < nrows) w = *reinterpret_cast<const uint32_t*>(sc + row * nkb + 4 * st);
-    return __builtin_amdgcn_perm(0u, w, psel);
-}
-
-template <int STEP, int TM>
-__device__ __forceinline__ void stage_step(const uint4* lw, const uint4* lx, int h, int wn, int wm, int r,
-                                           const uint32_t (&scw)[2], const uint32_t (&scx)[TM], f32x16g (&acc)[2][TM]) {
-    uint4 fw[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) fw[i] = lw[(2 * STEP + h) * kGemmTileN + wn * 64 + 32 * i + r];
-#pragma unroll
-    for (int j = 0; j < TM; ++j) {
-        const uint4 fx = lx[(2 * STEP + h) * (64 * TM) + wm * (32 * TM) + 32 * j + r];
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                operand(Frag{fw[i], 0u}), operand(Frag{fx, 0u}), acc[i][j], 4, 4, STEP, (int)scw[i], STEP, (int)scx[j]);
-    }
-}
-
-template <int TM>
-__global__ __launch_bounds__(256) void mxfp4_gemm_tiled_kernel(const GemmParams g) {
-    constexpr int kTileM = 64 * TM;  // two waves of TM instruction tiles along M
-    __shared__ uint4 lds_w[2][4 * kGemmTileN];
-    __shared__ uint4 lds_x[2][4 * kTileM];
-    const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-    const int r = lane & 31, h = lane >> 5;
-    const int wn = wave >> 1, wm = wave & 1;
-    const int64_t nb0 = (int64_t)blockIdx.x * kGemmTileN, mb0 = (int64_t)blockIdx.y * kTileM;
-    const int64_t nkb = g.K / 32, row_bytes = g.K / 2, nst = g.K / kGemmTileK;
-    const uint32_t psel = h ? 0x0c0c0301u : 0x0c0c0200u;
-    uint32_t scw[2], scx[TM];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) scw[i] = stage_scales(g.b_scales, nb0 + wn * 64 + 32 * i + r, g.N, nkb, 0, psel);
-#pragma unroll
-    for (int j = 0; j < TM; ++j) scx[j] = stage_scales(g.a_scales, mb0 + wm * (32 * TM) + 32 * j + r, g.M, nkb, 0, psel);
-    f32x16g acc[2][TM];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < TM; ++j) acc[i][j] = f32x16g{};
-    Stage<TM> sg;
-    load_stage(g, t, nb0, mb0, row_bytes, 0, sg);
-    store_stage(lds_w[0], lds_x[0], t, sg);
-    __syncthreads();
-    for (int64_t st = 0; st < nst; ++st) {
-        const int buf = (int)(st & 1);
-        const bool more = st + 1 < nst;
-        uint32_t nscw[2], nscx[TM];
-        if (more) {
-            load_stage(g, t, nb0, mb0, row_bytes, st + 1, sg);
-#pragma unroll
-            for (int i = 0; i < 2; ++i) nscw[i] = stage_scales(g.b_scales, nb0 + wn * 64 + 32 * i + r, g.N, nkb, st + 1, psel);
-#pragma unroll
-            for (int j = 0; j < TM; ++j) nscx[j] = stage_scales(g.a_scales, mb0 + wm * (32 * TM) + 32 * j + r, g.M, nkb, st + 1, psel);
-        }
-        stage_step<0, TM>(lds_w[buf], lds_x[buf], h, wn, wm, r, scw, scx, acc);
-        stage_step<1, TM>(lds_w[buf], lds_x[buf], h, wn, wm, r, scw, scx, acc);
-        if (more) {
-            store_stage(lds_w[buf ^ 1], lds_x[buf ^ 1], t, sg);
-#pragma unroll
-            for (int i = 0; i < 2; ++i) scw[i] = nscw[i];
-#pragma unroll
-            for (int j = 0; j < TM; ++j) scx[j] = nscx[j];
-        }
-        __syncthreads();
-    }
-    // acc[i][j][4q + e] = C[mb0 + wm 32 TM + 32 j + r][nb0 + wn 64 + 32 i + 8 q + 4 h + e]
-#pragma unroll
-    for (int j = 0; j < TM; ++j) {
-        const int64_t m = mb0 + wm * (32 * TM) + 32 * j + r;
-        if (m >= g.M) continue;
-        float* crow = g.C + m * g.ldc_out;
-        const float* brow = g.bias ? g.bias + m * g.ldc_out : g.accumulate ? crow : nullptr;
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int64_t n = nb0 + wn * 64 + 32 * i + 8 * q + 4 * h;
-                float4 v = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-                if (g.vec_ok && n + 3 < g.N) {
-                    if (brow) {
-                        const float4 o = *reinterpret_cast<const float4*>(brow + n);
-                        v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
-                    }
-                    *reinterpret_cast<float4*>(crow + n) = v;
-                } else {
-                    if (n + 0 < g.N) crow[n + 0] = brow ? brow[n + 0] + v.x : v.x;
-                    if (n + 1 < g.N) crow[n + 1] = brow ? brow[n + 1] + v.y : v.y;
-                    if (n + 2 < g.N) crow[n + 2] = brow ? brow[n + 2] + v.z : v.z;
-                    if (n + 3 < g.N) crow[n + 3] = brow ? brow[n + 3] + v.w : v.w;
-                }
-            }
-    }
-}
+// K advances 128 (four 32-blocks) per pipeline stage in the LDS-pipelined kernels below.
+constexpr int kGemmTileK = 128;
 
 // Pipelined variant (K a multiple of 128, 4-byte-aligned scales): workgroup
 // tile 128 (N) x 128 (M), waves 2 x 2 of 64 x 64, K 128 per stage.  Codes and
@@ -627,21 +475,12 @@ __global__ __launch_bounds__(512) void mxfp4_gemm_big_kernel(const GemmParams g)
 hipError_t launch_mxfp4_gemm(const GemmParams& g, hipStream_t st) {
     // the 256 x 256 tile once there are enough of them to spread over the chip, else 128 x 128
     const int64_t big_tiles = ((g.N + 255) / 256) * ((g.M + 255) / 256);
-    const bool big = g.tile_m == 8 || (g.tile_m == 0 && big_tiles >= kBigTileMin);
-    if (g.K % kGemmTileK == 0 && g.scales_aligned && big) {
+    if (g.K % kGemmTileK == 0 && g.scales_aligned && big_tiles >= kBigTileMin) {
         const dim3 grid((unsigned)((g.N + 255) / 256), (unsigned)((g.M + 255) / 256));
         hipLaunchKernelGGL(mxfp4_gemm_big_kernel, grid, dim3(512), 0, st, g);
-    } else if (g.K % kGemmTileK == 0 && g.scales_aligned && g.tile_m == 0) {
+    } else if (g.K % kGemmTileK == 0 && g.scales_aligned) {
         const dim3 grid((unsigned)((g.N + 127) / 128), (unsigned)((g.M + 127) / 128));
         hipLaunchKernelGGL(mxfp4_gemm_pipe_kernel, grid, dim3(256), 0, st, g);
-    } else if (g.K % kGemmTileK == 0 && g.scales_aligned) {
-        if (g.tile_m == 4) {
-            const dim3 grid((unsigned)((g.N + kGemmTileN - 1) / kGemmTileN), (unsigned)((g.M + 255) / 256));
-            hipLaunchKernelGGL(mxfp4_gemm_tiled_kernel<4>, grid, dim3(256), 0, st, g);
-        } else {
-            const dim3 grid((unsigned)((g.N + kGemmTileN - 1) / kGemmTileN), (unsigned)((g.M + 127) / 128));
-            hipLaunchKernelGGL(mxfp4_gemm_tiled_kernel<2>, grid, dim3(256), 0, st, g);
-        }
     } else {
         const dim3 grid((unsigned)((g.N + 127) / 128), (unsigned)((g.M + 127) / 128));
         hipLaunchKernelGGL(mxfp4_gemm_kernel, grid, dim3(256), 0, st, g);

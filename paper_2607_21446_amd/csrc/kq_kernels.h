@@ -31,18 +31,13 @@ struct Params {
     int64_t units;       // wave units, filled in by the launcher
 };
 
-struct LaunchConfig {
-    int64_t max_blocks = int64_t(1) << 30;  // cap on the workgroup count (grid-stride beyond it)
-    int64_t max_waves = 3072;               // workgroups (one wave each) of the on-the-fly matrix-core kernel
-    int units_per_wave = 1;                 // 64-block units it loads per step (1 or 2)
-    bool packed_one_unit = true;            // packed K: one unit per wave, no loop
-    bool build_unit = true;                 // K from the factors: built per 4-wave workgroup, one unit per wave
-    bool column_tile = true;                // per-block factors: 8-wave workgroups on strips of 8 column blocks
-    int tile_row_blocks = 0;                // 64-row steps per strip (0: chosen from the grid size)
-    int64_t interleave_max_units = 4096;    // packed K: interleave both tiles up to this many units
-    int smooth_path = 3;                    // SmoothQuant layout: 0 chunk, 1 per-lane, 2 column, 3 stationary
-    int64_t smooth_waves = 2048;            // target workgroups of the column-stationary SmoothQuant
-};
+// Launch shapes.
+constexpr int64_t kMaxGridStride = int64_t(1) << 30;  // workgroup cap of the grid-stride kernels
+constexpr int64_t kInterleaveMaxUnits = 4096;         // packed K: interleave both tiles up to this many units
+constexpr int64_t kSmoothWaves = 2048;                // target workgroups of the column-stationary SmoothQuant
+// Largest one-workgroup-per-unit grid (units of 64 blocks, or tiles of the
+// per-block kernel): launches beyond it are refused by the API layer.
+constexpr int64_t kMaxUnitGrid = (int64_t(1) << 31) - 1;
 
 // W4A4 MXFP4 GEMM C[M, N] (+)= deq(A)[M, K] . deq(B)[N, K]^T (kq_gemm.hip).
 struct GemmParams {
@@ -59,10 +54,9 @@ struct GemmParams {
     const float* bias = nullptr;  // if set: C = bias + product (bias [M, ldc_out], vec rule as C)
     int vec_ok;               // C 16-byte aligned and ldc_out a multiple of 4
     int scales_aligned;       // both scale arrays 4-byte aligned
-    int tile_m = 2;           // instruction tiles per wave along M in the tiled kernel (2 or 4)
 };
 
-hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg);
+hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st);
 hipError_t launch_mxfp4_gemm(const GemmParams& g, hipStream_t st);
 hipError_t launch_pack(int a, const float* A, const float* B, int64_t nfac, uint8_t* kpack, hipStream_t st);
 hipError_t launch_e2m1(const float* v, int64_t npairs, uint32_t s, uint8_t* codes, hipStream_t st);

@@ -10,7 +10,9 @@
 //    is evaluated with fp32 FMAs in the fixed order below, so every output
 //    is bit-identical to that order.  Factors are wave-uniform scalar loads.
 //    12 FMAs per element make it bound by VALU issue, not by HBM.
-//  * matrix-core (MFMA, kron_mfma_kernel): the materialised 32x32 block
+//  * matrix-core (MFMA; kron_mfma_unit_kernel with K from the pack,
+//    kron_build_unit_kernel with K built on chip, kron_tile_kernel for
+//    per-block factors): the materialised 32x32 block
 //    K = A (x) B, rounded to fp32 and split into three bf16 terms
 //    (hi + mid + lo), multiplies 32 blocks at a time with
 //    v_mfma_f32_32x32x16_bf16 (the bf16 input is the B operand as loaded),
@@ -112,35 +114,6 @@ struct PlainOp {
     __device__ __forceinline__ void apply(const float (&x)[32], float (&y)[32], int64_t) const {
 #pragma unroll
         for (int k = 0; k < 32; ++k) y[k] = x[k];
-    }
-};
-
-// COLUMN mapping: the wave's column block is uniform, multipliers come in
-// through scalar loads.
-struct SmoothUniformOp {
-    const float* m;
-    __device__ __forceinline__ void setup(const Params& p, int64_t j) { m = p.mult + j * 32; }
-    __device__ __forceinline__ void apply(const float (&x)[32], float (&y)[32], int64_t) const {
-#pragma unroll
-        for (int k = 0; k < 32; ++k) y[k] = x[k] * ld_uniform(m, k);
-    }
-};
-
-// FLAT mapping: every lane has its own column block, multipliers come in
-// through per-lane vector loads (the [d] array stays cache resident).
-struct SmoothLaneOp {
-    const float* m;
-    __device__ __forceinline__ void setup(const Params& p, int64_t) { m = p.mult; }
-    __device__ __forceinline__ void apply(const float (&x)[32], float (&y)[32], int64_t col) const {
-        const float4* mv = reinterpret_cast<const float4*>(m + col * 32);
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const float4 f = mv[k];
-            y[4 * k + 0] = x[4 * k + 0] * f.x;
-            y[4 * k + 1] = x[4 * k + 1] * f.y;
-            y[4 * k + 2] = x[4 * k + 2] * f.z;
-            y[4 * k + 3] = x[4 * k + 3] * f.w;
-        }
     }
 };
 
@@ -441,74 +414,6 @@ __device__ __forceinline__ float max_abs_bf16(const uint4 (&r)[2]) {
     return __uint_as_float(top << 16);
 }
 
-// SmoothQuant with the per-channel multiply applied to each 16-byte input
-// chunk while the chunks are still in the coalesced order (its 8 multipliers
-// are then 32 contiguous bytes, also coalesced across the wave), then parked
-// in LDS as fp32 and read back one block per lane.  LDS slot (16 B) of half
-// e of chunk m of block b: 8b + ((2m + e) ^ (b & 7)).
-__device__ __forceinline__ int lds_slot8(int b, int m8) { return 8 * b + (m8 ^ (b & 7)); }
-
-__global__ __launch_bounds__(64) void smooth_chunk_kernel(const Params p) {
-    __shared__ float4 lds[512];
-    const int lane = threadIdx.x;
-    const uint32_t nchunk_row = (uint32_t)(p.nb * 4);  // multiplier chunks per row (d < 2^29)
-    for (int64_t u = blockIdx.x; u < p.units; u += gridDim.x) {
-        const int64_t first = u * 64;
-        const int nvalid = (int)min<int64_t>(64, p.nblocks - first);
-        const uint4* src = reinterpret_cast<const uint4*>(p.X) + first * 4;
-        const uint32_t cbase = (uint32_t)((first * 4) % nchunk_row);  // wave-uniform
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const int ci = 64 * c + lane;
-            const int b = ci >> 2, m = ci & 3;
-            float x[8];
-            float4 lo4 = make_float4(0.f, 0.f, 0.f, 0.f), hi4 = lo4;
-            if (b < nvalid) {
-                unpack8(load_nt(src + ci), x);
-                // multiplier chunk of this input chunk: (first*4 + ci) mod (4 nb)
-                uint32_t mc = cbase + (uint32_t)ci;
-                if (nchunk_row >= 256u) {
-                    if (mc >= nchunk_row) mc -= nchunk_row;
-                } else {
-                    mc %= nchunk_row;
-                }
-                const float4* mv = reinterpret_cast<const float4*>(p.mult) + 2 * mc;
-                const float4 m0 = mv[0], m1 = mv[1];
-                lo4 = make_float4(x[0] * m0.x, x[1] * m0.y, x[2] * m0.z, x[3] * m0.w);
-                hi4 = make_float4(x[4] * m1.x, x[5] * m1.y, x[6] * m1.z, x[7] * m1.w);
-            }
-            lds[lds_slot8(b, 2 * m)] = lo4;
-            lds[lds_slot8(b, 2 * m + 1)] = hi4;
-        }
-        wave_lds_sync();
-        float y[32];
-#pragma unroll
-        for (int m8 = 0; m8 < 8; ++m8) {
-            const float4 v = lds[lds_slot8(lane, m8)];
-            y[4 * m8] = v.x;
-            y[4 * m8 + 1] = v.y;
-            y[4 * m8 + 2] = v.z;
-            y[4 * m8 + 3] = v.w;
-        }
-        wave_lds_sync();
-        if (lane < nvalid) {
-            const int64_t blk = first + lane;
-            uint32_t w[4];
-            const uint32_t sb = encode32(y, w);
-            if (p.codes) {
-                *reinterpret_cast<uint4*>(p.codes + blk * 16) = make_uint4(w[0], w[1], w[2], w[3]);
-                p.scales[blk] = (uint8_t)sb;
-            }
-            if (p.y) {
-                float4* dst = reinterpret_cast<float4*>(p.y + blk * 32);
-#pragma unroll
-                for (int m = 0; m < 8; ++m)
-                    dst[m] = make_float4(y[4 * m], y[4 * m + 1], y[4 * m + 2], y[4 * m + 3]);
-            }
-        }
-    }
-}
-
 // SmoothQuant, column-stationary: the grid stride G (in 64-block units) is a
 // multiple of nb / gcd(nb, 64), so 64 G is a multiple of nb and lane l of a
 // workgroup keeps the same column block (64 u + l) mod nb in every unit it
@@ -681,214 +586,6 @@ __device__ __forceinline__ float lu_entry(const float (&g)[5][4], int idx) {
         v *= ((k < na) == in_a) ? ge : 1.0f;
     }
     return v;
-}
-
-template <int NA, int NB>
-__device__ __forceinline__ void decode_lu_factors(const float* lu, int lane, float* out) {
-    float g[5][4];
-    lu_g(lu, g);
-    for (int idx = lane; idx < NA * NA + NB * NB; idx += 64) out[idx] = lu_entry<NA, NB>(g, idx);
-}
-
-// Matrix-core KroQuant.  A wave handles U consecutive units per step (all
-// their loads issued before any compute).  FLAT: workgroup g handles steps
-// g, g + G, ...;  COLUMN: workgroup g handles column block j = g % nb for
-// steps g / nb, g / nb + G / nb, ... (G a multiple of nb), so one K per wave.
-template <Mapping MAP, int NA, int NB, int U, bool PACKED, bool LU>
-__global__ __launch_bounds__(64) void kron_mfma_kernel(const Params p) {
-    __shared__ uint4 lds[U][256];
-    __shared__ float lu_fac[LU ? NA * NA + NB * NB : 1];  // decoded A then B (LU form)
-    const int lane = threadIdx.x;
-    const int h = lane >> 5, jl = lane & 31;
-    int64_t jcol = 0, s0 = blockIdx.x, sstep = gridDim.x;
-    if (MAP == Mapping::Column) {
-        jcol = blockIdx.x % p.nb;
-        s0 = blockIdx.x / p.nb;
-        sstep = gridDim.x / p.nb;
-    }
-    const int64_t f = (p.nfac == 1) ? 0 : jcol;
-    const float* Af = LU ? lu_fac : p.A + f * (NA * NA);
-    const float* Bf = LU ? lu_fac + NA * NA : p.B + f * (NB * NB);
-    if (LU) {
-        decode_lu_factors<NA, NB>(p.lu + f * 15, lane, lu_fac);
-        wave_lds_sync();
-    }
-    // K operand: from the pack (materialised offline) or built here from the factors
-    KFactors<NA, NB> kf;
-    KSlices ks;
-    float kbound = 0.0f;
-    if (PACKED) {
-        const uint4* pk = reinterpret_cast<const uint4*>(p.kpack + f * kPackBytes);
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            ks.hi[s] = __builtin_bit_cast(bf16x8, pk[(0 * 2 + s) * 64 + lane]);
-            ks.mid[s] = __builtin_bit_cast(bf16x8, pk[(1 * 2 + s) * 64 + lane]);
-            ks.lo[s] = __builtin_bit_cast(bf16x8, pk[(2 * 2 + s) * 64 + lane]);
-        }
-        kbound = ld_uniform(reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16), 0) * 0x1p-17f;
-    } else {
-        load_k_factors<NA, NB>(Af, Bf, lane, kf);  // first, so their latency overlaps the input loads
-    }
-    const int64_t nunits = (MAP == Mapping::Flat) ? (p.nblocks + 63) / 64 : (p.M + 63) / 64;
-    const int64_t nsteps = (nunits + U - 1) / U;
-    const uint32_t bstride = (MAP == Mapping::Flat) ? 1u : (uint32_t)p.nb;
-    // geometry of unit u: flat index of its block 0 and its number of blocks
-    auto unit_first = [&](int64_t u) -> int64_t {
-        return (MAP == Mapping::Flat) ? u * 64 : u * 64 * p.nb + jcol;
-    };
-    auto unit_valid = [&](int64_t u) -> int {
-        const int64_t left = (MAP == Mapping::Flat) ? p.nblocks - u * 64 : p.M - u * 64;
-        return (int)max<int64_t>(0, min<int64_t>(64, left));
-    };
-    // issue the (nontemporal, coalesced) loads of step st into v
-    uint4 v[U][4];
-    auto issue = [&](int64_t st) {
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-            const int64_t u = st * U + k;
-            const int nv = unit_valid(u);
-            const uint4* src = reinterpret_cast<const uint4*>(p.X) + unit_first(u) * 4;
-            if (nv == 64) {
-#pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const uint32_t ci = 64 * c + lane;
-                    v[k][c] = load_nt(src + ((ci >> 2) * bstride * 4 + (ci & 3)));
-                }
-            } else {
-#pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const uint32_t ci = 64 * c + lane;
-                    v[k][c] = make_uint4(0u, 0u, 0u, 0u);
-                    if ((int)(ci >> 2) < nv) v[k][c] = load_nt(src + ((ci >> 2) * bstride * 4 + (ci & 3)));
-                }
-            }
-        }
-    };
-    if (s0 < nsteps) issue(s0);
-    if (!PACKED) kbound = build_k<NA, NB>(kf, ks) * 0x1p-17f;
-    // no row of A and no row of B with every sign bit set: then an all-(+0)
-    // input block gives +0 for every output in the fixed order
-    bool zero_ok;
-    if (PACKED) {
-        zero_ok = __float_as_uint(ld_uniform(reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16), 2)) != 0u;
-    } else {
-        bool neg_row = false;
-        if (lane < NA) {
-            bool all = true;
-            for (int j = 0; j < NA; ++j) all = all && (__float_as_uint(Af[lane * NA + j]) >> 31);
-            neg_row = all;
-        }
-        if (lane < NB) {
-            bool all = true;
-            for (int j = 0; j < NB; ++j) all = all && (__float_as_uint(Bf[lane * NB + j]) >> 31);
-            neg_row = neg_row || all;
-        }
-        zero_ok = __builtin_amdgcn_ballot_w64(neg_row) == 0;
-    }
-    for (int64_t st = s0; st < nsteps; st += sstep) {
-        int64_t first[U];
-        int nvalid[U];
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-            first[k] = unit_first(st * U + k);
-            nvalid[k] = unit_valid(st * U + k);
-        }
-#pragma unroll
-        for (int k = 0; k < U; ++k)
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const int ci = 64 * c + lane;
-                lds[k][lds_slot(ci >> 2, ci & 3)] = v[k][c];
-            }
-        // the next step's loads are in flight while this step computes
-        if (st + sstep < nsteps) issue(st + sstep);
-        wave_lds_sync();
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-            if (nvalid[k] == 0) continue;
-            // both 32-block tiles of the unit: their MFMA chains interleave
-            uint4 raw[2][2];
-            f32x16 acc[2];
-#pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                raw[t][0] = lds[k][lds_slot(32 * t + jl, h)];
-                raw[t][1] = lds[k][lds_slot(32 * t + jl, 2 + h)];
-                acc[t] = f32x16{};
-            }
-            // smallest terms first; acc[n][block] += K[n][k-step] . x[block][k-step]
-#pragma unroll
-            for (int s = 0; s < 2; ++s)
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.lo[s], __builtin_bit_cast(bf16x8, raw[t][s]), acc[t], 0, 0, 0);
-#pragma unroll
-            for (int s = 0; s < 2; ++s)
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.mid[s], __builtin_bit_cast(bf16x8, raw[t][s]), acc[t], 0, 0, 0);
-#pragma unroll
-            for (int s = 0; s < 2; ++s)
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks.hi[s], __builtin_bit_cast(bf16x8, raw[t][s]), acc[t], 0, 0, 0);
-#pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                if (32 * t >= nvalid[k]) break;
-                const int bt = 32 * t + jl;  // this lane's block within the unit
-                const bool valid = bt < nvalid[k];
-                // lane holds y[16h + i] of block bt in acc[t][i]; all values >= 0 below
-                // compare as their fp32 bit patterns
-                float am = 0.0f;
-#pragma unroll
-                for (int i = 0; i < 16; ++i) am = fmaxf(am, fabsf(acc[t][i]));
-                uint32_t amb = __float_as_uint(am);
-                amb = max(amb, other_half(amb));
-                am = __uint_as_float(amb);
-                uint32_t mxb = __float_as_uint(max_abs_bf16(raw[t]));
-                mxb = max(mxb, other_half(mxb));
-                const float bnd = kbound * __uint_as_float(mxb);
-                const uint32_t e = amb >> 23;
-                const float lo_p2 = __uint_as_float(e << 23), hi_p2 = __uint_as_float((e + 1u) << 23);
-                bool near = valid && (e <= 3u || am - lo_p2 <= bnd || hi_p2 - am <= bnd);
-                if (amb == 0u && zero_ok && mxb == 0u) {
-                    // all outputs +-0: exact when the inputs are all +0 (bit patterns 0)
-                    const uint32_t any = raw[t][0].x | raw[t][0].y | raw[t][0].z | raw[t][0].w | raw[t][1].x |
-                                         raw[t][1].y | raw[t][1].z | raw[t][1].w;
-                    if ((any | other_half(any)) == 0u) near = false;
-                }
-                const uint64_t ob = (uint64_t)first[k] + (uint64_t)((uint32_t)bt * bstride);  // output block
-                const uint32_t sb = max(e, 2u) - 2u;
-                const float sc = __uint_as_float(sb << 23);
-                const uint2 out = make_uint2(codes8(acc[t], 0, sc, amb), codes8(acc[t], 8, sc, amb));
-                if (valid && !near) {
-                    if (p.codes) {
-                        *reinterpret_cast<uint2*>(p.codes + ob * 16 + 8 * h) = out;
-                        if (h == 0) p.scales[ob] = (uint8_t)sb;
-                    }
-                    if (p.y) {
-                        float* yb = p.y + ob * 32 + 16 * h;
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-                            *reinterpret_cast<float4*>(yb + 4 * q) =
-                                make_float4(acc[t][4 * q], acc[t][4 * q + 1], acc[t][4 * q + 2], acc[t][4 * q + 3]);
-                    }
-                    if (LU && p.y16) {
-                        uint4* yb = reinterpret_cast<uint4*>(p.y16 + ob * 32 + 16 * h);
-#pragma unroll
-                        for (int q = 0; q < 2; ++q)
-                            yb[q] = make_uint4(bf16_pair(acc[t][8 * q], acc[t][8 * q + 1]),
-                                               bf16_pair(acc[t][8 * q + 2], acc[t][8 * q + 3]),
-                                               bf16_pair(acc[t][8 * q + 4], acc[t][8 * q + 5]),
-                                               bf16_pair(acc[t][8 * q + 6], acc[t][8 * q + 7]));
-                    }
-                }
-                // blocks whose amax is on a binade edge: the fixed evaluation order decides
-                exact_flagged<NA, NB>((__builtin_amdgcn_ballot_w64(near) & 0xFFFFFFFFull) << (32 * t), lds[k],
-                                      first[k], bstride, Af, Bf, p);
-            }
-        }
-        wave_lds_sync();  // the next step's writes come after this step's reads
-    }
 }
 
 // Workgroups go to the 8 XCDs round robin (workgroup i to XCD i % 8).  This
@@ -1777,40 +1474,21 @@ __global__ __launch_bounds__(LOG2D == 14 ? 512 : 256) void fwht_kernel(const Par
 
 // ------------------------------------------------------------------ launchers
 template <Mapping MAP, class Op>
-static hipError_t launch_map(Params p, hipStream_t st, const LaunchConfig& cfg) {
+static hipError_t launch_map(Params p, hipStream_t st) {
     if (MAP == Mapping::Flat)
         p.units = (p.nblocks + 63) / 64;
     else
         p.units = ((p.M + 63) / 64) * p.nb;
-    int64_t g = p.units < cfg.max_blocks ? p.units : cfg.max_blocks;
+    int64_t g = p.units < kMaxGridStride ? p.units : kMaxGridStride;
     if (g < 1) g = 1;
     hipLaunchKernelGGL((quant_kernel<MAP, Op>), dim3((unsigned)g), dim3(64), 0, st, p);
     return hipGetLastError();
 }
 
 template <class Op>
-static hipError_t launch_op(const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
-    if (map == Mapping::Flat) return launch_map<Mapping::Flat, Op>(p, st, cfg);
-    return launch_map<Mapping::Column, Op>(p, st, cfg);
-}
-
-template <int NA, int NB, int U, bool PACKED, bool LU = false>
-static hipError_t launch_mfma_u(Params p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
-    int64_t g;
-    if (map == Mapping::Flat) {
-        const int64_t steps = ((p.nblocks + 63) / 64 + U - 1) / U;
-        g = steps < cfg.max_waves ? steps : cfg.max_waves;
-        if (g < 1) g = 1;
-        hipLaunchKernelGGL((kron_mfma_kernel<Mapping::Flat, NA, NB, U, PACKED, LU>), dim3((unsigned)g), dim3(64), 0, st, p);
-    } else {
-        const int64_t steps = ((p.M + 63) / 64 + U - 1) / U;  // per column block
-        int64_t per_col = (cfg.max_waves + p.nb - 1) / p.nb;   // workgroups per column block
-        if (per_col > steps) per_col = steps;
-        if (per_col < 1) per_col = 1;
-        g = per_col * p.nb;
-        hipLaunchKernelGGL((kron_mfma_kernel<Mapping::Column, NA, NB, U, PACKED, LU>), dim3((unsigned)g), dim3(64), 0, st, p);
-    }
-    return hipGetLastError();
+static hipError_t launch_op(const Params& p, Mapping map, hipStream_t st) {
+    if (map == Mapping::Flat) return launch_map<Mapping::Flat, Op>(p, st);
+    return launch_map<Mapping::Column, Op>(p, st);
 }
 
 template <Mapping MAP, int NA, int NB>
@@ -1839,14 +1517,14 @@ static hipError_t launch_tile(const Params& p, int rg, hipStream_t st) {
     return hipGetLastError();
 }
 
-// Row blocks per strip of the tile kernel (1 .. kTileMaxSteps): the
-// configured count, else as many as keep at least ~1728 workgroups when each
-// wave builds its K (about three rounds of the 512 that fit at once: more
-// steps amortise the build) and ~3456 when K comes from the pack (only its
-// load to amortise, so a shorter last round matters more).
-static int tile_rows(const Params& p, const LaunchConfig& cfg) {
+// Row blocks per strip of the tile kernel (1 .. kTileMaxSteps): as many as
+// keep at least ~1728 workgroups when each wave builds its K (about three
+// rounds of the 512 that fit at once: more steps amortise the build) and
+// ~3456 when K comes from the pack (only its load to amortise, so a shorter
+// last round matters more).
+static int tile_rows(const Params& p) {
     const int64_t tiles = ((p.M + 63) / 64) * ((p.nb + kTileCols - 1) / kTileCols);
-    const int64_t rg = cfg.tile_row_blocks > 0 ? cfg.tile_row_blocks : tiles / (p.kpack ? 3456 : 1728);
+    const int64_t rg = tiles / (p.kpack ? 3456 : 1728);
     return rg < 1 ? 1 : rg > kTileMaxSteps ? kTileMaxSteps : (int)rg;
 }
 
@@ -1868,41 +1546,26 @@ static hipError_t launch_build(const Params& p, Mapping map, hipStream_t st) {
     return hipGetLastError();
 }
 
-// grids of more workgroups than this take the grid-stride kernels
-constexpr int64_t kMaxUnitGrid = (int64_t(1) << 31) - 1;
-
+// Per-block factors (COLUMN mapping) run on the 8-column tile kernel; shared
+// factors on one 64-block unit per wave, K from the pack (the two tiles'
+// products interleaved on grids of at most kInterleaveMaxUnits units, where
+// fewer waves per SIMD hide less latency) or built per 4-wave workgroup.
+// The caller has checked that every grid fits (kq_max_units).
 template <int NA, int NB>
-static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
-    const int64_t units = (map == Mapping::Flat) ? (p.nblocks + 63) / 64 : ((p.M + 63) / 64) * p.nb;
-    const int64_t tiles = ((p.M + 63) / 64) * ((p.nb + kTileCols - 1) / kTileCols);
-    if (map == Mapping::Column && cfg.column_tile && tiles <= kMaxUnitGrid && p.d < (int64_t(1) << 25)) {
-        if (p.kpack) return launch_tile<NA, NB, true, false>(p, tile_rows(p, cfg), st);
-        return launch_tile<NA, NB, false, false>(p, tile_rows(p, cfg), st);
+static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st) {
+    if (map == Mapping::Column) {
+        if (p.kpack) return launch_tile<NA, NB, true, false>(p, tile_rows(p), st);
+        return launch_tile<NA, NB, false, false>(p, tile_rows(p), st);
     }
-    if (p.kpack) {
-        if (cfg.packed_one_unit && units <= kMaxUnitGrid) {
-            // small grids (few waves per SIMD) hide less latency: interleave the two tiles
-            const bool ilv = units <= cfg.interleave_max_units;
-            if (map == Mapping::Flat) return launch_unit<Mapping::Flat, NA, NB>(p, units, ilv, st);
-            return launch_unit<Mapping::Column, NA, NB>(p, units, ilv, st);
-        }
-        if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, true>(p, map, st, cfg);
-        return launch_mfma_u<NA, NB, 1, true>(p, map, st, cfg);
-    }
-    if (cfg.build_unit && units <= kMaxUnitGrid) return launch_build<NA, NB, false>(p, map, st);
-    if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, false>(p, map, st, cfg);
-    return launch_mfma_u<NA, NB, 1, false>(p, map, st, cfg);
+    const int64_t units = (p.nblocks + 63) / 64;
+    if (p.kpack) return launch_unit<Mapping::Flat, NA, NB>(p, units, units <= kInterleaveMaxUnits, st);
+    return launch_build<NA, NB, false>(p, map, st);
 }
 
 template <int NA, int NB>
-static hipError_t launch_lu(const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
-    const int64_t units = (map == Mapping::Flat) ? (p.nblocks + 63) / 64 : ((p.M + 63) / 64) * p.nb;
-    const int64_t tiles = ((p.M + 63) / 64) * ((p.nb + kTileCols - 1) / kTileCols);
-    if (map == Mapping::Column && cfg.column_tile && tiles <= kMaxUnitGrid && p.d < (int64_t(1) << 25))
-        return launch_tile<NA, NB, false, true>(p, tile_rows(p, cfg), st);
-    if (cfg.build_unit && units <= kMaxUnitGrid) return launch_build<NA, NB, true>(p, map, st);
-    if (cfg.units_per_wave == 2) return launch_mfma_u<NA, NB, 2, false, true>(p, map, st, cfg);
-    return launch_mfma_u<NA, NB, 1, false, true>(p, map, st, cfg);
+static hipError_t launch_lu(const Params& p, Mapping map, hipStream_t st) {
+    if (map == Mapping::Column) return launch_tile<NA, NB, false, true>(p, tile_rows(p), st);
+    return launch_build<NA, NB, true>(p, map, st);
 }
 
 hipError_t launch_pack(int a, const float* A, const float* B, int64_t nfac, uint8_t* kpack, hipStream_t st) {
@@ -1917,53 +1580,44 @@ hipError_t launch_pack(int a, const float* A, const float* B, int64_t nfac, uint
     return hipGetLastError();
 }
 
-hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st, const LaunchConfig& cfg) {
+hipError_t launch(Kind kind, int a, const Params& p, Mapping map, hipStream_t st) {
     switch (kind) {
-        case Kind::Plain: return launch_op<PlainOp>(p, map, st, cfg);
-        case Kind::Smooth:
-            if (cfg.smooth_path == 1) return launch_map<Mapping::Flat, SmoothLaneOp>(p, st, cfg);
-            if (cfg.smooth_path == 2) return launch_map<Mapping::Column, SmoothUniformOp>(p, st, cfg);
-            if (cfg.smooth_path == 3) {
-                Params q = p;
-                q.units = (p.nblocks + 63) / 64;
-                int64_t a = p.nb, b = 64;  // gcd(nb, 64)
-                while (b) { const int64_t t = a % b; a = b; b = t; }
-                const int64_t period = p.nb / a;  // stride multiple that keeps columns fixed
-                int64_t g = (cfg.smooth_waves + period - 1) / period * period;
-                if (g > q.units) g = q.units;  // one unit per workgroup: no stride needed
-                hipLaunchKernelGGL(smooth_stationary_kernel, dim3((unsigned)g), dim3(64), 0, st, q);
-                return hipGetLastError();
-            }
-            {
-                Params q = p;
-                q.units = (p.nblocks + 63) / 64;
-                const int64_t g = q.units < cfg.max_blocks ? q.units : cfg.max_blocks;
-                hipLaunchKernelGGL(smooth_chunk_kernel, dim3((unsigned)g), dim3(64), 0, st, q);
-                return hipGetLastError();
-            }
-        case Kind::Hadamard: return launch_op<HadamardOp>(p, map, st, cfg);
+        case Kind::Plain: return launch_op<PlainOp>(p, map, st);
+        case Kind::Smooth: {
+            // column-stationary: a grid stride that is a multiple of nb / gcd(nb, 64)
+            Params q = p;
+            q.units = (p.nblocks + 63) / 64;
+            int64_t a = p.nb, b = 64;  // gcd(nb, 64)
+            while (b) { const int64_t t = a % b; a = b; b = t; }
+            const int64_t period = p.nb / a;  // stride multiple that keeps columns fixed
+            int64_t g = (kSmoothWaves + period - 1) / period * period;
+            if (g > q.units) g = q.units;  // one unit per workgroup: no stride needed
+            hipLaunchKernelGGL(smooth_stationary_kernel, dim3((unsigned)g), dim3(64), 0, st, q);
+            return hipGetLastError();
+        }
+        case Kind::Hadamard: return launch_op<HadamardOp>(p, map, st);
         case Kind::KronMfma:
             switch (a) {
-                case 4: return launch_mfma<4, 8>(p, map, st, cfg);
-                case 2: return launch_mfma<2, 16>(p, map, st, cfg);
-                case 8: return launch_mfma<8, 4>(p, map, st, cfg);
-                case 1: return launch_mfma<1, 32>(p, map, st, cfg);
+                case 4: return launch_mfma<4, 8>(p, map, st);
+                case 2: return launch_mfma<2, 16>(p, map, st);
+                case 8: return launch_mfma<8, 4>(p, map, st);
+                case 1: return launch_mfma<1, 32>(p, map, st);
                 default: return hipErrorInvalidValue;
             }
         case Kind::KronLU:
             switch (a) {
-                case 4: return launch_lu<4, 8>(p, map, st, cfg);
-                case 2: return launch_lu<2, 16>(p, map, st, cfg);
-                case 8: return launch_lu<8, 4>(p, map, st, cfg);
-                case 1: return launch_lu<1, 32>(p, map, st, cfg);
+                case 4: return launch_lu<4, 8>(p, map, st);
+                case 2: return launch_lu<2, 16>(p, map, st);
+                case 8: return launch_lu<8, 4>(p, map, st);
+                case 1: return launch_lu<1, 32>(p, map, st);
                 default: return hipErrorInvalidValue;
             }
         case Kind::Kron:
             switch (a) {
-                case 4: return launch_op<KronOp<4, 8>>(p, map, st, cfg);
-                case 2: return launch_op<KronOp<2, 16>>(p, map, st, cfg);
-                case 8: return launch_op<KronOp<8, 4>>(p, map, st, cfg);
-                case 1: return launch_op<KronOp<1, 32>>(p, map, st, cfg);
+                case 4: return launch_op<KronOp<4, 8>>(p, map, st);
+                case 2: return launch_op<KronOp<2, 16>>(p, map, st);
+                case 8: return launch_op<KronOp<8, 4>>(p, map, st);
+                case 1: return launch_op<KronOp<1, 32>>(p, map, st);
                 default: return hipErrorInvalidValue;
             }
     }

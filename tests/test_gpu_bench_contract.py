@@ -41,5 +41,6 @@ def test_bench_json_line():
     assert abs(rf["frac"] - rf["achieved"] / rf["peak"]) < 1e-3
     assert rf["traffic"] is None or rf["traffic"] > nbytes * 0.99
     assert d["parity"]["hot_path"].startswith("ok"), d["parity"]
+    assert d["parity"]["onthefly"].startswith("ok"), d["parity"]
     assert d["parity"]["exact_path"] == "bit-exact"
 

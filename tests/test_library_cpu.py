@@ -58,6 +58,8 @@ def _q(**kw):
     (dict(scales=None), NULLP), (dict(X=FAKE + 8), MISALIGNED), (dict(codes=FAKE + 4), MISALIGNED),
     (dict(y=FAKE + 4), MISALIGNED), (dict(A=FAKE + 2), MISALIGNED),
     (dict(M=1 << 40, d=1 << 30), INVALID), (dict(d=1 << 25, nfac=1 << 20), UNSUPPORTED),
+    # more workgroups than one launch holds: 2^32 units of 64 blocks, 2^31 tiles of 64 rows x 8 blocks
+    (dict(M=1 << 37, d=64), UNSUPPORTED), (dict(M=1 << 36, d=512, nfac=16), UNSUPPORTED),
 ])
 def test_quantize_rejects(kw, status):
     assert _q(**kw) == status
@@ -95,6 +97,7 @@ def test_quantize_lu_rejects():
     assert q(a=3) == UNSUPPORTED and q(a=16) == UNSUPPORTED and q(a=0) == UNSUPPORTED
     assert q(nfac=3) == UNSUPPORTED
     assert q(d=1 << 25, nfac=1 << 20) == UNSUPPORTED
+    assert q(M=1 << 37, d=64) == UNSUPPORTED and q(M=1 << 36, d=512, nfac=16) == UNSUPPORTED
     assert q(lu=None) == NULLP
     assert q(lu=FAKE + 2) == MISALIGNED
     assert q(y16=FAKE + 8) == MISALIGNED
@@ -245,3 +248,41 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "exactly one GPU" in r.stderr
+
+
+# ---------------------------------------------------------------- binding argument checks
+def test_binding_rejects_wrong_buffer_sizes():
+    """The binding checks every caller-supplied buffer against the sizes the
+    call will touch before anything reaches the library (an undersized buffer
+    would otherwise be written out of bounds)."""
+    from paper_2607_21446_amd import binding as bd
+    X = torch.zeros((4, 64), dtype=torch.bfloat16)
+    c, s, y = bd._outputs(X, None, None, None, True)
+    assert c.shape == (4, 32) and s.shape == (4, 2) and y.shape == (4, 64)
+    with pytest.raises(ValueError):
+        bd._outputs(X, torch.empty(4 * 32 - 1, dtype=torch.uint8), None, None, False)
+    with pytest.raises(ValueError):
+        bd._outputs(X, None, torch.empty(7, dtype=torch.uint8), None, False)
+    with pytest.raises(ValueError):
+        bd._outputs(X, None, None, torch.empty((4, 63), dtype=torch.float32), False)
+    with pytest.raises(ValueError):
+        bd._outputs(torch.zeros(64, dtype=torch.bfloat16), None, None, None, False)
+    A, B = torch.zeros((3, 4, 4)), torch.zeros((3, 8, 8))
+    assert bd._pairs(A, B) == (4, 8, 3)
+    with pytest.raises(ValueError):
+        bd._pairs(A, torch.zeros((2, 8, 8)))          # pair counts differ
+    with pytest.raises(ValueError):
+        bd._pairs(torch.zeros((3, 4, 2)), B)          # A not square
+    with pytest.raises(ValueError):
+        bd._pairs(A, B, torch.device("cuda", 0))      # factors not on the input's device
+    with pytest.raises(ValueError):
+        bd._size(torch.zeros(10), 11, "kpack")
+
+
+def test_binding_rejects_before_the_library_is_called():
+    """Public calls with an inconsistent buffer raise ValueError/TypeError
+    (on this host the tensors are not device tensors, which is rejected too)."""
+    with pytest.raises((TypeError, ValueError)):
+        kq.quantize(torch.zeros((4, 64), dtype=torch.bfloat16), torch.zeros((1, 4, 4)), torch.zeros((1, 8, 8)))
+    with pytest.raises(ValueError):
+        kq.lu_to_factors(torch.zeros(14), 4)

@@ -7,6 +7,8 @@ threshold rule checked over every fp32 value in [0, 8], the bit-level scale
 rule, and invariants (sign symmetry, power-of-two equivariance, eq. (1)
 invariance, thread-count independence).  CPU only.
 """
+import functools
+
 import numpy as np
 import pytest
 
@@ -454,3 +456,56 @@ def test_rejects_bad_arguments():
         oracle.quantize(np.zeros((2, 48), np.uint16), A, B)      # d % 32 != 0
     c, s, _ = oracle.quantize(np.zeros((0, 64), np.uint16), A, B)
     assert c.shape == (0, 32) and s.shape == (0, 2)
+
+
+# ---------------------------------------------------------------- the tolerance rule itself
+def _tie_row():
+    # one block, amax 6 (s = 127, v = |y|): element 1 sits exactly on the 1.25 tie,
+    # element 2 at 1.1 (no tie near), element 3 at -0.2 (rounds to -0)
+    vals = np.zeros(32, np.float32)
+    vals[:4] = [6.0, 1.25, 1.1, -0.2]
+    eye_a, eye_b = np.eye(4, dtype=np.float32)[None], np.eye(8, dtype=np.float32)[None]
+    c, s, y = oracle.quantize_f32(vals[None], eye_a, eye_b, want_y=True)
+    assert int(s[0, 0]) == 127 and c[0, 0] == 0x27 and c[0, 1] == 0x82   # 6 -> 7, 1.25 -> 1.0 (2); 1.1 -> 2, -0.2 -> 8
+    return c, s, y
+
+
+def test_mx_compare_accepts_tie_flips_and_rejects_the_rest():
+    """Planted mistakes in the oracle's own output: an adjacent flip at an exact
+    tie passes; the same flip off a tie, a two-step flip, a sign flip of a
+    nonzero code, a scale change and a y error beyond 1e-5 all fail."""
+    c, s, y = _tie_row()
+    cmp = functools.partial(oracle.mx_compare, max_flip_frac=0.5)   # one block: 1 flip = 1/32 of its codes
+    assert cmp(c, s, c, s, y, y)["ok"]
+    at_tie = c.copy()
+    at_tie[0, 0] = 0x37                          # element 1: 1.0 -> 1.5 at the 1.25 tie
+    assert cmp(at_tie, s, c, s, y)["ok"]
+    off_tie = c.copy()
+    off_tie[0, 1] = 0x83                         # element 2: 1.0 -> 1.5 at v = 1.1
+    rep = cmp(off_tie, s, c, s, y)
+    assert not rep["ok"] and rep["off_tie"] == 1 and rep["non_adjacent"] == 0
+    assert cmp(off_tie, s, c, s)["ok"]        # without y only adjacency is checked
+    two_step = c.copy()
+    two_step[0, 0] = 0x47
+    assert cmp(two_step, s, c, s, y)["non_adjacent"] == 1
+    sign = c.copy()
+    sign[0, 0] = 0xA7                            # element 1: +1.0 -> -1.0
+    assert cmp(sign, s, c, s)["non_adjacent"] == 1
+    zero_sign = c.copy()
+    zero_sign[0, 1] = 0x02                       # element 3: -0 -> +0 (v = 0.2, not at the 0 decision)
+    rep = cmp(zero_sign, s, c, s, y)
+    assert rep["non_adjacent"] == 0 and rep["off_tie"] == 1
+    s2 = s.copy()
+    s2[0, 0] += 1
+    assert not cmp(c, s2, c, s, y)["ok"]
+    y2 = y.copy()
+    y2[0, 2] *= np.float32(1 + 2e-5)
+    assert not cmp(c, s, c, s, y, y2)["ok"]
+    y2[0, 2] = y[0, 2] * np.float32(1 + 4e-6)
+    assert cmp(c, s, c, s, y, y2)["ok"]
+    assert not oracle.mx_compare(at_tie, s, c, s, y)["ok"]  # 1 of 32 codes is above the 1e-4 budget
+
+
+def test_fwht_rejects_rows_longer_than_its_buffer():
+    with pytest.raises(ValueError):
+        oracle.fwht(np.zeros((2, 1 << 17), np.uint16))
