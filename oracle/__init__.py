@@ -377,7 +377,8 @@ def lu_to_factors(abc, a_dim):
 E2M1_DECISION_POINTS = np.array([0.0, 0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0], dtype=np.float64)
 
 
-def mx_compare(codes, scales, codes_ref, scales_ref, y_ref=None, y=None, rel_tol=1e-5, max_flip_frac=1e-4):
+def mx_compare(codes, scales, codes_ref, scales_ref, y_ref=None, y=None, rel_tol=1e-5, max_flip_frac=1e-4,
+               y_exact=None):
     """Compare an MXFP4 result with the oracle's under the tolerance of a path
     whose fp32 accumulation order differs from the oracle's:
 
@@ -389,7 +390,15 @@ def mx_compare(codes, scales, codes_ref, scales_ref, y_ref=None, y=None, rel_tol
       2^(s - 127) and t the nearest decision point (an fp32 result within
       rel_tol of max(|y_ref|, amax_block / 32) moves v by at most that much,
       since v < 8);
-    * with ``y`` as well: max |y - y_ref| / max(|y_ref|, amax_block / 32) <= rel_tol.
+    * with ``y`` as well: max |y - y_t| / max(|y_t|, amax_block(y_t) / 32) <=
+      rel_tol, y_t = ``y_exact`` (the exact transform of the input, e.g.
+      ``transform_f64``) when given, else ``y_ref``.  The fixed-order fp32
+      values are themselves one rounding of the exact ones (up to 33 u
+      sum_k |K_nk| |x_k| away, u = 2^-24), so two fp32 evaluation orders can
+      differ by the sum of their errors; the exact value is the reference the
+      relative error is meant against.  Below the smallest normal fp32 the
+      denominator is 2^-126: subnormal fp32 values are spaced 2^-149 apart,
+      so no fp32 result holds a relative error of 1e-5 there.
 
     Works on the packed bytes and unpacks only the differing ones, so it is
     cheap at full size.  Returns a dict with the counts and ``ok``."""
@@ -424,15 +433,15 @@ def mx_compare(codes, scales, codes_ref, scales_ref, y_ref=None, y=None, rel_tol
     elif y_ref is not None:
         rep["off_tie"] = 0
     rep["y_max_err"] = None
-    if y is not None and y_ref is not None:
+    y_t = y_exact if y_exact is not None else y_ref
+    if y is not None and y_t is not None:
         worst = 0.0
         step = max(1, (1 << 22) // max(nbytes_row * 2, 1))
         for r0 in range(0, M, step):
-            yr = np.asarray(y_ref[r0:r0 + step], np.float64)
+            yr = np.asarray(y_t[r0:r0 + step], np.float64)
             yg = np.asarray(y[r0:r0 + step], np.float64)
             amax = np.abs(yr).reshape(yr.shape[0], -1, 32).max(-1)
-            den = np.maximum(np.abs(yr), np.repeat(amax, 32, axis=1) / 32.0)
-            den = np.where(den > 0, den, 1.0)
+            den = np.maximum(np.maximum(np.abs(yr), np.repeat(amax, 32, axis=1) / 32.0), 2.0 ** -126)
             if yr.size:
                 worst = max(worst, float(np.max(np.abs(yg - yr) / den)))
         rep["y_max_err"] = worst

@@ -54,15 +54,16 @@ def assert_exact(got, want, what=""):
         assert np.array_equal(yg.view(np.uint32), yr.view(np.uint32)), f"{what}: y differs"
 
 
-def assert_mx_close(got, want, what=""):
+def assert_mx_close(got, want, what="", y_exact=None):
     """The tolerance of a path whose fp32 order differs from the oracle's
     (oracle.mx_compare): scales identical; codes identical except adjacent
     flips (or a sign-only flip of magnitude 0) at most 1e-4 of them, each at a
     rounding decision of the oracle's y when the oracle's y is given; the
-    path's y within 1e-5 when both are given."""
+    path's y within 1e-5 of y_exact (the exact transform, oracle.transform_f64)
+    when given, else of the oracle's fixed-order fp32 y."""
     cg, sg, yg = got
     cr, sr, yr = want
-    rep = oracle.mx_compare(cg, sg, cr, sr, y_ref=yr, y=yg)
+    rep = oracle.mx_compare(cg, sg, cr, sr, y_ref=yr, y=yg, y_exact=y_exact)
     assert rep["ok"], f"{what}: {rep}"
 
 
@@ -119,9 +120,10 @@ def test_kroquant_parity(ab, per_block, M, d):
     A, B = synth.factors(a, b, d // 32 if per_block else 1, seed=d + a)
     want = oracle.quantize(X, A, B, want_y=True)
     assert_exact(gpu_quantize(X, A, B, exact=True), want, f"exact {ab} pb={per_block} {M}x{d}")
+    ye = oracle.transform_f64(X, A, B)
     hot = gpu_quantize(X, A, B, exact=False)
-    assert_mx_close(hot, want, f"mfma {ab} pb={per_block} {M}x{d}")
-    assert_mx_close(gpu_quantize_packed(X, A, B), want, f"packed {ab} pb={per_block} {M}x{d}")
+    assert_mx_close(hot, want, f"mfma {ab} pb={per_block} {M}x{d}", ye)
+    assert_mx_close(gpu_quantize_packed(X, A, B), want, f"packed {ab} pb={per_block} {M}x{d}", ye)
 
 
 @pytest.mark.parametrize("M,d", [(1, 32), (3, 64), (257, 1152), (64, 2240), (130, 5600)])
@@ -155,7 +157,7 @@ def test_tiny_config_all_paths():
     w = synth.workload("tiny_256x1152")
     want = oracle.quantize(w.X, w.A, w.B, want_y=True)
     assert_exact(gpu_quantize(w.X, w.A, w.B), want, "tiny exact")
-    assert_mx_close(gpu_quantize(w.X, w.A, w.B, exact=False), want, "tiny mfma")
+    assert_mx_close(gpu_quantize(w.X, w.A, w.B, exact=False), want, "tiny mfma", oracle.transform_f64(w.X, w.A, w.B))
 
 
 # ------------------------------------------------------------------ edge blocks
@@ -204,7 +206,7 @@ def test_edge_blocks_kron(ab):
     A, B = synth.factors(a, b, 2, seed=3)
     want = oracle.quantize(X, A, B, want_y=True)
     assert_exact(gpu_quantize(X, A, B), want, f"kron edges {ab}")
-    assert_mx_close(gpu_quantize(X, A, B, exact=False), want, f"mfma edges {ab}")
+    assert_mx_close(gpu_quantize(X, A, B, exact=False), want, f"mfma edges {ab}", oracle.transform_f64(X, A, B))
     # identity factors: plain MXFP4 (the -0.0 row excepted, products give +0.0);
     # on the matrix-core path every block max here is a power of two or on a
     # binade edge, so this also drives the exact re-evaluation of tiles
@@ -234,12 +236,13 @@ def test_zero_blocks_signed_zeros(ab):
     for nfac_mode in ("shared", "per_block"):
         Af, Bf = (A[3:4], B[3:4]) if nfac_mode == "shared" else (A, B)
         want = oracle.quantize(X, Af, Bf, want_y=True)
+        ye = oracle.transform_f64(X, Af, Bf)
         for got in (gpu_quantize(X, Af, Bf, exact=False), gpu_quantize_packed(X, Af, Bf)):
             assert np.array_equal(got[1], want[1]), f"{ab} {nfac_mode}: scales"
             zero_rows = np.zeros(M, bool)
             zero_rows[::3] = True
             assert np.array_equal(got[0][zero_rows], want[0][zero_rows]), f"{ab} {nfac_mode}: zero-row codes"
-            assert_mx_close(got, want, f"{ab} {nfac_mode}")
+            assert_mx_close(got, want, f"{ab} {nfac_mode}", ye)
 
 
 @pytest.mark.parametrize("ab", [(4, 8), (2, 16)])
@@ -266,8 +269,9 @@ def test_binade_edge_stress(ab):
     rows = int(np.ceil(blocks.shape[0] / nb))
     X = np.concatenate([blocks, blocks[: rows * nb - blocks.shape[0]]]).reshape(rows, nb * 32)
     want = oracle.quantize(X, A, B, want_y=True)
+    ye = oracle.transform_f64(X, A, B)
     for name, got in (("onthefly", gpu_quantize(X, A, B, exact=False)), ("packed", gpu_quantize_packed(X, A, B))):
-        assert_mx_close(got, want, f"{ab} {name} near-edge blocks ({pick.size} picked, T={T})")
+        assert_mx_close(got, want, f"{ab} {name} near-edge blocks ({pick.size} picked, T={T})", ye)
 
 
 def gpu_quantize_lu(X, lu, a):
@@ -287,7 +291,8 @@ def test_kroquant_lu_parity(a, per_block, M, d):
     lu = synth.lu_params(d // 32 if per_block else 1, seed=62 + a)
     cr, sr, yr, y16r = oracle.quantize_lu(X, lu, a, want_y=True)
     c, s, y, y16 = gpu_quantize_lu(X, lu, a)
-    assert_mx_close((c, s, y), (cr, sr, yr), f"lu a={a} per_block={per_block}")
+    assert_mx_close((c, s, y), (cr, sr, yr), f"lu a={a} per_block={per_block}",
+                    oracle.transform_f64(X, *oracle.lu_factors_f32(lu, a)))
     assert np.array_equal(y16, oracle.f32_to_bf16(y)), "y16 is not bf16(y)"
     assert (y16 != y16r).mean() <= 1e-3
 
@@ -386,7 +391,8 @@ def test_guard_bands_and_full_coverage():
         assert np.all(cb[:G] == canary) and np.all(cb[-G:] == canary)
         assert np.all(sb[:G] == canary) and np.all(sb[-G:] == canary)
         assert np.all(np.isnan(yb[:G])) and np.all(np.isnan(yb[-G:]))
-        assert_mx_close((cb[G:-G].reshape(M, -1), sb[G:-G].reshape(M, -1), yb[G:-G].reshape(M, d)), want)
+        assert_mx_close((cb[G:-G].reshape(M, -1), sb[G:-G].reshape(M, -1), yb[G:-G].reshape(M, d)), want,
+                        "guard bands", oracle.transform_f64(X, A, B))
 
 
 def test_flat_and_column_mappings_agree():
@@ -416,7 +422,8 @@ def test_non_default_stream():
     s.synchronize()
     want = oracle.quantize(X, A, B, want_y=True)
     assert_exact((c.cpu().numpy(), sc.cpu().numpy(), y.cpu().numpy()), want)
-    assert_mx_close((c2.cpu().numpy(), sc2.cpu().numpy(), y2.cpu().numpy()), want)
+    assert_mx_close((c2.cpu().numpy(), sc2.cpu().numpy(), y2.cpu().numpy()), want, "stream",
+                    oracle.transform_f64(X, A, B))
 
 
 def test_binding_rejects_inconsistent_buffers():
@@ -432,8 +439,8 @@ def test_binding_rejects_inconsistent_buffers():
         kq.quantize(X, Ad, Bd, scales=u8(8))
     with pytest.raises(ValueError):
         kq.quantize(X, Ad, dev_f32(np.repeat(B, 2, 0)))
-    with pytest.raises(ValueError):
-        kq.quantize(X, Ad.cpu(), Bd.cpu())
+    with pytest.raises(TypeError):
+        kq.quantize(X, Ad.cpu(), Bd.cpu())          # host factors
     kp = kq.pack_factors(Ad, Bd)
     with pytest.raises(ValueError):
         kq.quantize_packed(X, Ad, Bd, kp[:-16])
@@ -540,6 +547,7 @@ def test_full_size_workloads(name):
     Xd = dev_bf16(w.X)
     Ad, Bd = dev_f32(w.A), dev_f32(w.B)
     cr, sr, yr = oracle.quantize(w.X, w.A, w.B, want_y=True)
+    ye = oracle.transform_f64(w.X, w.A, w.B)
     c, s, _ = kq.quantize_exact(Xd, Ad, Bd)
     assert_exact((host(c), host(s), None), (cr, sr, None), name)
     kp = kq.pack_factors(Ad, Bd)
@@ -547,7 +555,7 @@ def test_full_size_workloads(name):
                       ("packed", lambda wy: kq.quantize_packed(Xd, Ad, Bd, kp, want_y=wy))):
         c, s, y = run(True)
         with_y = (host(c), host(s), host(y))
-        assert_mx_close(with_y, (cr, sr, yr), f"{name} {what}")
+        assert_mx_close(with_y, (cr, sr, yr), f"{name} {what}", ye)
         c, s, _ = run(False)
         c, s = host(c), host(s)
         assert np.array_equal(c, with_y[0]) and np.array_equal(s, with_y[1]), f"{name} {what}: y on/off differ"
@@ -576,7 +584,7 @@ def test_lu_form_full_size(name):
     c2, s2, y, y16 = kq.quantize_lu(Xd, lud, 4, want_y=True, want_y16=True)
     assert np.array_equal(host(c2), c) and np.array_equal(host(s2), s), f"{name} lu: outputs on/off differ"
     y = host(y)
-    assert_mx_close((c, s, y), (cr, sr, yr), f"{name} lu (with y)")
+    assert_mx_close((c, s, y), (cr, sr, yr), f"{name} lu (with y)", oracle.transform_f64(w.X, *oracle.lu_factors_f32(lu, 4)))
     assert np.array_equal(host(y16.view(torch.int16)).view(np.uint16), oracle.f32_to_bf16(y))
 
 
@@ -591,12 +599,13 @@ def test_per_block_strips_ragged():
     X = synth.activations(M, d, "student_t3", seed=21, chan_frac=0.01, chan_factor=40)
     A, B = synth.factors(4, 8, d // 32, seed=22)
     cr, sr, yr = oracle.quantize(X, A, B, want_y=True)
+    ye = oracle.transform_f64(X, A, B)
     Xd, Ad, Bd = dev_bf16(X), dev_f32(A), dev_f32(B)
     c, s, y = kq.quantize(Xd, Ad, Bd, want_y=True)
-    assert_mx_close((host(c), host(s), host(y)), (cr, sr, yr), "on the fly")
+    assert_mx_close((host(c), host(s), host(y)), (cr, sr, yr), "on the fly", ye)
     c, s, y = kq.quantize_packed(Xd, Ad, Bd, kq.pack_factors(Ad, Bd), want_y=True)
-    assert_mx_close((host(c), host(s), host(y)), (cr, sr, yr), "packed")
-    del y
+    assert_mx_close((host(c), host(s), host(y)), (cr, sr, yr), "packed", ye)
+    del y, ye
     A1, B1 = synth.factors(4, 8, 1, seed=23)
     nb = d // 32
     g1 = gpu_quantize(X, A1, B1, exact=False)
@@ -619,7 +628,7 @@ def test_per_block_lu_strips_ragged(a):
     lu = synth.lu_params(nb, seed=32 + a)
     cr, sr, yr, _ = oracle.quantize_lu(X, lu, a, want_y=True)
     c, s, y, y16 = gpu_quantize_lu(X, lu, a)
-    assert_mx_close((c, s, y), (cr, sr, yr), f"lu a={a}")
+    assert_mx_close((c, s, y), (cr, sr, yr), f"lu a={a}", oracle.transform_f64(X, *oracle.lu_factors_f32(lu, a)))
     assert np.array_equal(y16, oracle.f32_to_bf16(y)), "y16 is not bf16(y)"
     del y, y16, yr
     lu1 = synth.lu_params(1, seed=33 + a)

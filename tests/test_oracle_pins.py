@@ -503,6 +503,21 @@ def test_mx_compare_accepts_tie_flips_and_rejects_the_rest():
     assert not cmp(c, s, c, s, y, y2)["ok"]
     y2[0, 2] = y[0, 2] * np.float32(1 + 4e-6)
     assert cmp(c, s, c, s, y, y2)["ok"]
+    # with the exact values given, y is measured against them instead of the fixed-order y
+    y_exact = y.astype(np.float64)
+    y_exact[0, 2] *= 1 + 1.5e-5
+    assert not cmp(c, s, c, s, y, y, y_exact=y_exact)["ok"]
+    y2[0, 2] = np.float32(y_exact[0, 2])
+    assert cmp(c, s, c, s, y, y2, y_exact=y_exact)["ok"] and not cmp(c, s, c, s, y, y2)["ok"]
+    # subnormal results: measured against 2^-126 (fp32 spacing 2^-149 there)
+    tiny = np.zeros((1, 32), np.float32)
+    tiny[0, 0] = np.float32(2.0 ** -140)
+    tiny2 = tiny.copy()
+    tiny2[0, 0] = np.float32(2.0 ** -140 + 2.0 ** -148)    # 1/256 relative, 2^-22 of 2^-126
+    ct, st, _ = oracle.quantize_f32(tiny, np.eye(4, dtype=np.float32)[None], np.eye(8, dtype=np.float32)[None])
+    assert cmp(ct, st, ct, st, tiny, tiny2)["ok"]
+    tiny2[0, 0] = np.float32(2.0 ** -140 + 2.0 ** -133)    # 2^-7 of 2^-126: too far
+    assert not cmp(ct, st, ct, st, tiny, tiny2)["ok"]
     assert not oracle.mx_compare(at_tie, s, c, s, y)["ok"]  # 1 of 32 codes is above the 1e-4 budget
 
 
