@@ -350,6 +350,31 @@ kq_status kq_calib_step(const uint16_t* X, int64_t R, int64_t d, const uint16_t*
                         float* adam_m, float* adam_v, int adam_t, float lr, void* workspace,
                         size_t workspace_bytes, void* stream);
 
+/* Scratch bytes held per GPU for kq_calib_step_noalloc (64 MiB). */
+#define KQ_CALIB_NOALLOC_MAX_BYTES (64u << 20)
+
+/*
+ * kq_calib_step_noalloc -- kq_calib_step without the workspace argument and
+ * without any allocation, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight loops, harnesses that forbid
+ * hipMalloc).  Its workspace is a scratch array of the library in device
+ * memory, KQ_CALIB_NOALLOC_MAX_BYTES bytes, one copy per GPU, held from the
+ * library's first use on that GPU until the process ends; its device address
+ * is looked up once per GPU on the first call there (with that GPU current).
+ * Arguments, results and errors as kq_calib_step; sizes whose workspace
+ * (kq_calib_workspace_size) exceeds KQ_CALIB_NOALLOC_MAX_BYTES return
+ * KQ_ERROR_INVALID_VALUE before any HIP call (e.g. R = 2048 rows with
+ * o = d = 1024 fit, R = 4096 with o = d = 1152 do not).  The step writes every
+ * part of the scratch it reads, so what an earlier call left there does not
+ * matter.  All calls on one GPU share its scratch: calls that overlap in time
+ * on one GPU (concurrent streams, or host threads enqueueing on different
+ * streams) race and give undefined results; calls on one stream are ordered
+ * and safe.  Enqueued on `stream`; no allocation, no synchronization.
+ */
+kq_status kq_calib_step_noalloc(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o,
+                                const float* Yneg, float* lu, int a, int64_t nfac, const float* lambdas, float* grad,
+                                double* losses, float* adam_m, float* adam_v, int adam_t, float lr, void* stream);
+
 /*
  * kq_calibrate -- the per-layer optimisation of Sec. 3.3 in one call:
  *   1. evaluate the objective at the given lu (the initial transform T_0,

@@ -25,6 +25,7 @@ EXPORTED = (
     "kq_stream_floor",
     "kq_e2m1_encode", "kq_weight_transform", "kq_factors_inverse_transpose", "kq_lu_to_factors",
     "kq_calib_workspace_size", "kq_calib_reference", "kq_calib_step", "kq_calibrate",
+    "kq_calib_step_noalloc",
     "kq_status_string", "kq_last_error_detail", "kq_version",
 )
 
@@ -64,7 +65,8 @@ def lib() -> ctypes.CDLL:
     L.kq_calib_reference.argtypes = [P, I64, I64, P, I64, P, P]
     L.kq_calib_step.argtypes = [P, I64, I64, P, I64, P, P, I, I64, P, P, P, P, P, I, F, P, ctypes.c_size_t, P]
     L.kq_calibrate.argtypes = [P, I64, I64, P, I64, P, P, I, I64, I, F, P, P, ctypes.c_size_t, P]
-    for name in EXPORTED[:18]:
+    L.kq_calib_step_noalloc.argtypes = [P, I64, I64, P, I64, P, P, I, I64, P, P, P, P, P, I, F, P]
+    for name in EXPORTED[:20]:
         getattr(L, name).restype = ctypes.c_int
     L.kq_status_string.argtypes = [I]
     L.kq_status_string.restype = ctypes.c_char_p
@@ -451,6 +453,42 @@ def calib_step(X, W, Yneg, lu, lambdas, a=4, workspace=None, adam=None, grad=Non
     _check(lib().kq_calib_step(_ptr(X), R, d, _ptr(W), o, _ptr(Yneg), _ptr(lu), a, nfac, _ptr(lambdas), _ptr(grad),
                                _ptr(losses), _ptr(m), _ptr(v), int(t), float(lr), _ptr(workspace),
                                workspace.numel(), _stream(stream)), "kq_calib_step")
+    return losses, grad
+
+
+CALIB_NOALLOC_MAX_BYTES = 64 << 20
+
+
+def calib_step_noalloc(X, W, Yneg, lu, lambdas, a=4, adam=None, grad=None, losses=None, stream=None):
+    """kq_calib_step_noalloc: kq_calib_step on the library's own per-GPU
+    scratch (no workspace argument, no allocation inside the call; for sizes
+    whose workspace fits CALIB_NOALLOC_MAX_BYTES).  ``grad`` and ``losses``
+    are allocated here when not given (pass them to allocate nothing).
+    Returns (losses, grad)."""
+    _need(X, torch.bfloat16, "X")
+    _need(W, torch.bfloat16, "W")
+    _need(lu, torch.float32, "lu")
+    _need(lambdas, torch.float32, "lambdas")
+    R, d, o, nfac = _calib_shapes(X, W, Yneg, lu)
+    _size(lambdas, 2, "lambdas", X.device)
+    if grad is None:
+        grad = torch.empty((nfac, 5, 3), dtype=torch.float32, device=X.device)
+    if losses is None:
+        losses = torch.empty(4, dtype=torch.float64, device=X.device)
+    _need(grad, torch.float32, "grad")
+    _size(grad, nfac * 15, "grad", X.device)
+    _need(losses, torch.float64, "losses")
+    _size(losses, 4, "losses", X.device)
+    m = v = None
+    t, lr = 0, 0.0
+    if adam is not None:
+        m, v, t, lr = adam
+        for buf, name in ((m, "adam m"), (v, "adam v")):
+            _need(buf, torch.float32, name)
+            _size(buf, nfac * 15, name, X.device)
+    _check(lib().kq_calib_step_noalloc(_ptr(X), R, d, _ptr(W), o, _ptr(Yneg), _ptr(lu), a, nfac, _ptr(lambdas),
+                                       _ptr(grad), _ptr(losses), _ptr(m), _ptr(v), int(t), float(lr),
+                                       _stream(stream)), "kq_calib_step_noalloc")
     return losses, grad
 
 

@@ -9,6 +9,7 @@
 #include <cstdio>
 #include <cstdint>
 #include <cstdlib>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -508,10 +509,10 @@ static kq_status check_workspace(const kq::CalibPlan& pl, const void* ws, size_t
     return ok();
 }
 
-kq_status kq_calib_step(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o, const float* Yneg,
-                        float* lu, int a, int64_t nfac, const float* lambdas, float* grad, double* losses,
-                        float* adam_m, float* adam_v, int adam_t, float lr, void* workspace,
-                        size_t workspace_bytes, void* stream) {
+// Argument checks of one calibration step (everything but the workspace).
+static kq_status check_step(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o, const float* Yneg,
+                            const float* lu, int a, int64_t nfac, const float* lambdas, const float* grad,
+                            const double* losses, const float* adam_m, const float* adam_v, int adam_t) {
     kq_status st = check_calib(X, R, d, W, o, a, nfac);
     if (st != KQ_SUCCESS) return st;
     if (!Yneg || !lu || !lambdas || !grad || !losses)
@@ -523,11 +524,79 @@ kq_status kq_calib_step(const uint16_t* X, int64_t R, int64_t d, const uint16_t*
         return fail(KQ_ERROR_NULL_POINTER, "adam_m and adam_v must not be NULL when adam_t > 0");
     if (adam_t > 0 && (!aligned(adam_m, 4) || !aligned(adam_v, 4)))
         return fail(KQ_ERROR_MISALIGNED, "adam_m and adam_v must be 4-byte aligned");
+    return ok();
+}
+
+kq_status kq_calib_step(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o, const float* Yneg,
+                        float* lu, int a, int64_t nfac, const float* lambdas, float* grad, double* losses,
+                        float* adam_m, float* adam_v, int adam_t, float lr, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+    kq_status st = check_step(X, R, d, W, o, Yneg, lu, a, nfac, lambdas, grad, losses, adam_m, adam_v, adam_t);
+    if (st != KQ_SUCCESS) return st;
     const kq::CalibPlan pl = kq::calib_plan(R, o, d, a, nfac);
     st = check_workspace(pl, workspace, workspace_bytes);
     if (st != KQ_SUCCESS) return st;
     return calib_step_impl(pl, X, W, Yneg, lu, lambdas, grad, losses, adam_m, adam_v, adam_t, lr,
                            static_cast<unsigned char*>(workspace), (hipStream_t)stream);
+}
+
+}  // extern "C"
+
+// Device-resident scratch of kq_calib_step_noalloc: one copy per GPU, held
+// until the process ends.  Host code never passes `calib_scratch` itself (on
+// the host that name is a stand-in, not a device address): the device address
+// of each GPU's copy comes from hipGetSymbolAddress, taken once per device
+// with that device current, and only that address reaches the kernels.
+static __device__ __align__(256) unsigned char calib_scratch[KQ_CALIB_NOALLOC_MAX_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of the current device's calib_scratch (looked up on the
+// first call on that device).
+kq_status scratch_address(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return from_hip(e, "kq_calib_step_noalloc: hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(KQ_ERROR_UNSUPPORTED, "kq_calib_step_noalloc: device %d is beyond the %d devices supported", dev,
+                    kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(calib_scratch));
+        if (e != hipSuccess) return from_hip(e, "kq_calib_step_noalloc: hipGetSymbolAddress");
+        if (!ptr || !aligned(ptr, 256))
+            return fail(KQ_ERROR_HIP, "kq_calib_step_noalloc: unusable scratch address %p", ptr);
+        g_scratch[dev] = ptr;
+    }
+    *out = g_scratch[dev];
+    return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+kq_status kq_calib_step_noalloc(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o,
+                                const float* Yneg, float* lu, int a, int64_t nfac, const float* lambdas, float* grad,
+                                double* losses, float* adam_m, float* adam_v, int adam_t, float lr, void* stream) {
+    kq_status st = check_step(X, R, d, W, o, Yneg, lu, a, nfac, lambdas, grad, losses, adam_m, adam_v, adam_t);
+    if (st != KQ_SUCCESS) return st;
+    const kq::CalibPlan pl = kq::calib_plan(R, o, d, a, nfac);
+    if (pl.total > (size_t)KQ_CALIB_NOALLOC_MAX_BYTES)
+        return fail(KQ_ERROR_INVALID_VALUE,
+                    "kq_calib_step_noalloc: these sizes need %zu bytes of scratch, more than the %zu it holds "
+                    "(use kq_calib_step with a workspace)", pl.total, (size_t)KQ_CALIB_NOALLOC_MAX_BYTES);
+    void* ws = nullptr;
+    if ((st = scratch_address(&ws)) != KQ_SUCCESS) return st;
+    // every buffer of the plan is written before it is read within the step,
+    // so the previous call's contents need no clearing
+    return calib_step_impl(pl, X, W, Yneg, lu, lambdas, grad, losses, adam_m, adam_v, adam_t, lr,
+                           static_cast<unsigned char*>(ws), (hipStream_t)stream);
 }
 
 kq_status kq_calibrate(const uint16_t* X, int64_t R, int64_t d, const uint16_t* W, int64_t o, const float* Yneg,

@@ -286,3 +286,15 @@ def test_binding_rejects_before_the_library_is_called():
         kq.quantize(torch.zeros((4, 64), dtype=torch.bfloat16), torch.zeros((1, 4, 4)), torch.zeros((1, 8, 8)))
     with pytest.raises(ValueError):
         kq.lu_to_factors(torch.zeros(14), 4)
+
+
+def test_calib_step_noalloc_refuses_before_any_hip_call():
+    """Sizes whose workspace exceeds the library's per-GPU scratch are refused
+    before any HIP call (so this runs without a GPU)."""
+    L = kq.lib()
+    st = L.kq_calib_step_noalloc(FAKE, 4096, 1152, FAKE, 1152, FAKE, FAKE, 4, 36, FAKE, FAKE, FAKE, None, None, 0,
+                                 0.0, None)
+    assert st == INVALID and b"scratch" in L.kq_last_error_detail()
+    assert L.kq_calib_step_noalloc(FAKE, 0, 64, FAKE, 8, FAKE, FAKE, 4, 1, FAKE, FAKE, FAKE, None, None, 0, 0.0,
+                                   None) == INVALID
+    assert kq.CALIB_NOALLOC_MAX_BYTES == 64 << 20
