@@ -83,10 +83,11 @@ def parse():
     ap.add_argument("--no-calib", action="store_true", help="skip the layer-wise calibration timing")
     ap.add_argument("--calib-samples", type=int, default=128,
                     help="calibration samples of 4608 tokens for the calibration timing")
-    ap.add_argument("--no-large", action="store_true",
-                    help="skip the large stress shape, X [18432, 12288] with 384 per-block factor pairs")
-    ap.add_argument("--no-wide", action="store_true",
-                    help="skip the second FLUX shape, X [4608, 12288] (the MLP down-projection input)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-workload table (every DiT shape, the one-GPU shard and the large per-block "
+                         "stress shape; KroQuant variants and comparators)")
+    ap.add_argument("--configs", default=",".join(CONFIG_WORKLOADS),
+                    help="comma-separated workloads of the table (default: all)")
     ap.add_argument("--no-table2", action="store_true",
                     help="skip the power-of-two-d comparison (Q4, Scale, K1, K2, FWHT) at the paper's Table 2 shapes")
     return ap.parse_args()
@@ -311,6 +312,7 @@ def main():
         comparators[name + "_us"] = round(ms * 1e3, 3)
         comparators[name + "_gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
     ms_floor_eager, _ = timed_eager(run_floor, args.steps, args.warmup)
+    ceiling = launch_sweep(kq, Xs, Cs, Ss, nsets, args.steps, nbytes, stream)
     ms_warm, _ = timed(run_kq, args.steps, args.warmup, rotate=False)
     # the vendor's device-to-device copy moving the same HBM bytes as one step
     # (half of them read, half written), with the same rotation
@@ -324,8 +326,9 @@ def main():
     ms_copy, _ = timed(run_copy, args.steps, args.warmup)
     del copy_dst
     table2 = None if args.no_table2 else table2_shapes(kq, synth, dev, stream, sptr)
-    wide = None if args.no_wide else wide_shape(kq, synth, dev, stream, timed_graph_steps=args.steps)
-    large = None if args.no_large else large_per_block(kq, synth, dev, stream)
+    wl_cache = {WORKLOAD: w}
+    configs = None if args.no_configs else config_table(kq, synth, dev, stream, names=args.configs.split(","),
+                                                        cache=wl_cache)
     gemm = None if args.no_gemm else gemm_timing(kq, synth, dev, stream, sptr, Cs[0], Ss[0], M, d)
     calib = None if args.no_calib else calib_timing(kq, synth, dev, stream, sptr, args.calib_samples)
     dist = per_launch(run_kq)
@@ -343,7 +346,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, nbytes)
+        cpu = cpu_baseline(w, nbytes, wl_cache, synth)
 
     line = {
         "metric": METRIC,
@@ -369,6 +372,8 @@ def main():
                           "frac_of_peak": round(comparators["stream_floor_gbs"] / HBM_PEAK_GBS, 4),
                           "hot_path_frac_of_floor": round(comparators["stream_floor_us"] / us_kq, 4),
                           "what": "kq_stream_floor: the same loads, stores and launch shape with no arithmetic"},
+        "single_launch_ceiling": ceiling,
+        "hot_path_frac_of_ceiling": round(ceiling["us"] / us_kq, 4),
         "vendor_copy": {"us": round(ms_copy * 1e3, 3), "gbs": round(2 * half / (ms_copy * 1e-3) / 1e9, 1),
                         "frac_of_peak": round(2 * half / (ms_copy * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                         "what": "torch copy_ (device to device) of half the step's bytes: the same HBM traffic "
@@ -388,8 +393,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
         "cpu_baseline": cpu,
-        "flux_4608x12288": wide,
-        "large_18432x12288_per_block": large,
+        "configs": configs,
         "table2_pow2_d": table2,
         "w4a4_gemm": gemm,
         "calibration": calib,
@@ -397,109 +401,148 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def wide_shape(kq, synth, dev, stream, timed_graph_steps=1000, warmup=1000):
-    """The other FLUX.1-schnell activation shape, X bf16 [4608, 12288] (input of
-    the MLP down-projection; 143 MB per step): the hot path, SmoothQuant, plain
-    MXFP4 and the traffic-only kernel, each as K launches captured into a HIP
-    graph (MALL-cold rotation) replayed between HIP events."""
+# Every workload of the paper's shapes that the benchmark times (name -> how it is built):
+# the DiT activation shapes, the shard one GPU holds when FLUX's 12288-wide MLP input is split
+# eight ways along d (tensor parallelism; the quantizer has no cross-GPU step), and the large
+# per-block stress shape in both factor splits.
+CONFIG_WORKLOADS = ["tiny_256x1152", "pixart_8192x1152", "pixart_8192x4608", "sana_4096x2240", "sana_4096x5600",
+                    "flux_4608x3072", "flux_4608x12288", "shard_4608x1536", "large_18432x12288",
+                    "large_18432x12288_2x16"]
+
+
+def _config_inputs(name, synth, dev, cache):
+    """(X on the device, A, B, lu, mult, per_block, description) of one table workload."""
     import torch
-    w = synth.workload("flux_4608x12288")
-    M, d = w.X.shape
-    nbytes = algorithmic_bytes(M, d)
-    nsets = max(2, int(np.ceil(2 * MALL_BYTES / nbytes)) + 1)
-    X0 = torch.from_numpy(w.X.view(np.int16)).view(torch.bfloat16).to(dev)
-    Xs = [X0.clone() for _ in range(nsets)]
-    Cs = [torch.empty((M, d // 2), dtype=torch.uint8, device=dev) for _ in range(nsets)]
-    Ss = [torch.empty((M, d // 32), dtype=torch.uint8, device=dev) for _ in range(nsets)]
-    A, B = torch.from_numpy(w.A).to(dev), torch.from_numpy(w.B).to(dev)
-    mult = torch.from_numpy(w.mult).to(dev)
-    kpack = kq.pack_factors(A, B)
-    fns = {
-        "kroquant": lambda i: kq.quantize_packed(Xs[i], A, B, kpack, codes=Cs[i], scales=Ss[i]),
-        "smoothquant": lambda i: kq.smoothquant(Xs[i], mult, codes=Cs[i], scales=Ss[i]),
-        "mxfp4": lambda i: kq.mxfp4(Xs[i], codes=Cs[i], scales=Ss[i]),
-        "stream_floor": lambda i: kq.stream_floor(Xs[i], out16=Cs[i], out1=Ss[i]),
-    }
-    steps = max(1, timed_graph_steps // 4)  # ~25 us per step: a quarter of the headline's step count
-    out = {"M": M, "d": d, "algorithmic_bytes": nbytes, "steps": steps,
-           "mall": f"cold: {nsets} rotating buffer sets, {nsets * nbytes / 1e6:.0f} MB"}
-    for name, fn in fns.items():
-        for i in range(warmup):
-            fn(i % nsets)
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            for i in range(steps):
-                fn(i % nsets)
-        g.replay()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        g.replay()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        us = e0.elapsed_time(e1) / steps * 1e3
-        gbs = nbytes / us * 1e-3
-        out[name] = {"us": round(us, 3), "gbs": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
-        del g
-    out["kroquant_vs_smoothquant"] = round(out["smoothquant"]["us"] / out["kroquant"]["us"], 3)
-    del Xs, Cs, Ss, X0
-    torch.cuda.empty_cache()
-    return out
-
-
-def large_per_block(kq, synth, dev, stream, steps=50, warmup=20):
-    """The large stress shape: FLUX batch 4, X bf16 [18432, 12288] (453 MB in,
-    573 MB per step), one factor pair per 32-column block (384 pairs), for
-    the (4, 8) and (2, 16) splits: the packed and on-the-fly KroQuant calls
-    and SmoothQuant, as `steps` launches over two rotating input sets (1.15 GB)
-    captured into a HIP graph and replayed between HIP events.  The input is
-    drawn on the device (the Student-t(3) recipe with torch's generator; the
-    host generator would take about a minute at this size); outputs at this
-    shape are checked against the oracle by the GPU tests on sampled rows."""
-    import torch
-    M, d = 18432, 12288
-    nb = d // 32
-    nbytes = algorithmic_bytes(M, d)
-    nsets = 2
-    Xs = [synth.activations_device(M, d, seed=100 + i, device=dev) for i in range(nsets)]
-    Cs = [torch.empty((M, d // 2), dtype=torch.uint8, device=dev) for _ in range(nsets)]
-    Ss = [torch.empty((M, nb), dtype=torch.uint8, device=dev) for _ in range(nsets)]
-    mult = torch.ones(d, dtype=torch.float32, device=dev)
-    out = {"M": M, "d": d, "nfac": nb, "algorithmic_bytes": nbytes, "steps": steps,
-           "mall": f"cold: {nsets} rotating input sets, {nsets * nbytes / 1e6:.0f} MB",
-           "inputs": "drawn on the device (Student-t(3), 0.5% channels x50)"}
-
-    def time_fn(fn):
-        for i in range(warmup):
-            fn(i % nsets)
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            for i in range(steps):
-                fn(i % nsets)
-        g.replay()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        g.replay()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        us = e0.elapsed_time(e1) / steps * 1e3
-        del g
-        gbs = nbytes / us * 1e-3
-        return {"us": round(us, 2), "gbs": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
-
-    for a, b in ((4, 8), (2, 16)):
+    if name.startswith("large"):
+        a, b = (2, 16) if name.endswith("2x16") else (4, 8)
+        M, d = 18432, 12288
+        nb = d // 32
+        if "large_X" not in cache:
+            cache["large_X"] = synth.activations_device(M, d, seed=100, device=dev)
+        X = cache["large_X"]
         A, B = synth.factors(a, b, nb, seed=4)
+        lu = synth.lu_params(nb, seed=8)
+        amax = X.abs().amax(0).float()
+        mult = torch.where(amax > 0, amax.rsqrt(), torch.ones_like(amax))
+        return X, A, B, lu, mult, True, (f"Student-t(3), 0.5% channels x50, drawn on the device; {nb} factor "
+                                         f"pairs ({a}x{a} (x) {b}x{b}) and {nb} LU sets, one per 32-column block")
+    if name == "shard_4608x1536":
+        w = cache.get("flux_4608x12288") or synth.workload("flux_4608x12288")
+        cache["flux_4608x12288"] = w
+        Xh = np.ascontiguousarray(w.X[:, :1536])
+        desc = "columns 0..1535 of flux_4608x12288 (its share of one GPU when d is split 8 ways)"
+        A, B, mult = w.A, w.B, synth.smoothquant_multipliers(Xh)
+    else:
+        w = cache.get(name) or synth.workload(name)
+        cache[name] = w
+        Xh, A, B, mult = w.X, w.A, w.B, w.mult
+        desc = f"{w.meta['dist']}, seed {w.meta['seed']}"
+    X = torch.from_numpy(Xh.view(np.int16)).view(torch.bfloat16).to(dev)
+    return X, A, B, synth.lu_params(1, seed=7), torch.from_numpy(mult).to(dev), False, desc
+
+
+def _graph_us(fn, nsets, steps, stream):
+    """Per-launch time of `steps` launches of fn(i % nsets) captured once into
+    a HIP graph: 3 untimed replays, then the median of 3 replays between HIP
+    events on the launch stream."""
+    import torch
+    for i in range(nsets):  # eager pass over every set
+        fn(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(steps):
+            fn(i % nsets)
+    for _ in range(3):  # untimed: upload, then clocks settle
+        g.replay()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) / steps * 1e3)
+    del g
+    return float(np.median(ts))
+
+
+# Launch shapes of the traffic-only probe: (waves per workgroup, 64-block units per wave, workgroups;
+# 0 = one pass over the units, else a grid-stride loop)
+PROBE_SHAPES = [(1, 1, 0), (2, 1, 0), (4, 1, 0), (8, 1, 0), (16, 1, 0), (1, 2, 0), (1, 4, 0), (2, 4, 0),
+                (1, 1, 2048), (1, 1, 4096), (4, 1, 1024), (16, 1, 256)]
+
+
+def launch_sweep(kq, Xs, Cs, Ss, nsets, steps, nbytes, stream):
+    """The quantizers' traffic (kq_stream_probe) in every launch shape of
+    PROBE_SHAPES, and kq_stream_floor (one wave, one unit, the quantizers'
+    own shape): what one launch of these bytes reaches on this chip."""
+    sweep = {"kq_stream_floor": round(_graph_us(lambda i: kq.stream_floor(Xs[i], out16=Cs[i], out1=Ss[i]), nsets,
+                                                steps, stream), 3)}
+    for w, u, g in PROBE_SHAPES:
+        us = _graph_us(lambda i: kq.stream_probe(Xs[i], w, u, g, out16=Cs[i], out1=Ss[i]), nsets, steps, stream)
+        sweep[f"waves{w}_units{u}_" + (f"stride{g}" if g else "onepass")] = round(us, 3)
+    best = min(sweep, key=sweep.get)
+    gbs = nbytes / sweep[best] * 1e-3
+    return {"us": sweep[best], "gbs": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4), "shape": best,
+            "sweep_us": sweep,
+            "what": "kq_stream_probe: the quantizers' bytes (2 B read, 17/32 B written per element) in each launch "
+                    "shape listed, and kq_stream_floor; the best one is the single-launch ceiling of this traffic"}
+
+
+def config_table(kq, synth, dev, stream, names=CONFIG_WORKLOADS, graph_bytes=20e9, cache=None):
+    """Every workload of CONFIG_WORKLOADS: KroQuant (packed K1, on-the-fly K2
+    from A and B, LU-form K2 from the 15 parameters), SmoothQuant, Hadamard-32,
+    plain MXFP4 and the traffic-only kernel on identical inputs.  Each kernel's
+    launches (about graph_bytes of traffic, 30 to 2000 launches) are captured
+    once into a HIP graph over enough rotating buffer sets to exceed twice the
+    MALL, and the graph is replayed between HIP events."""
+    import torch
+    cache = {} if cache is None else cache
+    out = {}
+    for name in names:
+        X0, A, B, lu, mult, per_block, desc = _config_inputs(name, synth, dev, cache)
+        M, d = X0.shape
+        nbytes = algorithmic_bytes(M, d)
+        nsets = 2 if per_block else max(2, int(np.ceil(2 * MALL_BYTES / nbytes)) + 1)
+        Xs = [X0] + [X0.clone() for _ in range(nsets - 1)]
+        Cs = [torch.empty((M, d // 2), dtype=torch.uint8, device=dev) for _ in range(nsets)]
+        Ss = [torch.empty((M, d // 32), dtype=torch.uint8, device=dev) for _ in range(nsets)]
         Ad, Bd = torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev)
+        lud = torch.from_numpy(lu).to(dev)
         kpack = kq.pack_factors(Ad, Bd)
-        out[f"kroquant_packed_{a}x{b}"] = time_fn(
-            lambda i: kq.quantize_packed(Xs[i], Ad, Bd, kpack, codes=Cs[i], scales=Ss[i]))
-        out[f"kroquant_onthefly_{a}x{b}"] = time_fn(lambda i: kq.quantize(Xs[i], Ad, Bd, codes=Cs[i], scales=Ss[i]))
-    out["smoothquant"] = time_fn(lambda i: kq.smoothquant(Xs[i], mult, codes=Cs[i], scales=Ss[i]))
-    del Xs, Cs, Ss
+        fns = {
+            "kroquant_packed": lambda i: kq.quantize_packed(Xs[i], Ad, Bd, kpack, codes=Cs[i], scales=Ss[i]),
+            "kroquant_onthefly": lambda i: kq.quantize(Xs[i], Ad, Bd, codes=Cs[i], scales=Ss[i]),
+            "kroquant_lu": lambda i: kq.quantize_lu(Xs[i], lud, A.shape[-1], codes=Cs[i], scales=Ss[i]),
+            "smoothquant": lambda i: kq.smoothquant(Xs[i], mult, codes=Cs[i], scales=Ss[i]),
+            "hadamard32": lambda i: kq.hadamard32(Xs[i], codes=Cs[i], scales=Ss[i]),
+            "mxfp4": lambda i: kq.mxfp4(Xs[i], codes=Cs[i], scales=Ss[i]),
+            "stream_floor": lambda i: kq.stream_floor(Xs[i], out16=Cs[i], out1=Ss[i]),
+        }
+        steps = int(min(2000, max(30, graph_bytes // nbytes)))
+        row = {"M": M, "d": d, "a": int(A.shape[-1]), "b": int(B.shape[-1]), "nfac": int(A.shape[0]),
+               "input": desc, "algorithmic_bytes": nbytes, "steps": steps,
+               "mall": f"cold: {nsets} rotating buffer sets, {nsets * nbytes / 1e6:.0f} MB"}
+        for kname, fn in fns.items():
+            us = _graph_us(fn, nsets, steps, stream)
+            gbs = nbytes / us * 1e-3
+            row[kname] = {"us": round(us, 3), "gbs": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
+        sq = row["smoothquant"]["us"]
+        for k in ("kroquant_packed", "kroquant_onthefly", "kroquant_lu"):
+            row[k]["vs_smoothquant"] = round(sq / row[k]["us"], 3)
+        row["hadamard32"]["vs_smoothquant"] = round(sq / row["hadamard32"]["us"], 3)
+        if name == "flux_4608x12288":
+            row["single_launch_ceiling"] = launch_sweep(kq, Xs, Cs, Ss, nsets, steps, nbytes, stream)
+        out[name] = row
+        del Xs, Cs, Ss, X0, kpack
+        torch.cuda.empty_cache()
+    cache.pop("large_X", None)
     torch.cuda.empty_cache()
+    out["timing"] = ("per kernel: a HIP graph of `steps` launches over MALL-cold rotating buffer sets, replayed 3 "
+                     "times untimed, then the median of 3 replays between HIP events; vs_smoothquant = SmoothQuant "
+                     "time / this kernel's time")
     return out
 
 
@@ -702,9 +745,21 @@ def check_parity(w, run_kq, run_k2, run_kx, Cs, Ss):
     return out
 
 
-def cpu_baseline(w, nbytes):
-    """The oracle, untuned, on this host's cores: whole-workload passes until
-    at least 10 s have elapsed (at most 30 s, at least one pass)."""
+def _oracle_seconds(w, passes):
+    import oracle
+    t = []
+    for _ in range(passes):
+        t0 = time.perf_counter()
+        oracle.quantize(w.X, w.A, w.B)
+        t.append(time.perf_counter() - t0)
+    return float(np.median(t))
+
+
+def cpu_baseline(w, nbytes, cache, synth):
+    """The oracle, untuned, on this host's cores: whole-workload passes of the
+    headline workload until at least 10 s have elapsed (at most 30 s, at least
+    one pass), then the same oracle on one thread (median of 3); and the Tiny
+    and wide FLUX workloads on all cores and on one thread (median of 3 each)."""
     import oracle
     threads = oracle.num_threads()
     times = []
@@ -717,21 +772,31 @@ def cpu_baseline(w, nbytes):
         if el >= 10.0 or el + times[-1] > 30.0:
             break
     t = float(np.median(times))
-    # the same oracle on one thread: three passes (median)
+    others = {}
     oracle.set_num_threads(1)
     try:
-        t1 = []
-        for _ in range(3):
-            t0 = time.perf_counter()
-            oracle.quantize(w.X, w.A, w.B)
-            t1.append(time.perf_counter() - t0)
+        t1m = _oracle_seconds(w, 3)
     finally:
         oracle.set_num_threads(threads)
-    t1m = float(np.median(t1))
+    for name in ("tiny_256x1152", "flux_4608x12288"):
+        wo = cache.get(name) or synth.workload(name)
+        cache[name] = wo
+        nb_o = algorithmic_bytes(*wo.X.shape)
+        t_all = _oracle_seconds(wo, 3)
+        oracle.set_num_threads(1)
+        try:
+            t_one = _oracle_seconds(wo, 3)
+        finally:
+            oracle.set_num_threads(threads)
+        others[name] = {"all_cores": {"gbs": round(nb_o / t_all / 1e9, 3), "s_per_pass": round(t_all, 4),
+                                      "threads": threads},
+                        "one_thread": {"gbs": round(nb_o / t_one / 1e9, 3), "s_per_pass": round(t_one, 4)},
+                        "sample": "3 full passes each (median)"}
     return {"value": round(nbytes / t / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"{len(times)} full passes of {w.name} (median {t:.3f} s per pass)",
             "single_thread": {"value": round(nbytes / t1m / 1e9, 3), "unit": "GB/s",
                               "sample": f"3 full passes of {w.name} on 1 thread (median {t1m:.3f} s per pass)"},
+            "other_workloads": others,
             "host_cpus": os.cpu_count(), "cpu_model": _cpu_model()}
 
 

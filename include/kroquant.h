@@ -235,6 +235,21 @@ kq_status kq_mxfp4_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* co
 kq_status kq_stream_floor(const uint16_t* X, int64_t M, int64_t d, uint8_t* out16, uint8_t* out1, void* stream);
 
 /*
+ * kq_stream_probe -- a measurement aid like kq_stream_floor (same traffic,
+ * same outputs) in a launch shape given by the caller, to measure what a
+ * single launch of that traffic can reach independently of the quantizers'
+ * own shape: waves_per_group (1, 2, 4, 8 or 16) waves per workgroup, each
+ * taking units_per_wave (1, 2 or 4) consecutive 64-block units with all
+ * their loads issued before any store; groups = 0 launches one pass
+ * (ceil(units / (waves_per_group * units_per_wave)) workgroups), groups > 0
+ * that many workgroups walking the units in a grid-stride loop.  Other
+ * arguments, outputs and errors as kq_stream_floor; a shape outside these
+ * sets is KQ_ERROR_INVALID_VALUE.
+ */
+kq_status kq_stream_probe(const uint16_t* X, int64_t M, int64_t d, uint8_t* out16, uint8_t* out1,
+                          int waves_per_group, int units_per_wave, int64_t groups, void* stream);
+
+/*
  * kq_e2m1_encode -- the element-encode step alone, for checking the device
  * conversion: codes[i] = code(v[2i]) | code(v[2i+1]) << 4 at E8M0 byte s
  * (0..254), with the rounding rule above.  v device fp32 [n], n even;

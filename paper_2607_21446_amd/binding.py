@@ -22,7 +22,7 @@ STATUS = {
 EXPORTED = (
     "kq_quantize", "kq_quantize_exact", "kq_quantize_packed", "kq_pack_factors", "kq_quantize_lu",
     "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_fwht_quantize", "kq_mxfp4_quantize", "kq_mxfp4_gemm",
-    "kq_stream_floor",
+    "kq_stream_floor", "kq_stream_probe",
     "kq_e2m1_encode", "kq_weight_transform", "kq_factors_inverse_transpose", "kq_lu_to_factors",
     "kq_calib_workspace_size", "kq_calib_reference", "kq_calib_step", "kq_calibrate",
     "kq_calib_step_noalloc",
@@ -57,6 +57,7 @@ def lib() -> ctypes.CDLL:
     L.kq_mxfp4_gemm.argtypes = [P, P, I64, P, P, I64, I64, P, I64, I, P]
     L.kq_mxfp4_quantize.argtypes = [P, I64, I64, P, P, P]
     L.kq_stream_floor.argtypes = [P, I64, I64, P, P, P]
+    L.kq_stream_probe.argtypes = [P, I64, I64, P, P, I, I, I64, P]
     L.kq_e2m1_encode.argtypes = [P, I64, I, P, P]
     L.kq_weight_transform.argtypes = [P, I64, I64, P, P, I, I, I64, P, P, P, P]
     L.kq_factors_inverse_transpose.argtypes = [P, P, I, I, I64, P, P]
@@ -66,7 +67,7 @@ def lib() -> ctypes.CDLL:
     L.kq_calib_step.argtypes = [P, I64, I64, P, I64, P, P, I, I64, P, P, P, P, P, I, F, P, ctypes.c_size_t, P]
     L.kq_calibrate.argtypes = [P, I64, I64, P, I64, P, P, I, I64, I, F, P, P, ctypes.c_size_t, P]
     L.kq_calib_step_noalloc.argtypes = [P, I64, I64, P, I64, P, P, I, I64, P, P, P, P, P, I, F, P]
-    for name in EXPORTED[:20]:
+    for name in EXPORTED[:21]:
         getattr(L, name).restype = ctypes.c_int
     L.kq_status_string.argtypes = [I]
     L.kq_status_string.restype = ctypes.c_char_p
@@ -306,6 +307,16 @@ def stream_floor(X, out16=None, out1=None, stream=None):
     out16, out1, _ = _outputs(X, out16, out1, None, False)
     M, d = X.shape
     _check(lib().kq_stream_floor(_ptr(X), M, d, _ptr(out16), _ptr(out1), _stream(stream)), "kq_stream_floor")
+    return out16, out1
+
+
+def stream_probe(X, waves=1, units=1, groups=0, out16=None, out1=None, stream=None):
+    """kq_stream_probe: kq_stream_floor's traffic in another launch shape (a timing aid)."""
+    _need(X, torch.bfloat16, "X")
+    out16, out1, _ = _outputs(X, out16, out1, None, False)
+    M, d = X.shape
+    _check(lib().kq_stream_probe(_ptr(X), M, d, _ptr(out16), _ptr(out1), int(waves), int(units), int(groups),
+                                 _stream(stream)), "kq_stream_probe")
     return out16, out1
 
 

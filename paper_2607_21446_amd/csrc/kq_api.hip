@@ -291,6 +291,23 @@ kq_status kq_stream_floor(const uint16_t* X, int64_t M, int64_t d, uint8_t* out1
     return from_hip(kq::launch_stream_floor(p, (hipStream_t)stream), "kq_stream_floor");
 }
 
+kq_status kq_stream_probe(const uint16_t* X, int64_t M, int64_t d, uint8_t* out16, uint8_t* out1,
+                          int waves_per_group, int units_per_wave, int64_t groups, void* stream) {
+    kq_status st = check_common(X, M, d, out16, out1, nullptr, true);
+    if (st != KQ_SUCCESS) return st;
+    const int w = waves_per_group, u = units_per_wave;
+    if (w != 1 && w != 2 && w != 4 && w != 8 && w != 16)
+        return fail(KQ_ERROR_INVALID_VALUE, "waves_per_group = %d must be 1, 2, 4, 8 or 16", w);
+    if (u != 1 && u != 2 && u != 4) return fail(KQ_ERROR_INVALID_VALUE, "units_per_wave = %d must be 1, 2 or 4", u);
+    if (groups < 0 || groups > kq::kMaxUnitGrid)
+        return fail(KQ_ERROR_INVALID_VALUE, "groups = %lld must be in [0, 2^31 - 1]", (long long)groups);
+    if (M == 0) return ok();
+    kq::Params p = make_params(X, M, d, out16, out1, nullptr);
+    if (groups == 0 && ((p.nblocks + 63) / 64 + (int64_t)w * u - 1) / ((int64_t)w * u) > kq::kMaxUnitGrid)
+        return fail(KQ_ERROR_INVALID_VALUE, "M * d = %lld * %lld is too large for one pass", (long long)M, (long long)d);
+    return from_hip(kq::launch_stream_probe(p, w, u, groups, (hipStream_t)stream), "kq_stream_probe");
+}
+
 static kq::GemmParams gemm_params(const uint8_t* a_codes, const uint8_t* a_scales, int64_t M, const uint8_t* b_codes,
                                   const uint8_t* b_scales, int64_t N, int64_t K, float* C, int64_t ldc, int accumulate,
                                   const float* bias) {

@@ -62,5 +62,8 @@ hipError_t launch_pack(int a, const float* A, const float* B, int64_t nfac, uint
 hipError_t launch_e2m1(const float* v, int64_t npairs, uint32_t s, uint8_t* codes, hipStream_t st);
 hipError_t launch_fwht(const Params& p, hipStream_t st);  // d a power of two, 32 .. 16384
 hipError_t launch_stream_floor(const Params& p, hipStream_t st);  // traffic of the quantizers, no arithmetic
+// the same traffic in another launch shape: waves per workgroup (1, 2, 4, 8, 16), units per wave (1, 2, 4),
+// groups > 0: that many workgroups in a grid-stride loop, else one pass
+hipError_t launch_stream_probe(const Params& p, int waves, int units, int64_t groups, hipStream_t st);
 
 }  // namespace kq

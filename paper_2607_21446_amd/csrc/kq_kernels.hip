@@ -1364,6 +1364,53 @@ __global__ __launch_bounds__(64) void stream_floor_kernel(const Params p) {
     }
 }
 
+// Launch-shape probe of the same traffic, a measurement aid that is not tied
+// to the quantizers' launch shape: W waves per workgroup, U units per wave
+// with all U x 4 loads issued before any store; with `stride` the grid walks
+// the units in a grid-stride loop, else each wave takes U units once.  Same
+// outputs as stream_floor_kernel.
+template <int U, int W>
+__global__ __launch_bounds__(64 * W) void stream_probe_kernel(const Params p, int stride) {
+    const int lane = threadIdx.x & 63;
+    const int64_t nunits = (p.nblocks + 63) / 64;
+    const int64_t wstep = (int64_t)gridDim.x * W;
+    for (int64_t wv = (int64_t)blockIdx.x * W + (threadIdx.x >> 6); wv * U < nunits; wv += wstep) {
+        uint4 v[U][4];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int64_t first = (wv * U + k) * 64;
+            const int64_t nvalid = min<int64_t>(64, max<int64_t>(0, p.nblocks - first));
+            const uint4* src = reinterpret_cast<const uint4*>(p.X) + first * 4;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int ci = 64 * c + lane;
+                v[k][c] = make_uint4(0u, 0u, 0u, 0u);
+                if ((ci >> 2) < nvalid) v[k][c] = load_nt(src + ci);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int64_t first = (wv * U + k) * 64;
+            const int64_t nvalid = min<int64_t>(64, max<int64_t>(0, p.nblocks - first));
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                uint32_t w[4] = {v[k][c].x, v[k][c].y, v[k][c].z, v[k][c].w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    w[i] ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w[i], 0xB1, 0xF, 0xF, false);  // lane ^ 1
+                    w[i] ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w[i], 0x4E, 0xF, 0xF, false);  // lane ^ 2
+                }
+                const int b = 16 * c + (lane >> 2);
+                if ((lane & 3) == 0 && b < nvalid) {
+                    *reinterpret_cast<uint4*>(p.codes + (first + b) * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+                    p.scales[first + b] = (uint8_t)(w[0] ^ w[1]);
+                }
+            }
+        }
+        if (!stride) break;
+    }
+}
+
 // element encode alone (checks of the device conversion)
 __global__ __launch_bounds__(kThreads) void e2m1_kernel(const float* __restrict__ v, int64_t npairs,
                                                        uint32_t s, uint8_t* __restrict__ codes) {
@@ -1654,6 +1701,32 @@ hipError_t launch_stream_floor(const Params& p, hipStream_t st) {
     const int64_t units = (p.nblocks + 63) / 64;
     hipLaunchKernelGGL(stream_floor_kernel, dim3((unsigned)units), dim3(64), 0, st, p);
     return hipGetLastError();
+}
+
+template <int U>
+static hipError_t launch_probe_u(const Params& p, int waves, int64_t groups, hipStream_t st) {
+    const int64_t units = (p.nblocks + 63) / 64;
+    const int64_t g = groups > 0 ? groups : (units + (int64_t)U * waves - 1) / ((int64_t)U * waves);
+    const int stride = groups > 0 ? 1 : 0;
+    const dim3 grid((unsigned)g), b(64 * waves);
+    switch (waves) {
+        case 1: hipLaunchKernelGGL((stream_probe_kernel<U, 1>), grid, b, 0, st, p, stride); break;
+        case 2: hipLaunchKernelGGL((stream_probe_kernel<U, 2>), grid, b, 0, st, p, stride); break;
+        case 4: hipLaunchKernelGGL((stream_probe_kernel<U, 4>), grid, b, 0, st, p, stride); break;
+        case 8: hipLaunchKernelGGL((stream_probe_kernel<U, 8>), grid, b, 0, st, p, stride); break;
+        case 16: hipLaunchKernelGGL((stream_probe_kernel<U, 16>), grid, b, 0, st, p, stride); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_stream_probe(const Params& p, int waves, int units, int64_t groups, hipStream_t st) {
+    switch (units) {
+        case 1: return launch_probe_u<1>(p, waves, groups, st);
+        case 2: return launch_probe_u<2>(p, waves, groups, st);
+        case 4: return launch_probe_u<4>(p, waves, groups, st);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_e2m1(const float* v, int64_t npairs, uint32_t s, uint8_t* codes, hipStream_t st) {

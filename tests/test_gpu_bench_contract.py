@@ -20,8 +20,8 @@ def _bench(*args, timeout=240):
 
 
 def test_bench_json_line():
-    r = _bench("--steps", "20", "--warmup", "20", "--no-calib", "--no-gemm", "--no-table2", "--no-large",
-               "--no-wide", "--no-cpu-baseline")
+    r = _bench("--steps", "20", "--warmup", "20", "--no-calib", "--no-gemm", "--no-table2",
+               "--configs", "tiny_256x1152,shard_4608x1536", "--no-cpu-baseline")
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [ln for ln in r.stdout.splitlines() if ln.startswith("{")]
     assert len(lines) == 1, r.stdout[-2000:]
@@ -43,4 +43,16 @@ def test_bench_json_line():
     assert d["parity"]["hot_path"].startswith("ok"), d["parity"]
     assert d["parity"]["onthefly"].startswith("ok"), d["parity"]
     assert d["parity"]["exact_path"] == "bit-exact"
+    # the single-launch ceiling: the best launch shape of the same traffic
+    c = d["single_launch_ceiling"]
+    assert c["us"] == min(c["sweep_us"].values()) and len(c["sweep_us"]) >= 10
+    assert abs(d["hot_path_frac_of_ceiling"] - c["us"] / d["kernel_us"]) < 1e-3
+    # the per-workload table: every kernel timed, its bandwidth the workload's bytes over its time
+    for name, (M, dd) in (("tiny_256x1152", (256, 1152)), ("shard_4608x1536", (4608, 1536))):
+        row = d["configs"][name]
+        assert (row["M"], row["d"]) == (M, dd) and row["algorithmic_bytes"] == M * dd * (2 + 0.5 + 1 / 32)
+        for k in ("kroquant_packed", "kroquant_onthefly", "kroquant_lu", "smoothquant", "hadamard32", "mxfp4",
+                  "stream_floor"):
+            gbs = row["algorithmic_bytes"] / row[k]["us"] * 1e-3
+            assert row[k]["us"] > 0 and abs(row[k]["gbs"] - gbs) <= 1e-3 * gbs + 0.1
 

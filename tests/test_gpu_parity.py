@@ -153,6 +153,18 @@ def test_stream_floor_outputs(M, d):
     assert np.array_equal(host(o1), ((fold[:, :, 0] ^ fold[:, :, 1]) & 0xFF).astype(np.uint8))
 
 
+@pytest.mark.parametrize("M,d", [(37, 96), (300, 3072)])
+def test_stream_probe_matches_stream_floor(M, d):
+    """kq_stream_probe (the same traffic in other launch shapes) writes what
+    kq_stream_floor writes, for one-pass and grid-stride shapes."""
+    X = synth.activations(M, d, "normal", seed=M + d)
+    Xd = dev_bf16(X)
+    f16, f1 = (host(t) for t in kq.stream_floor(Xd))
+    for waves, units, groups in ((1, 1, 0), (2, 4, 0), (16, 1, 0), (4, 2, 3), (1, 1, 5), (8, 4, 1)):
+        o16, o1 = (host(t) for t in kq.stream_probe(Xd, waves, units, groups))
+        assert np.array_equal(o16, f16) and np.array_equal(o1, f1), (waves, units, groups)
+
+
 def test_tiny_config_all_paths():
     w = synth.workload("tiny_256x1152")
     want = oracle.quantize(w.X, w.A, w.B, want_y=True)

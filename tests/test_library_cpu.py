@@ -138,6 +138,9 @@ def test_comparators_reject():
     assert L.kq_stream_floor(FAKE + 2, 4, 64, FAKE, FAKE, None) == MISALIGNED
     assert L.kq_stream_floor(FAKE, 4, 48, FAKE, FAKE, None) == INVALID
     assert L.kq_stream_floor(FAKE, 4, 64, None, FAKE, None) == NULLP
+    for w, u, g in ((3, 1, 0), (1, 3, 0), (32, 1, 0), (1, 1, -1), (1, 1, 1 << 31)):
+        assert L.kq_stream_probe(FAKE, 4, 64, FAKE, FAKE, w, u, g, None) == INVALID
+    assert L.kq_stream_probe(FAKE, 0, 64, FAKE, FAKE, 1, 1, 0, None) == SUCCESS
     assert L.kq_stream_floor(FAKE, 0, 64, FAKE, FAKE, None) == 0
     assert L.kq_e2m1_encode(FAKE, 3, 127, FAKE, None) == INVALID
     assert L.kq_e2m1_encode(FAKE, 4, 255, FAKE, None) == INVALID
