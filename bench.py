@@ -617,7 +617,8 @@ FP4_PEAK_TFLOPS = 10100.0  # MI355X dense MXFP4 matrix-core peak, TFLOP/s
 def gemm_timing(kq, synth, dev, stream, sptr, xc, xs, M, K, steps=100):
     """The W4A4 product that consumes the quantizer output (kq_mxfp4_gemm):
     the headline activation's MXFP4 codes times an MXFP4 weight from
-    kq_weight_transform (synthetic weights, N = 3072 and 12288), fp32 output."""
+    kq_weight_transform (synthetic weights, N = 3072 and 12288), fp32 output,
+    and the same product rounded to bf16 (kq_mxfp4_gemm_bf16)."""
     import torch
     out = {}
     A, B = synth.factors(4, 8, 1, seed=5)
@@ -637,9 +638,23 @@ def gemm_timing(kq, synth, dev, stream, sptr, xc, xs, M, K, steps=100):
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) / steps * 1e3
         tf = 2.0 * M * N * K / us * 1e-6
-        out[f"{M}x{N}x{K}"] = {"us": round(us, 2), "tflops": round(tf, 1),
-                                "frac_fp4_peak": round(tf / FP4_PEAK_TFLOPS, 4)}
-        del W, Wd, wc, ws, C
+        row = {"us": round(us, 2), "tflops": round(tf, 1), "frac_fp4_peak": round(tf / FP4_PEAK_TFLOPS, 4)}
+        # the same product with the output rounded to bf16 (kq_mxfp4_gemm_bf16): half the C bytes
+        C16 = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        for _ in range(10):
+            kq.mxfp4_gemm(xc, xs, wc, ws, C=C16, stream=sptr)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            kq.mxfp4_gemm(xc, xs, wc, ws, C=C16, stream=sptr)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us16 = e0.elapsed_time(e1) / steps * 1e3
+        tf16 = 2.0 * M * N * K / us16 * 1e-6
+        row["bf16_output"] = {"us": round(us16, 2), "tflops": round(tf16, 1),
+                              "frac_fp4_peak": round(tf16 / FP4_PEAK_TFLOPS, 4)}
+        out[f"{M}x{N}x{K}"] = row
+        del W, Wd, wc, ws, C, C16
     out["peak_tflops"] = FP4_PEAK_TFLOPS
     return out
 

@@ -213,6 +213,17 @@ kq_status kq_mxfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, int64_t
                         void* stream);
 
 /*
+ * kq_mxfp4_gemm_bf16 -- kq_mxfp4_gemm with the product rounded to bf16
+ * (nearest, ties to even) into C [M, ldc] (bf16 bit patterns, 2-byte
+ * aligned; ldc >= N), the layer output's 16-bit form: the same matrix-core
+ * products and fp32 accumulation, then one rounding per element, half the
+ * output bytes of the fp32 call.  No accumulate mode.  Other arguments and
+ * errors as kq_mxfp4_gemm.
+ */
+kq_status kq_mxfp4_gemm_bf16(const uint8_t* a_codes, const uint8_t* a_scales, int64_t M, const uint8_t* b_codes,
+                             const uint8_t* b_scales, int64_t N, int64_t K, uint16_t* C, int64_t ldc, void* stream);
+
+/*
  * kq_mxfp4_quantize -- the bare MXFP4 quantizer ("Q4", the lower bound of
  * Sec. 4.4): y = x, then MXFP4.
  */

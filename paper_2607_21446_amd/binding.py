@@ -22,6 +22,7 @@ STATUS = {
 EXPORTED = (
     "kq_quantize", "kq_quantize_exact", "kq_quantize_packed", "kq_pack_factors", "kq_quantize_lu",
     "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_fwht_quantize", "kq_mxfp4_quantize", "kq_mxfp4_gemm",
+    "kq_mxfp4_gemm_bf16",
     "kq_stream_floor", "kq_stream_probe",
     "kq_e2m1_encode", "kq_weight_transform", "kq_factors_inverse_transpose", "kq_lu_to_factors",
     "kq_calib_workspace_size", "kq_calib_reference", "kq_calib_step", "kq_calibrate",
@@ -55,6 +56,7 @@ def lib() -> ctypes.CDLL:
     L.kq_hadamard32_quantize.argtypes = [P, I64, I64, P, P, P, P]
     L.kq_fwht_quantize.argtypes = [P, I64, I64, P, P, P, P]
     L.kq_mxfp4_gemm.argtypes = [P, P, I64, P, P, I64, I64, P, I64, I, P]
+    L.kq_mxfp4_gemm_bf16.argtypes = [P, P, I64, P, P, I64, I64, P, I64, P]
     L.kq_mxfp4_quantize.argtypes = [P, I64, I64, P, P, P]
     L.kq_stream_floor.argtypes = [P, I64, I64, P, P, P]
     L.kq_stream_probe.argtypes = [P, I64, I64, P, P, I, I, I64, P]
@@ -67,7 +69,7 @@ def lib() -> ctypes.CDLL:
     L.kq_calib_step.argtypes = [P, I64, I64, P, I64, P, P, I, I64, P, P, P, P, P, I, F, P, ctypes.c_size_t, P]
     L.kq_calibrate.argtypes = [P, I64, I64, P, I64, P, P, I, I64, I, F, P, P, ctypes.c_size_t, P]
     L.kq_calib_step_noalloc.argtypes = [P, I64, I64, P, I64, P, P, I, I64, P, P, P, P, P, I, F, P]
-    for name in EXPORTED[:21]:
+    for name in EXPORTED[:22]:
         getattr(L, name).restype = ctypes.c_int
     L.kq_status_string.argtypes = [I]
     L.kq_status_string.restype = ctypes.c_char_p
@@ -268,9 +270,11 @@ def fwht(X, codes=None, scales=None, y=None, want_y=False, stream=None):
     return codes, scales, y
 
 
-def mxfp4_gemm(a_codes, a_scales, b_codes, b_scales, C=None, accumulate=False, stream=None):
+def mxfp4_gemm(a_codes, a_scales, b_codes, b_scales, C=None, accumulate=False, stream=None, out_dtype=None):
     """kq_mxfp4_gemm: C[M, N] (+)= deq(A) deq(B)^T for MXFP4 operands (codes
-    uint8 [rows, K/2], scales uint8 [rows, K/32]).  Returns C (fp32)."""
+    uint8 [rows, K/2], scales uint8 [rows, K/32]).  Returns C (fp32; with
+    out_dtype=torch.bfloat16 or a bf16 C, kq_mxfp4_gemm_bf16: the product
+    rounded to bf16, no accumulate)."""
     for t, name in ((a_codes, "a_codes"), (a_scales, "a_scales"), (b_codes, "b_codes"), (b_scales, "b_scales")):
         _need(t, torch.uint8, name)
     _matrix(a_codes, "a_codes")
@@ -282,10 +286,17 @@ def mxfp4_gemm(a_codes, a_scales, b_codes, b_scales, C=None, accumulate=False, s
     if any(t.device != dev for t in (a_scales, b_codes, b_scales)):
         raise ValueError("all operands must be on one device")
     if C is None:
-        C = torch.empty((M, N), dtype=torch.float32, device=dev)
-    _need(C, torch.float32, "C")
+        C = torch.empty((M, N), dtype=out_dtype or torch.float32, device=dev)
     if tuple(C.shape) != (M, N) or C.device != dev:
         raise ValueError(f"C must be [{M}, {N}] on {dev}, got {tuple(C.shape)} on {C.device}")
+    if C.dtype == torch.bfloat16:
+        _need(C, torch.bfloat16, "C")
+        if accumulate:
+            raise ValueError("the bf16 output has no accumulate mode")
+        _check(lib().kq_mxfp4_gemm_bf16(_ptr(a_codes), _ptr(a_scales), M, _ptr(b_codes), _ptr(b_scales), N, K, _ptr(C),
+                                        C.stride(0), _stream(stream)), "kq_mxfp4_gemm_bf16")
+        return C
+    _need(C, torch.float32, "C")
     _check(lib().kq_mxfp4_gemm(_ptr(a_codes), _ptr(a_scales), M, _ptr(b_codes), _ptr(b_scales), N, K, _ptr(C),
                                C.stride(0), int(accumulate), _stream(stream)), "kq_mxfp4_gemm")
     return C

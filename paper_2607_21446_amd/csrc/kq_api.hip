@@ -328,9 +328,9 @@ static kq::GemmParams gemm_params(const uint8_t* a_codes, const uint8_t* a_scale
     return g;
 }
 
-kq_status kq_mxfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, int64_t M, const uint8_t* b_codes,
-                        const uint8_t* b_scales, int64_t N, int64_t K, float* C, int64_t ldc, int accumulate,
-                        void* stream) {
+static kq_status check_gemm(const uint8_t* a_codes, const uint8_t* a_scales, int64_t M, const uint8_t* b_codes,
+                            const uint8_t* b_scales, int64_t N, int64_t K, const void* C, int64_t ldc, int accumulate,
+                            size_t c_align) {
     if (M < 0 || N < 0) return fail(KQ_ERROR_INVALID_VALUE, "M = %lld and N = %lld must be >= 0", (long long)M, (long long)N);
     if (K <= 0 || K % 32 != 0) return fail(KQ_ERROR_INVALID_VALUE, "K = %lld must be a positive multiple of 32", (long long)K);
     if (ldc < N) return fail(KQ_ERROR_INVALID_VALUE, "ldc = %lld must be >= N = %lld", (long long)ldc, (long long)N);
@@ -341,9 +341,27 @@ kq_status kq_mxfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, int64_t
     if (!a_codes || !a_scales || !b_codes || !b_scales || !C)
         return fail(KQ_ERROR_NULL_POINTER, "codes, scales and C must not be NULL");
     if (!aligned(a_codes, 16) || !aligned(b_codes, 16)) return fail(KQ_ERROR_MISALIGNED, "codes must be 16-byte aligned");
-    if (!aligned(C, 4)) return fail(KQ_ERROR_MISALIGNED, "C must be 4-byte aligned");
+    if (!aligned(C, c_align)) return fail(KQ_ERROR_MISALIGNED, "C must be %zu-byte aligned", c_align);
+    return ok();
+}
+
+kq_status kq_mxfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, int64_t M, const uint8_t* b_codes,
+                        const uint8_t* b_scales, int64_t N, int64_t K, float* C, int64_t ldc, int accumulate,
+                        void* stream) {
+    const kq_status st = check_gemm(a_codes, a_scales, M, b_codes, b_scales, N, K, C, ldc, accumulate, 4);
+    if (st != KQ_SUCCESS || M == 0 || N == 0) return st;
     const kq::GemmParams g = gemm_params(a_codes, a_scales, M, b_codes, b_scales, N, K, C, ldc, accumulate, nullptr);
     return from_hip(kq::launch_mxfp4_gemm(g, (hipStream_t)stream), "kq_mxfp4_gemm");
+}
+
+kq_status kq_mxfp4_gemm_bf16(const uint8_t* a_codes, const uint8_t* a_scales, int64_t M, const uint8_t* b_codes,
+                             const uint8_t* b_scales, int64_t N, int64_t K, uint16_t* C, int64_t ldc, void* stream) {
+    const kq_status st = check_gemm(a_codes, a_scales, M, b_codes, b_scales, N, K, C, ldc, 0, 2);
+    if (st != KQ_SUCCESS || M == 0 || N == 0) return st;
+    kq::GemmParams g = gemm_params(a_codes, a_scales, M, b_codes, b_scales, N, K, nullptr, ldc, 0, nullptr);
+    g.C16 = C;
+    g.vec_ok = aligned(C, 8) && ldc % 4 == 0;
+    return from_hip(kq::launch_mxfp4_gemm(g, (hipStream_t)stream), "kq_mxfp4_gemm_bf16");
 }
 
 kq_status kq_mxfp4_quantize(const uint16_t* X, int64_t M, int64_t d, uint8_t* codes, uint8_t* scales,

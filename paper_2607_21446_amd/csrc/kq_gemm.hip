@@ -56,6 +56,39 @@ __device__ __forceinline__ i32x8 operand(const Frag& f) {
     return v;
 }
 
+// Four consecutive C values of row m from column n: fp32 (with the bias or
+// the accumulate mode), or rounded to bf16 (nearest even) when C16 is set.
+__device__ __forceinline__ void store_c4(const GemmParams& g, int64_t m, int64_t n, float4 v) {
+    if (g.C16) {
+        uint16_t* crow = g.C16 + m * g.ldc_out;
+        const float f[4] = {v.x, v.y, v.z, v.w};
+        if (g.vec_ok && n + 3 < g.N) {
+            typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+            const bf16x4 b = {(__bf16)v.x, (__bf16)v.y, (__bf16)v.z, (__bf16)v.w};
+            *reinterpret_cast<uint2*>(crow + n) = __builtin_bit_cast(uint2, b);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (n + e < g.N) crow[n + e] = __builtin_bit_cast(uint16_t, (__bf16)f[e]);
+        }
+        return;
+    }
+    float* crow = g.C + m * g.ldc_out;
+    const float* brow = g.bias ? g.bias + m * g.ldc_out : g.accumulate ? crow : nullptr;
+    if (g.vec_ok && n + 3 < g.N) {
+        if (brow) {
+            const float4 o = *reinterpret_cast<const float4*>(brow + n);
+            v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
+        }
+        *reinterpret_cast<float4*>(crow + n) = v;
+    } else {
+        if (n + 0 < g.N) crow[n + 0] = brow ? brow[n + 0] + v.x : v.x;
+        if (n + 1 < g.N) crow[n + 1] = brow ? brow[n + 1] + v.y : v.y;
+        if (n + 2 < g.N) crow[n + 2] = brow ? brow[n + 2] + v.z : v.z;
+        if (n + 3 < g.N) crow[n + 3] = brow ? brow[n + 3] + v.w : v.w;
+    }
+}
+
 }  // namespace
 
 __global__ __launch_bounds__(256) void mxfp4_gemm_kernel(const GemmParams g) {
@@ -110,6 +143,10 @@ __global__ __launch_bounds__(256) void mxfp4_gemm_kernel(const GemmParams g) {
                 for (int e = 0; e < 4; ++e) {
                     const int64_t row = m0 + 32 * i + 8 * q + 4 * h + e;
                     if (row >= g.M) continue;
+                    if (g.C16) {
+                        g.C16[row * g.ldc_out + col] = __builtin_bit_cast(uint16_t, (__bf16)acc[i][j][4 * q + e]);
+                        continue;
+                    }
                     float* dst = g.C + row * g.ldc_out + col;
                     const float base = g.bias ? g.bias[row * g.ldc_out + col] : g.accumulate ? *dst : 0.0f;
                     *dst = (g.bias || g.accumulate) ? base + acc[i][j][4 * q + e] : acc[i][j][4 * q + e];
@@ -270,27 +307,12 @@ __global__ __launch_bounds__(256) void mxfp4_gemm_pipe_kernel(const GemmParams g
     for (int j = 0; j < 2; ++j) {
         const int64_t m = mb0 + wm * 64 + 32 * j + r;
         if (m >= g.M) continue;
-        float* crow = g.C + m * g.ldc_out;
-        const float* brow = g.bias ? g.bias + m * g.ldc_out : g.accumulate ? crow : nullptr;
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int64_t n = nb0 + wn * 64 + 32 * i + 8 * q + 4 * h;
-                float4 v = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-                if (g.vec_ok && n + 3 < g.N) {
-                    if (brow) {
-                        const float4 o = *reinterpret_cast<const float4*>(brow + n);
-                        v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
-                    }
-                    *reinterpret_cast<float4*>(crow + n) = v;
-                } else {
-                    if (n + 0 < g.N) crow[n + 0] = brow ? brow[n + 0] + v.x : v.x;
-                    if (n + 1 < g.N) crow[n + 1] = brow ? brow[n + 1] + v.y : v.y;
-                    if (n + 2 < g.N) crow[n + 2] = brow ? brow[n + 2] + v.z : v.z;
-                    if (n + 3 < g.N) crow[n + 3] = brow ? brow[n + 3] + v.w : v.w;
-                }
-            }
+            for (int q = 0; q < 4; ++q)
+                store_c4(g, m, nb0 + wn * 64 + 32 * i + 8 * q + 4 * h,
+                         make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]));
     }
 }
 
@@ -397,27 +419,12 @@ __device__ __forceinline__ void big_store(const GemmParams& g, const PipeCtx& c,
     for (int j = 0; j < 2; ++j) {
         const int64_t m = c.mb0 + wm * 64 + 32 * j + r;
         if (m >= g.M) continue;
-        float* crow = g.C + m * g.ldc_out;
-        const float* brow = g.bias ? g.bias + m * g.ldc_out : g.accumulate ? crow : nullptr;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int64_t n = c.nb0 + wn * 128 + 32 * i + 8 * q + 4 * h;
-                float4 v = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-                if (g.vec_ok && n + 3 < g.N) {
-                    if (brow) {
-                        const float4 o = *reinterpret_cast<const float4*>(brow + n);
-                        v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
-                    }
-                    *reinterpret_cast<float4*>(crow + n) = v;
-                } else {
-                    if (n + 0 < g.N) crow[n + 0] = brow ? brow[n + 0] + v.x : v.x;
-                    if (n + 1 < g.N) crow[n + 1] = brow ? brow[n + 1] + v.y : v.y;
-                    if (n + 2 < g.N) crow[n + 2] = brow ? brow[n + 2] + v.z : v.z;
-                    if (n + 3 < g.N) crow[n + 3] = brow ? brow[n + 3] + v.w : v.w;
-                }
-            }
+            for (int q = 0; q < 4; ++q)
+                store_c4(g, m, c.nb0 + wn * 128 + 32 * i + 8 * q + 4 * h,
+                         make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]));
     }
 }
 

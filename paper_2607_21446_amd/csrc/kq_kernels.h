@@ -52,7 +52,8 @@ struct GemmParams {
     int64_t ldc_out;
     int accumulate;           // 1: C += product, 0: C = product
     const float* bias = nullptr;  // if set: C = bias + product (bias [M, ldc_out], vec rule as C)
-    int vec_ok;               // C 16-byte aligned and ldc_out a multiple of 4
+    uint16_t* C16 = nullptr;      // if set: bf16 output [M, ldc_out] instead of C (no bias, no accumulate)
+    int vec_ok;               // C 16-byte (C16 8-byte) aligned and ldc_out a multiple of 4
     int scales_aligned;       // both scale arrays 4-byte aligned
 };
 

@@ -523,6 +523,27 @@ def test_mxfp4_gemm_parity(M, N, K):
     assert np.all(np.abs(host(Cd) - (ref + C0)) <= tol + 2.0 ** -23 * np.abs(ref + C0))
 
 
+@pytest.mark.parametrize("M,N,K", [(77, 200, 2240), (33, 70, 1120), (300, 257, 3072), (5, 3, 128), (3000, 2200, 384),
+                                   (2500, 2470, 1664)])
+def test_mxfp4_gemm_bf16_output(M, N, K):
+    """kq_mxfp4_gemm_bf16: the fp32 call's product rounded to bf16 (nearest
+    even) element by element -- the same matrix-core sums, one rounding --
+    and so within half a bf16 step of the oracle product plus the fp32
+    accumulation bound; every kernel the dispatcher picks (small, 128 x 128
+    and 256 x 256 tiles, ragged edges)."""
+    ac, as_ = _rand_mx(M, K, seed=M + 3 * K)
+    bc, bs = _rand_mx(N, K, seed=N + 5 * K)
+    t = lambda a: torch.from_numpy(a).cuda()
+    C32 = kq.mxfp4_gemm(t(ac), t(as_), t(bc), t(bs))
+    C16 = kq.mxfp4_gemm(t(ac), t(as_), t(bc), t(bs), out_dtype=torch.bfloat16)
+    c16 = host(C16.view(torch.int16)).view(np.uint16)
+    assert np.array_equal(c16, oracle.f32_to_bf16(host(C32)))
+    ref = oracle.mxfp4_gemm(ac, as_, bc, bs)
+    tol = _gemm_tolerance(ac, as_, bc, bs)
+    got = oracle.bf16_to_f32(c16).astype(np.float64)
+    assert np.all(np.abs(got - ref) <= 2.0 ** -8 * (np.abs(ref) + tol) + tol)
+
+
 def test_w4a4_layer_end_to_end():
     """X -> kq_quantize_packed, W -> kq_weight_transform, then kq_mxfp4_gemm:
     the layer output against the oracle's W4A4 product, and E(T) (Sec. 3.1)

@@ -126,6 +126,13 @@ def test_mxfp4_gemm_rejects():
     assert g(ac=None) == NULLP and g(C=None) == NULLP
     assert g(ac=FAKE + 8) == MISALIGNED and g(C=FAKE + 2) == MISALIGNED
     assert g(M=0) == SUCCESS and g(N=0, ldc=0) == SUCCESS
+    h = lambda **kw: L.kq_mxfp4_gemm_bf16(kw.get("ac", FAKE), kw.get("as_", FAKE), kw.get("M", 4), kw.get("bc", FAKE),
+                                          kw.get("bs", FAKE), kw.get("N", 4), kw.get("K", 64), kw.get("C", FAKE),
+                                          kw.get("ldc", 4), None)
+    assert h(K=48) == INVALID and h(ldc=3) == INVALID and h(M=-1) == INVALID
+    assert h(bs=None) == NULLP and h(C=None) == NULLP
+    assert h(bc=FAKE + 4) == MISALIGNED and h(C=FAKE + 1) == MISALIGNED
+    assert h(M=0) == SUCCESS and h(N=0, ldc=0) == SUCCESS
 
 
 def test_comparators_reject():
