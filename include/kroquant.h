@@ -117,6 +117,9 @@ kq_status kq_pack_factors(const float* A, const float* B, int a, int b, int64_t 
  * (identical scales, codes within tie flips, y within the stated bound); the
  * edge window is 2^-17 cond_inf(A (x) B) amax here, taken from the pack,
  * instead of a per-block bound, so the set of re-evaluated blocks can differ.
+ * With per-block factors (nfac = d/32) the pack is not read: every pair's K
+ * is rebuilt on chip from its 320 bytes of A and B, which costs less than
+ * reading its 6160-byte pack, and the result is exactly kq_quantize's.
  */
 kq_status kq_quantize_packed(const uint16_t* X, int64_t M, int64_t d, const float* A,
                              const float* B, int a, int b, int64_t nfac, const void* kpack,

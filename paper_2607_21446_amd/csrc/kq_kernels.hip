@@ -1049,10 +1049,12 @@ __global__ __launch_bounds__(256) void kron_build_unit_kernel(const Params p) {
 // each row of a step is 512 contiguous bytes of X, 128 of codes and 8 of
 // scales (one wave per 64-byte piece of 64 rows would touch a different cache
 // line per row in every load and store).  Wave w owns column block 8 j + w of
-// the strip and keeps its K in registers for all the strip's steps: read from
-// the pack (PACKED), or built by each lane from its rows of A and B, which the
-// wave stages in LDS (loaded, or decoded from the 15 parameters of G_1..G_5
-// when LU), with the window 2^-17 ||K||_inf max|x|.  A step: wave w loads rows
+// the strip and keeps its K in registers for all the strip's steps, built by
+// each lane from its rows of A and B, which the wave stages in LDS (loaded,
+// or decoded from the 15 parameters of G_1..G_5 when LU), with the window
+// 2^-17 ||K||_inf max|x|.  (With a pair per block, building K from the 320
+// bytes of A and B is cheaper than reading its 6 KiB pack: the pack would add
+// 19-37% to a strip's input bytes.)  A step: wave w loads rows
 // 8 w .. 8 w + 7 (two rows per 1 KiB load) and writes each 16-byte chunk to
 // the LDS tile of the wave that owns its column block, then issues the next
 // step's loads; after a barrier each wave runs the unit body on its column
@@ -1073,7 +1075,7 @@ constexpr int kTileSlots = 260;
 constexpr int kCodeSlots = 68;  // 64 blocks x 16 code bytes, then 64 scale bytes
 constexpr int kTileMaxSteps = 8;
 
-template <int NA, int NB, bool PACKED, bool LU, bool WY, bool WY16>
+template <int NA, int NB, bool LU, bool WY, bool WY16>
 __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params p, int rg) {
     constexpr int NF = NA * NA + NB * NB;
     constexpr int FPL = (NF + 63) / 64;  // factor entries per lane
@@ -1081,7 +1083,7 @@ __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params 
     __shared__ uint4 lds_c[kTileCols * kCodeSlots];
     __shared__ uint64_t stmask[kTileCols];
     __shared__ uint64_t sedges[kTileCols][kTileMaxSteps];
-    __shared__ float fac[PACKED ? 1 : kTileCols * NF];  // each wave's A then B
+    __shared__ float fac[kTileCols * NF];  // each wave's A then B
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int64_t ntc = (p.nb + kTileCols - 1) / kTileCols;
     const int64_t nrb = (p.M + 63) / 64;
@@ -1095,8 +1097,8 @@ __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params 
     // K from the factors: this wave's A and B are staged in its LDS area,
     // loaded first (coalesced; loads retire in order, so waiting for them does
     // not wait for the input) or, LU, decoded there from the 15 parameters
-    float fv[PACKED || LU ? 1 : FPL];
-    if (!PACKED && !LU) {
+    float fv[LU ? 1 : FPL];
+    if (!LU) {
 #pragma unroll
         for (int q = 0; q < FPL; ++q) {
             // unconditional (clamped index), so no branch hides the load from the wait counting
@@ -1130,10 +1132,8 @@ __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params 
     EdgeTest et;
     const float* Af = p.A + f * (NA * NA);
     const float* Bf = p.B + f * (NB * NB);
-    if (PACKED) {
-        packed_k(p, f, ks, zero_ok, et);
-    } else {
-        float* const facw = fac + (PACKED ? 0 : w * NF);
+    {
+        float* const facw = fac + w * NF;
         if (LU) {
             float gm[5][4];
             lu_g(p.lu + f * 15, gm);
@@ -1188,7 +1188,7 @@ __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params 
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
         if (active)
-            unit_compute<Mapping::Column, NA, NB, false, WY, WY16, false, PACKED, true>(
+            unit_compute<Mapping::Column, NA, NB, false, WY, WY16, false, false, true>(
                 p, lds_x + kTileSlots * w, row0 * p.nb + jc, nrows, (uint32_t)p.nb, v, ks, zero_ok, et, Af, Bf,
                 TileSink{lds_c + kCodeSlots * w, &stmask[w], &sedges[w][it]});
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
@@ -1551,13 +1551,13 @@ static hipError_t launch_unit(const Params& p, int64_t units, bool ilv, hipStrea
     return hipGetLastError();
 }
 
-// Per-block factors: the 8-column tile kernel (K from the pack or built per wave).
-template <int NA, int NB, bool PACKED, bool LU>
+// Per-block factors: the 8-column tile kernel (K built per wave).
+template <int NA, int NB, bool LU>
 static hipError_t launch_tile(const Params& p, int rg, hipStream_t st) {
     const int64_t nrb = (p.M + 63) / 64, ntc = (p.nb + kTileCols - 1) / kTileCols;
     const dim3 g((unsigned)(((nrb + rg - 1) / rg) * ntc)), b(64 * kTileCols);
     const bool wy = p.y != nullptr, wy16 = LU && p.y16 != nullptr;
-#define KQ_TILE(WY, WY16) hipLaunchKernelGGL((kron_tile_kernel<NA, NB, PACKED, LU, WY, WY16>), g, b, 0, st, p, rg)
+#define KQ_TILE(WY, WY16) hipLaunchKernelGGL((kron_tile_kernel<NA, NB, LU, WY, WY16>), g, b, 0, st, p, rg)
     if (wy16) { if (wy) KQ_TILE(true, LU); else KQ_TILE(false, LU); }
     else { if (wy) KQ_TILE(true, false); else KQ_TILE(false, false); }
 #undef KQ_TILE
@@ -1565,13 +1565,11 @@ static hipError_t launch_tile(const Params& p, int rg, hipStream_t st) {
 }
 
 // Row blocks per strip of the tile kernel (1 .. kTileMaxSteps): as many as
-// keep at least ~1728 workgroups when each wave builds its K (about three
-// rounds of the 512 that fit at once: more steps amortise the build) and
-// ~3456 when K comes from the pack (only its load to amortise, so a shorter
-// last round matters more).
+// keep at least ~1728 workgroups (about three rounds of the 512 that fit at
+// once: more steps amortise each wave's K build).
 static int tile_rows(const Params& p) {
     const int64_t tiles = ((p.M + 63) / 64) * ((p.nb + kTileCols - 1) / kTileCols);
-    const int64_t rg = tiles / (p.kpack ? 3456 : 1728);
+    const int64_t rg = tiles / 1728;
     return rg < 1 ? 1 : rg > kTileMaxSteps ? kTileMaxSteps : (int)rg;
 }
 
@@ -1593,17 +1591,15 @@ static hipError_t launch_build(const Params& p, Mapping map, hipStream_t st) {
     return hipGetLastError();
 }
 
-// Per-block factors (COLUMN mapping) run on the 8-column tile kernel; shared
+// Per-block factors (COLUMN mapping) run on the 8-column tile kernel, which
+// builds each pair's K from A and B even when a pack is given; shared
 // factors on one 64-block unit per wave, K from the pack (the two tiles'
 // products interleaved on grids of at most kInterleaveMaxUnits units, where
 // fewer waves per SIMD hide less latency) or built per 4-wave workgroup.
-// The caller has checked that every grid fits (kq_max_units).
+// The API layer has checked that every grid fits one launch.
 template <int NA, int NB>
 static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st) {
-    if (map == Mapping::Column) {
-        if (p.kpack) return launch_tile<NA, NB, true, false>(p, tile_rows(p), st);
-        return launch_tile<NA, NB, false, false>(p, tile_rows(p), st);
-    }
+    if (map == Mapping::Column) return launch_tile<NA, NB, false>(p, tile_rows(p), st);  // the pack is not read
     const int64_t units = (p.nblocks + 63) / 64;
     if (p.kpack) return launch_unit<Mapping::Flat, NA, NB>(p, units, units <= kInterleaveMaxUnits, st);
     return launch_build<NA, NB, false>(p, map, st);
@@ -1611,7 +1607,7 @@ static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st) {
 
 template <int NA, int NB>
 static hipError_t launch_lu(const Params& p, Mapping map, hipStream_t st) {
-    if (map == Mapping::Column) return launch_tile<NA, NB, false, true>(p, tile_rows(p), st);
+    if (map == Mapping::Column) return launch_tile<NA, NB, true>(p, tile_rows(p), st);
     return launch_build<NA, NB, true>(p, map, st);
 }
 
