@@ -77,6 +77,10 @@ def parse():
                     help="turn the FETCH_SIZE / WRITE_SIZE counter runs under DIR (DIR/<kernel>/p3, p4 from "
                          "rocprofv3 --pmc, kernels 'kroquant' and 'copy') into the traffic record read by the "
                          "roofline field; needs no GPU")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="summarize a rocprofv3 --kernel-trace run under DIR (per kernel and grid: calls and duration "
+                         "statistics, and for every group of at least 4000 launches the windows of dispatches "
+                         "2001-3000 and 3001-4000, the headline's first and timed graph replays); needs no GPU")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")
     ap.add_argument("--no-gemm", action="store_true", help="skip the W4A4 MXFP4 GEMM consumer timing")
@@ -141,10 +145,48 @@ def summarize_pmc(root, workload):
     print(json.dumps(rec, indent=1))
 
 
+def summarize_trace(root):
+    """Kernel durations from a rocprofv3 kernel trace, grouped by kernel name
+    and grid size, in launch order (markdown on stdout)."""
+    import csv
+    import glob
+    import statistics
+    rows = []
+    for f in glob.glob(os.path.join(root, "**", "*kernel_trace.csv"), recursive=True):
+        with open(f) as fh:
+            rows.extend(csv.DictReader(fh))
+    if not rows:
+        raise SystemExit(f"no kernel trace under {root}")
+    gcol = [c for c in rows[0] if c.startswith("Grid_Size")]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    groups = {}
+    for r in rows:
+        key = (r["Kernel_Name"], "x".join(r[c] for c in gcol))
+        groups.setdefault(key, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0)
+
+    def stats(v):
+        s = sorted(v)
+        q = lambda p: s[min(len(s) - 1, int(p * len(s)))]
+        return f"{statistics.mean(v):.3f} | {statistics.median(v):.3f} | {q(0.1):.3f} | {q(0.9):.3f}"
+
+    print(f"{len(rows)} dispatches\n")
+    print("| kernel | grid (work-items) | calls | mean us | median us | p10 | p90 |\n|---|---|---|---|---|---|---|")
+    for (k, grid), v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        print(f"| `{k}` | {grid} | {len(v)} | {stats(v)} |")
+    print("\nwindows (launch order within a kernel and grid):\n")
+    for (k, grid), v in groups.items():
+        if len(v) >= 4000:
+            for a, b in ((2001, 3000), (3001, 4000)):
+                print(f"- `{k}` grid {grid}, launches {a}-{b}: mean | median | p10 | p90 = {stats(v[a - 1:b])} us")
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
         summarize_pmc(args.summarize_pmc, args.workload)
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this quantizer benchmark runs on exactly one GPU (--gpus 1); the quantizer "
