@@ -14,8 +14,12 @@ variant (K2, kq_quantize) and the fixed-order VALU variant are timed too.
   enough distinct input/output buffer sets that their footprint exceeds twice
   the 256 MB last-level (MALL) cache, so every step streams from HBM.
 * Time: after W warmup steps, exactly K back-to-back steps are captured into a
-  HIP graph (outside the timed region) and the graph is replayed once between
-  HIP events on the launch stream; value = algorithmic bytes (2 B bf16 in +
+  HIP graph (outside the timed region) behind W more warmup launches and
+  between two stamps of the device's 100 MHz real-time counter
+  (kq_timestamp); the graph is replayed once between synchronizations and the
+  stamp difference times exactly the K launches (HIP events around the whole
+  replay, which also hold the fixed cost of launching a graph, are reported
+  beside it); value = algorithmic bytes (2 B bf16 in +
   0.5 B codes + 1/32 B scale per element) / time per step.  One Python-side
   launch through ctypes costs about as much host time as the whole kernel
   (~7 us), so the same K launches from the Python loop are reported beside it
@@ -305,18 +309,31 @@ def main():
         wall = time.perf_counter() - t0
         return e0.elapsed_time(e1) / steps, wall
 
-    def timed(fn, steps, warmup, rotate=True):
+    stamps = torch.zeros(2, dtype=torch.int64, device=dev)
+    replay_us = {}
+
+    def timed(fn, steps, warmup, rotate=True, name=None):
         """K launches captured once into a HIP graph before the timed region
-        (same kernels, arguments and buffer rotation as the eager loop), then
-        one replay between HIP events on the launch stream: the GPU time of
-        exactly K back-to-back steps, without the host's per-call cost."""
+        (same kernels, arguments and buffer rotation as the eager loop), behind
+        the W warmup launches and between two device stamps of the 100 MHz
+        real-time counter (kq_timestamp); one replay between
+        torch.cuda.synchronize() calls.  The time per step is the stamp
+        difference over K: exactly the K back-to-back launches, without the
+        host's per-call cost and without the fixed cost of launching the graph
+        (which, spread over a short K, would read as a slower step).  HIP
+        events around the same replay (warmup steps and graph launch included)
+        are kept beside it in `replay_us`."""
         for i in range(warmup):
             fn(i % nsets if rotate else 0)
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
+            for i in range(warmup):
+                fn((steps + i) % nsets if rotate else 0)
+            kq.timestamp(stamps, 0)
             for i in range(steps):
                 fn(i % nsets if rotate else 0)
+            kq.timestamp(stamps, 1)
         g.replay()  # untimed: first replay uploads the graph
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
@@ -328,7 +345,11 @@ def main():
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         del g
-        return e0.elapsed_time(e1) / steps, wall
+        t = stamps.cpu().numpy()
+        ms = (int(t[1]) - int(t[0])) / kq.TIMESTAMP_HZ * 1e3 / steps
+        if name:
+            replay_us[name] = round(e0.elapsed_time(e1) * 1e3 / (steps + warmup), 3)
+        return ms, wall
 
     def per_launch(fn, n=200):
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
@@ -342,7 +363,7 @@ def main():
                 "p90_us": round(float(np.percentile(t, 90)), 3)}
 
     # timed region: exactly K steps of the hot path, after W warmup steps
-    ms_kq, wall_kq = timed(run_kq, args.steps, args.warmup)
+    ms_kq, wall_kq = timed(run_kq, args.steps, args.warmup, name="kroquant")
     us_kq = ms_kq * 1e3
     ms_kq_eager, _ = timed_eager(run_kq, args.steps, args.warmup)
     gbs = nbytes / (ms_kq * 1e-3) / 1e9
@@ -350,11 +371,11 @@ def main():
     comparators = {}
     for name in ("kroquant_onthefly", "kroquant_lu", "kroquant_exact", "smoothquant", "hadamard32", "mxfp4",
                  "stream_floor"):
-        ms, _ = timed(runs[name], args.steps, args.warmup)
+        ms, _ = timed(runs[name], args.steps, args.warmup, name=name)
         comparators[name + "_us"] = round(ms * 1e3, 3)
         comparators[name + "_gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
     ms_floor_eager, _ = timed_eager(run_floor, args.steps, args.warmup)
-    ceiling = launch_sweep(kq, Xs, Cs, Ss, nsets, args.steps, nbytes, stream)
+    ceiling = launch_sweep(kq, Xs, Cs, Ss, nsets, int(min(2000, max(30, 20e9 // nbytes))), nbytes, stream)
     ms_warm, _ = timed(run_kq, args.steps, args.warmup, rotate=False)
     # the vendor's device-to-device copy moving the same HBM bytes as one step
     # (half of them read, half written), with the same rotation
@@ -425,8 +446,12 @@ def main():
         "path": "kq_quantize_packed: matrix cores (v_mfma_f32_32x32x16_bf16, 3-term bf16 split of the "
                 "materialised A(x)B packed offline)",
         "comparators": comparators,
-        "timing": "value: HIP graph of the K launches (captured before the timed region), one replay between HIP "
-                  "events; eager_python: the same K launches from the Python loop (ctypes call per step)",
+        "timing": "value: the K launches captured into a HIP graph (before the timed region) behind the W warmup "
+                  "launches and between two kq_timestamp stamps of the 100 MHz device counter; one replay between "
+                  "synchronizations, time per step = stamp difference / K. replay_events_us_per_launch: HIP events "
+                  "around that replay (the W warmup steps and the graph launch included) / (W + K); eager_python: "
+                  "the same K launches from the Python loop (ctypes call per step)",
+        "replay_events_us_per_launch": replay_us,
         "eager_python": {"kroquant_us": round(ms_kq_eager * 1e3, 3), "stream_floor_us": round(ms_floor_eager * 1e3, 3)},
         "per_launch_events": dist,
         "warm_single_buffer": {"us": round(ms_warm * 1e3, 3), "gbs": round(nbytes / (ms_warm * 1e-3) / 1e9, 1)},
@@ -485,27 +510,31 @@ def _config_inputs(name, synth, dev, cache):
 
 def _graph_us(fn, nsets, steps, stream):
     """Per-launch time of `steps` launches of fn(i % nsets) captured once into
-    a HIP graph: 3 untimed replays, then the median of 3 replays between HIP
-    events on the launch stream."""
+    a HIP graph between two kq_timestamp stamps of the 100 MHz device counter:
+    3 untimed replays, then the median of 3 replays of (stamp difference) /
+    steps -- the launches alone, without the fixed cost of launching the
+    graph."""
     import torch
+    import paper_2607_21446_amd as kq
+    stamps = torch.zeros(2, dtype=torch.int64, device="cuda")
     for i in range(nsets):  # eager pass over every set
         fn(i)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
+        kq.timestamp(stamps, 0)
         for i in range(steps):
             fn(i % nsets)
+        kq.timestamp(stamps, 1)
     for _ in range(3):  # untimed: upload, then clocks settle
         g.replay()
     torch.cuda.synchronize()
     ts = []
     for _ in range(3):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
         g.replay()
-        e1.record(stream)
         torch.cuda.synchronize()
-        ts.append(e0.elapsed_time(e1) / steps * 1e3)
+        t = stamps.cpu().numpy()
+        ts.append((int(t[1]) - int(t[0])) / kq.TIMESTAMP_HZ * 1e6 / steps)
     del g
     return float(np.median(ts))
 
@@ -582,22 +611,22 @@ def config_table(kq, synth, dev, stream, names=CONFIG_WORKLOADS, graph_bytes=20e
         torch.cuda.empty_cache()
     cache.pop("large_X", None)
     torch.cuda.empty_cache()
-    out["timing"] = ("per kernel: a HIP graph of `steps` launches over MALL-cold rotating buffer sets, replayed 3 "
-                     "times untimed, then the median of 3 replays between HIP events; vs_smoothquant = SmoothQuant "
-                     "time / this kernel's time")
+    out["timing"] = ("per kernel: a HIP graph of `steps` launches over MALL-cold rotating buffer sets between two "
+                     "kq_timestamp stamps, replayed 3 times untimed, then the median of 3 replays of the stamp "
+                     "difference / steps; vs_smoothquant = SmoothQuant time / this kernel's time")
     return out
 
 
 TABLE2_SHAPES = [(4096, 1024), (4096, 4096), (4096, 16384), (512, 4096), (512, 16384)]
 
 
-def table2_shapes(kq, synth, dev, stream, sptr, steps=500, warmup=3):
+def table2_shapes(kq, synth, dev, stream, sptr, steps=500):
     """The paper's power-of-two-d comparison (Sec. 4.4, Table 2): Q4, Scale
     (SmoothQuant), K1 (kq_quantize_packed), K2 (kq_quantize_lu, 15 parameters
     decoded on chip) and the full-row FWHT.  Several of these kernels take less
     time than one Python-side launch, so each kernel's `steps` launches
     (MALL-cold rotation over buffer sets) are captured once into a HIP graph
-    and the graph is replayed; time = HIP events around one replay / steps."""
+    between two device stamps and the graph is replayed (_graph_us)."""
     import torch
     A, B = synth.factors(4, 8, 1, seed=5)
     Ad, Bd = torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev)
@@ -624,23 +653,7 @@ def table2_shapes(kq, synth, dev, stream, sptr, steps=500, warmup=3):
         }
         row = {}
         for name, fn in fns.items():
-            for i in range(nsets):   # eager pass over every set (also warms the TLB)
-                fn(i)
-            torch.cuda.synchronize()
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                for i in range(steps):
-                    fn(i % nsets)
-            for _ in range(warmup):
-                g.replay()
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            g.replay()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            row[name + "_us"] = round(e0.elapsed_time(e1) / steps * 1e3, 3)
-            del g
+            row[name + "_us"] = round(_graph_us(fn, nsets, steps, stream), 3)
         row["k1_gbs"] = round(nbytes / row["k1_us"] * 1e-3, 1)
         row["scale_over_k1"] = round(row["scale_us"] / row["k1_us"], 3)
         row["scale_over_k2"] = round(row["scale_us"] / row["k2_us"], 3)
@@ -648,7 +661,8 @@ def table2_shapes(kq, synth, dev, stream, sptr, steps=500, warmup=3):
         out[f"{m}x{d}"] = row
         del Xs, Cs, Ss, X0
         torch.cuda.empty_cache()
-    out["timing"] = "HIP graph of 500 launches per kernel, replayed; MALL-cold rotation"
+    out["timing"] = ("HIP graph of 500 launches per kernel between two kq_timestamp stamps, median of 3 replays; "
+                     "MALL-cold rotation")
     return out
 
 

@@ -264,6 +264,18 @@ kq_status kq_stream_probe(const uint16_t* X, int64_t M, int64_t d, uint8_t* out1
                           int waves_per_group, int units_per_wave, int64_t groups, void* stream);
 
 /*
+ * kq_timestamp -- a measurement aid, not part of the method: enqueues on
+ * `stream` a one-lane kernel that stores the device's constant-rate real-time
+ * counter (100 MHz, the same counter on every compute unit) into dst[0], so
+ * that a sequence of launches can be timed between two such stamps, also
+ * inside a captured graph, without the cost of launching the graph itself.
+ * dst device uint64 [1], 8-byte aligned (KQ_ERROR_NULL_POINTER /
+ * KQ_ERROR_MISALIGNED otherwise, checked before anything is enqueued).  No
+ * allocation, no synchronization.
+ */
+kq_status kq_timestamp(uint64_t* dst, void* stream);
+
+/*
  * kq_e2m1_encode -- the element-encode step alone, for checking the device
  * conversion: codes[i] = code(v[2i]) | code(v[2i+1]) << 4 at E8M0 byte s
  * (0..254), with the rounding rule above.  v device fp32 [n], n even;

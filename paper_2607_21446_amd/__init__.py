@@ -7,7 +7,7 @@ from .binding import (  # noqa: F401
     CALIB_NOALLOC_MAX_BYTES, EXPORTED, PACK_BYTES_PER_FACTOR, KQError, calib_reference, calib_step,
     calib_step_noalloc, calib_workspace, calibrate, e2m1_encode, factors_inverse_transpose, fwht, hadamard32, hadamard_lu, lib, lu_to_factors, mxfp4, mxfp4_gemm,
     pack_factors, quantize, quantize_exact, quantize_lu, quantize_packed, smoothquant, status_string, stream_floor,
-    stream_probe,
+    stream_probe, TIMESTAMP_HZ, timestamp,
     version,
     weight_transform,
 )

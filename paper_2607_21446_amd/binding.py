@@ -23,7 +23,7 @@ EXPORTED = (
     "kq_quantize", "kq_quantize_exact", "kq_quantize_packed", "kq_pack_factors", "kq_quantize_lu",
     "kq_smoothquant_quantize", "kq_hadamard32_quantize", "kq_fwht_quantize", "kq_mxfp4_quantize", "kq_mxfp4_gemm",
     "kq_mxfp4_gemm_bf16",
-    "kq_stream_floor", "kq_stream_probe",
+    "kq_stream_floor", "kq_stream_probe", "kq_timestamp",
     "kq_e2m1_encode", "kq_weight_transform", "kq_factors_inverse_transpose", "kq_lu_to_factors",
     "kq_calib_workspace_size", "kq_calib_reference", "kq_calib_step", "kq_calibrate",
     "kq_calib_step_noalloc",
@@ -69,7 +69,8 @@ def lib() -> ctypes.CDLL:
     L.kq_calib_step.argtypes = [P, I64, I64, P, I64, P, P, I, I64, P, P, P, P, P, I, F, P, ctypes.c_size_t, P]
     L.kq_calibrate.argtypes = [P, I64, I64, P, I64, P, P, I, I64, I, F, P, P, ctypes.c_size_t, P]
     L.kq_calib_step_noalloc.argtypes = [P, I64, I64, P, I64, P, P, I, I64, P, P, P, P, P, I, F, P]
-    for name in EXPORTED[:22]:
+    L.kq_timestamp.argtypes = [P, P]
+    for name in EXPORTED[:23]:
         getattr(L, name).restype = ctypes.c_int
     L.kq_status_string.argtypes = [I]
     L.kq_status_string.restype = ctypes.c_char_p
@@ -319,6 +320,19 @@ def stream_floor(X, out16=None, out1=None, stream=None):
     M, d = X.shape
     _check(lib().kq_stream_floor(_ptr(X), M, d, _ptr(out16), _ptr(out1), _stream(stream)), "kq_stream_floor")
     return out16, out1
+
+
+def timestamp(dst, index=0, stream=None):
+    """kq_timestamp: enqueue a store of the 100 MHz device real-time counter
+    into dst[index] (dst a device int64 tensor; a timing aid)."""
+    if not (isinstance(dst, torch.Tensor) and dst.is_cuda and dst.dtype == torch.int64 and dst.is_contiguous()):
+        raise TypeError("timestamp: dst must be a contiguous device int64 tensor")
+    if not 0 <= index < dst.numel():
+        raise ValueError(f"timestamp: index {index} outside dst of {dst.numel()} entries")
+    _check(lib().kq_timestamp(ctypes.c_void_p(dst.data_ptr() + 8 * int(index)), _stream(stream)), "kq_timestamp")
+
+
+TIMESTAMP_HZ = 100_000_000  # rate of the counter kq_timestamp stores
 
 
 def stream_probe(X, waves=1, units=1, groups=0, out16=None, out1=None, stream=None):

@@ -308,6 +308,12 @@ kq_status kq_stream_probe(const uint16_t* X, int64_t M, int64_t d, uint8_t* out1
     return from_hip(kq::launch_stream_probe(p, w, u, groups, (hipStream_t)stream), "kq_stream_probe");
 }
 
+kq_status kq_timestamp(uint64_t* dst, void* stream) {
+    if (!dst) return fail(KQ_ERROR_NULL_POINTER, "dst is null");
+    if (!aligned(dst, 8)) return fail(KQ_ERROR_MISALIGNED, "dst must be 8-byte aligned");
+    return from_hip(kq::launch_timestamp(dst, (hipStream_t)stream), "kq_timestamp");
+}
+
 static kq::GemmParams gemm_params(const uint8_t* a_codes, const uint8_t* a_scales, int64_t M, const uint8_t* b_codes,
                                   const uint8_t* b_scales, int64_t N, int64_t K, float* C, int64_t ldc, int accumulate,
                                   const float* bias) {

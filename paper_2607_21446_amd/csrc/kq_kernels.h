@@ -66,5 +66,6 @@ hipError_t launch_stream_floor(const Params& p, hipStream_t st);  // traffic of 
 // the same traffic in another launch shape: waves per workgroup (1, 2, 4, 8, 16), units per wave (1, 2, 4),
 // groups > 0: that many workgroups in a grid-stride loop, else one pass
 hipError_t launch_stream_probe(const Params& p, int waves, int units, int64_t groups, hipStream_t st);
+hipError_t launch_timestamp(uint64_t* dst, hipStream_t st);  // the 100 MHz real-time counter into dst[0]
 
 }  // namespace kq

@@ -1435,6 +1435,18 @@ __global__ __launch_bounds__(kThreads) void e2m1_kernel(const float* __restrict_
 //     deposit(v, other bits) | (j mod 2^k) << lo,   v = tl | (j >> k) << (LOG2D - 5),
 // "other bits" being the index bits outside [lo, lo + k) in increasing order,
 // tl the thread's index within its row.  Pass 0 is the thread's own block.
+// Measurement aid: one lane stores the device's constant-rate real-time
+// counter (100 MHz), so that a stream of launches can be timed between two
+// of these from inside a captured graph.
+__global__ __launch_bounds__(64) void timestamp_kernel(uint64_t* dst) {
+    if (threadIdx.x == 0) dst[0] = __builtin_amdgcn_s_memrealtime();
+}
+
+hipError_t launch_timestamp(uint64_t* dst, hipStream_t st) {
+    hipLaunchKernelGGL(timestamp_kernel, dim3(1), dim3(64), 0, st, dst);
+    return hipGetLastError();
+}
+
 template <int LOG2D>
 __device__ __forceinline__ int fwht_index(int lo, int k, int j, int tl) {
     const int v = tl | ((j >> k) << (LOG2D - 5));

@@ -36,6 +36,9 @@ def test_bench_json_line():
     # value is the algorithmic bytes of one step over the measured time per step
     nbytes = 4608 * 3072 * (2 + 0.5 + 1 / 32)
     assert abs(d["value"] - nbytes / (d["ms_per_step"] * 1e-3) / 1e9) <= 1e-3 * d["value"] + 0.5
+    # the stamps time exactly the K steps, inside the replay that the HIP events bracket
+    ev = d["replay_events_us_per_launch"]["kroquant"] * (d["steps"] + d["warmup"])
+    assert 0 < d["ms_per_step"] * 1e3 * d["steps"] <= ev * 1.001
     rf = d["roofline"]
     assert rf["bound"] == "hbm" and rf["unit"] == "GB/s" and rf["peak"] == 8000.0
     assert abs(rf["frac"] - rf["achieved"] / rf["peak"]) < 1e-3

@@ -168,6 +168,45 @@ def test_stream_probe_matches_stream_floor(M, d):
         assert np.array_equal(o16, f16) and np.array_equal(o1, f1), (waves, units, groups)
 
 
+def test_timestamp_counts_at_100_mhz():
+    """kq_timestamp: stamps around 1000 launches, on the launch stream and
+    inside a captured graph, advance at the documented 100 MHz: they lie
+    inside the HIP-event window around the same work and cover at least 97%
+    of it (the rest is the host-side gap before the first stamp, or the
+    graph's own launch)."""
+    X = dev_bf16(synth.activations(4608, 3072, "normal", seed=5))
+    f16, f1 = kq.stream_floor(X)
+    ts = torch.zeros(4, dtype=torch.int64, device="cuda")
+    st = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(st)
+    kq.timestamp(ts, 0)
+    for _ in range(1000):
+        kq.stream_floor(X, out16=f16, out1=f1)
+    kq.timestamp(ts, 1)
+    b.record(st)
+    torch.cuda.synchronize()
+    t = host(ts)
+    assert t[1] > t[0] > 0
+    ratio = (t[1] - t[0]) / kq.TIMESTAMP_HZ * 1e3 / a.elapsed_time(b)
+    assert 0.97 < ratio <= 1.001, ratio
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        kq.timestamp(ts, 2)
+        for _ in range(1000):
+            kq.stream_floor(X, out16=f16, out1=f1)
+        kq.timestamp(ts, 3)
+    g.replay()
+    torch.cuda.synchronize()
+    a.record(st)
+    g.replay()
+    b.record(st)
+    torch.cuda.synchronize()
+    t = host(ts)
+    ratio = (t[3] - t[2]) / kq.TIMESTAMP_HZ * 1e3 / a.elapsed_time(b)
+    assert 0.97 < ratio <= 1.001, ratio
+
+
 def test_tiny_config_all_paths():
     w = synth.workload("tiny_256x1152")
     want = oracle.quantize(w.X, w.A, w.B, want_y=True)

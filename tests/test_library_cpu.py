@@ -66,6 +66,15 @@ def test_quantize_rejects(kw, status):
     assert kq.lib().kq_last_error_detail() != b""
 
 
+def test_timestamp_rejects_before_enqueueing():
+    """kq_timestamp checks its destination before anything is enqueued."""
+    L = kq.lib()
+    assert L.kq_timestamp(None, None) == NULLP
+    assert L.kq_timestamp(FAKE + 4, None) == MISALIGNED
+    with pytest.raises(TypeError):
+        kq.timestamp(torch.zeros(2, dtype=torch.int64))  # a host tensor
+
+
 def test_zero_rows_is_a_no_op():
     assert _q(M=0) == SUCCESS
     assert _q(M=0, nfac=2) == SUCCESS
