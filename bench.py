@@ -149,7 +149,7 @@ def summarize_pmc(root, workload):
     print(json.dumps(rec, indent=1))
 
 
-def summarize_trace(root):
+def summarize_trace(root, warmup, steps):
     """Kernel durations from a rocprofv3 kernel trace, grouped by kernel name
     and grid size, in launch order (markdown on stdout)."""
     import csv
@@ -177,11 +177,16 @@ def summarize_trace(root):
     print("| kernel | grid (work-items) | calls | mean us | median us | p10 | p90 |\n|---|---|---|---|---|---|---|")
     for (k, grid), v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
         print(f"| `{k}` | {grid} | {len(v)} | {stats(v)} |")
-    print("\nwindows (launch order within a kernel and grid):\n")
+    # launch order of a timed measurement: W eager warmup launches, then the graph (W warmup launches, the K
+    # timed ones) replayed twice -- an untimed upload, then the timed replay
+    W, K = warmup, steps
+    wins = ((2 * W + 1, 2 * W + K, "upload replay"), (3 * W + K + 1, 3 * W + 2 * K, "timed replay"))
+    print(f"\nwindows (launch order within a kernel and grid; W = {W}, K = {K}):\n")
     for (k, grid), v in groups.items():
-        if len(v) >= 4000:
-            for a, b in ((2001, 3000), (3001, 4000)):
-                print(f"- `{k}` grid {grid}, launches {a}-{b}: mean | median | p10 | p90 = {stats(v[a - 1:b])} us")
+        if len(v) >= 3 * W + 2 * K:
+            for a, b, what in wins:
+                print(f"- `{k}` grid {grid}, launches {a}-{b} ({what}): mean | median | p10 | p90 = "
+                      f"{stats(v[a - 1:b])} us")
 
 
 def main():
@@ -190,7 +195,7 @@ def main():
         summarize_pmc(args.summarize_pmc, args.workload)
         return
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace)
+        summarize_trace(args.summarize_trace, args.warmup, args.steps)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this quantizer benchmark runs on exactly one GPU (--gpus 1); the quantizer "
