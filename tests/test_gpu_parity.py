@@ -238,6 +238,72 @@ def _edge_matrix():
     return synth.to_bf16_bits(np.stack(rows))
 
 
+def _sweep_case(seed):
+    """Shape, factors and input of one randomized case (seeded)."""
+    rng = np.random.default_rng(1000 + seed)
+    M = int(rng.integers(1, 700))
+    d = 32 * int(rng.integers(1, 200))
+    a = int(rng.choice([1, 2, 4, 8]))
+    b = 32 // a
+    nfac = d // 32 if rng.random() < 0.5 else 1
+    dist = str(rng.choice(["normal", "student_t3", "laplace"]))
+    X = synth.activations(M, d, dist, seed=2000 + seed, chan_frac=float(rng.choice([0.0, 0.01, 0.05])),
+                          chan_factor=float(rng.choice([5.0, 50.0])))
+    e = int(rng.integers(-60, 61))  # a power-of-two scale keeps the bf16 values exact
+    x = (X.astype(np.uint32) << 16).view(np.float32) * np.float32(2.0 ** e)
+    X = (x.view(np.uint32) >> 16).astype(np.uint16)
+    # factor families of the method: perturbed identities (the calibrated transforms start at the identity or
+    # a Hadamard and move little) at three strengths, and random orthogonal pairs (Hadamard-like, condition 1)
+    kind = str(rng.choice(["identity+0.05", "identity+0.15", "identity+0.3", "orthogonal"]))
+
+    def draw(n):
+        if kind == "orthogonal":
+            return np.stack([np.linalg.qr(rng.normal(size=(n, n)))[0] for _ in range(nfac)]).astype(np.float32)
+        eps = float(kind.split("+")[1])
+        return (np.eye(n) + eps * rng.normal(size=(nfac, n, n)) / np.sqrt(n)).astype(np.float32)
+
+    A, B = draw(a), draw(b)
+    return M, d, a, b, nfac, dist, e, kind, X, A, B
+
+
+@pytest.mark.parametrize("seed", range(32))
+def test_randomized_sweep(seed):
+    """Seeded random cases -- rows 1..699, d = 32..6368, every split, shared or
+    per-block factors (cond_inf(K) from 1
+    to about 30), three input distributions with or without outlier
+    channels, scaled by 2^-60..2^60; factors perturbed identities or random
+    orthogonal pairs) -- through every quantizer entry point:
+    the fixed-order path and the comparators bit-exact, the matrix-core paths
+    (on the fly, packed, LU form) within the tolerance, and the y-less calls
+    byte-identical to the calls that also write y."""
+    M, d, a, b, nfac, dist, e, kind, X, A, B = _sweep_case(seed)
+    what = f"seed {seed}: {M}x{d} ({a},{b}) nfac={nfac} {dist} 2^{e} {kind}"
+    want = oracle.quantize(X, A, B, want_y=True)
+    ye = oracle.transform_f64(X, A, B)
+    assert_exact(gpu_quantize(X, A, B, exact=True), want, what + " exact")
+    hot = gpu_quantize(X, A, B, exact=False)
+    assert_mx_close(hot, want, what + " on the fly", ye)
+    packed = gpu_quantize_packed(X, A, B)
+    assert_mx_close(packed, want, what + " packed", ye)
+    for got, full in ((gpu_quantize(X, A, B, want_y=False, exact=False), hot),
+                      (gpu_quantize_packed(X, A, B, want_y=False), packed)):
+        assert np.array_equal(got[0], full[0]) and np.array_equal(got[1], full[1]), what + " without y"
+    lu = synth.lu_params(nfac, seed=4000 + seed)
+    cr, sr, yr, _ = oracle.quantize_lu(X, lu, a, want_y=True)
+    c, s, y, y16 = gpu_quantize_lu(X, lu, a)
+    assert_mx_close((c, s, y), (cr, sr, yr), what + " lu", oracle.transform_f64(X, *oracle.lu_factors_f32(lu, a)))
+    assert np.array_equal(y16, oracle.f32_to_bf16(y)), what + " y16"
+    Xd = dev_bf16(X)
+    mult = synth.smoothquant_multipliers(X)
+    c, s, y = kq.smoothquant(Xd, dev_f32(mult), want_y=True)
+    assert_exact((host(c), host(s), host(y)), oracle.smoothquant(X, mult, want_y=True), what + " smooth")
+    c, s, y = kq.hadamard32(Xd, want_y=True)
+    assert_exact((host(c), host(s), host(y)), oracle.hadamard32(X, want_y=True), what + " hadamard")
+    c, s = kq.mxfp4(Xd)
+    cr, sr = oracle.mxfp4(X)
+    assert_exact((host(c), host(s), None), (cr, sr, None), what + " mxfp4")
+
+
 def test_edge_blocks_plain_smooth_hadamard():
     X = _edge_matrix()
     Xd = dev_bf16(X)
