@@ -367,6 +367,9 @@ def main():
         return {"median_us": round(float(np.median(t)), 3), "p10_us": round(float(np.percentile(t, 10)), 3),
                 "p90_us": round(float(np.percentile(t, 90)), 3)}
 
+    # the single-launch ceiling of this traffic first (about 50 ms of GPU work, reported below), so that the
+    # GPU's clocks are at their working level, as inside a model's step, when the hot path is timed
+    ceiling = launch_sweep(kq, Xs, Cs, Ss, nsets, int(min(2000, max(30, 20e9 // nbytes))), nbytes, stream)
     # timed region: exactly K steps of the hot path, after W warmup steps
     ms_kq, wall_kq = timed(run_kq, args.steps, args.warmup, name="kroquant")
     us_kq = ms_kq * 1e3
@@ -380,7 +383,6 @@ def main():
         comparators[name + "_us"] = round(ms * 1e3, 3)
         comparators[name + "_gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
     ms_floor_eager, _ = timed_eager(run_floor, args.steps, args.warmup)
-    ceiling = launch_sweep(kq, Xs, Cs, Ss, nsets, int(min(2000, max(30, 20e9 // nbytes))), nbytes, stream)
     ms_warm, _ = timed(run_kq, args.steps, args.warmup, rotate=False)
     # the vendor's device-to-device copy moving the same HBM bytes as one step
     # (half of them read, half written), with the same rotation
