@@ -406,6 +406,7 @@ def main():
     parity = "skipped"
     if not args.no_parity:
         parity = check_parity(w, run_kq, run_k2, run_kx, Cs, Ss)
+    quality = quantization_error(kq, Xs[0], A, B, kpack, mult)
 
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
@@ -464,6 +465,7 @@ def main():
         "warm_single_buffer": {"us": round(ms_warm * 1e3, 3), "gbs": round(nbytes / (ms_warm * 1e-3) / 1e9, 1)},
         "wall_s_timed_region": round(wall_kq, 4),
         "parity": parity,
+        "quantization_error": quality,
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
         "cpu_baseline": cpu,
@@ -794,6 +796,41 @@ def calib_timing(kq, synth, dev, stream, sptr, samples, steps=5, warmup=2):
     }
     del X, W, Yneg, ws
     torch.cuda.empty_cache()
+    return out
+
+
+E2M1_MAGNITUDES = (0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0)
+
+
+def quantization_error(kq, X, A, B, kpack, mult):
+    """The quality side metric (not a target): ||deq(Q(y)) - y||_F / ||y||_F
+    for each method's own transformed values y (Sec. 3.1's activation loss
+    L_A) on the headline input -- KroQuant (its random near-identity factors
+    are not calibrated, so it is not expected to win here), SmoothQuant,
+    Hadamard-32 and plain MXFP4.  Dequantization (E2M1 magnitude x 2^(s-127))
+    and the norms are torch ops on the device, in fp64."""
+    import torch
+    mags = torch.tensor(E2M1_MAGNITUDES, dtype=torch.float64, device=X.device)
+
+    def rel(codes, scales, y):
+        c = codes.to(torch.int64)
+        nib = torch.stack((c & 15, c >> 4), dim=-1).reshape(codes.shape[0], -1)  # element 2i in the low nibble
+        v = mags[nib & 7] * torch.where(nib >= 8, -1.0, 1.0)
+        scale = torch.exp2(scales.to(torch.float64) - 127.0).repeat_interleave(32, dim=1)
+        y64 = y.to(torch.float64)
+        return round(float(torch.linalg.norm(v * scale - y64) / torch.linalg.norm(y64)), 6)
+
+    out = {}
+    c, s, y = kq.quantize_packed(X, A, B, kpack, want_y=True)
+    out["kroquant"] = rel(c, s, y)
+    c, s, y = kq.smoothquant(X, mult, want_y=True)
+    out["smoothquant"] = rel(c, s, y)
+    c, s, y = kq.hadamard32(X, want_y=True)
+    out["hadamard32"] = rel(c, s, y)
+    c, s = kq.mxfp4(X)
+    out["mxfp4"] = rel(c, s, X.to(torch.float32))
+    out["what"] = ("||deq(Q(y)) - y||_F / ||y||_F on the headline input, y each method's transformed values; "
+                   "KroQuant with random near-identity (uncalibrated) factors")
     return out
 
 

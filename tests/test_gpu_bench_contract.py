@@ -46,6 +46,9 @@ def test_bench_json_line():
     assert d["parity"]["hot_path"].startswith("ok"), d["parity"]
     assert d["parity"]["onthefly"].startswith("ok"), d["parity"]
     assert d["parity"]["exact_path"] == "bit-exact"
+    # the quality side metric: a relative error in (0, 1) per method
+    q = d["quantization_error"]
+    assert all(0.0 < q[k] < 1.0 for k in ("kroquant", "smoothquant", "hadamard32", "mxfp4")), q
     # the single-launch ceiling: the best launch shape of the same traffic
     c = d["single_launch_ceiling"]
     assert c["us"] == min(c["sweep_us"].values()) and len(c["sweep_us"]) >= 10
