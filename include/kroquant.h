@@ -117,9 +117,11 @@ kq_status kq_pack_factors(const float* A, const float* B, int a, int b, int64_t 
  * (identical scales, codes within tie flips, y within the stated bound); the
  * edge window is 2^-17 cond_inf(A (x) B) amax here, taken from the pack,
  * instead of a per-block bound, so the set of re-evaluated blocks can differ.
- * With per-block factors (nfac = d/32) the pack is not read: every pair's K
- * is rebuilt on chip from its 320 bytes of A and B, which costs less than
- * reading its 6160-byte pack, and the result is exactly kq_quantize's.
+ * With per-block factors (nfac = d/32) only the 16-byte window header of
+ * each pair's pack is read: every pair's K is rebuilt on chip from its 320
+ * bytes of A and B, which costs less than reading its 6160-byte pack, and
+ * gives the K terms the pack holds, so the result equals this call's with
+ * the same pair repeated in a single-pair pack (nfac = 1), y included.
  */
 kq_status kq_quantize_packed(const uint16_t* X, int64_t M, int64_t d, const float* A,
                              const float* B, int a, int b, int64_t nfac, const void* kpack,

@@ -1052,9 +1052,11 @@ __global__ __launch_bounds__(256) void kron_build_unit_kernel(const Params p) {
 // the strip and keeps its K in registers for all the strip's steps, built by
 // each lane from its rows of A and B, which the wave stages in LDS (loaded,
 // or decoded from the 15 parameters of G_1..G_5 when LU), with the window
-// 2^-17 ||K||_inf max|x|.  (With a pair per block, building K from the 320
-// bytes of A and B is cheaper than reading its 6 KiB pack: the pack would add
-// 19-37% to a strip's input bytes.)  A step: wave w loads rows
+// 2^-17 ||K||_inf max|x|, or, PW (kq_quantize_packed), with the pair's
+// conditioning window T from its pack, as the flat packed kernel (with a pair
+// per block, building K from the 320 bytes of A and B is cheaper than reading
+// its 6 KiB pack, which would add 19-37% to a strip's input bytes; the 16-byte
+// window header is all the packed call reads of it).  A step: wave w loads rows
 // 8 w .. 8 w + 7 (two rows per 1 KiB load) and writes each 16-byte chunk to
 // the LDS tile of the wave that owns its column block, then issues the next
 // step's loads; after a barrier each wave runs the unit body on its column
@@ -1075,7 +1077,7 @@ constexpr int kTileSlots = 260;
 constexpr int kCodeSlots = 68;  // 64 blocks x 16 code bytes, then 64 scale bytes
 constexpr int kTileMaxSteps = 8;
 
-template <int NA, int NB, bool LU, bool WY, bool WY16>
+template <int NA, int NB, bool LU, bool WY, bool WY16, bool PW = false>
 __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params p, int rg) {
     constexpr int NF = NA * NA + NB * NB;
     constexpr int FPL = (NF + 63) / 64;  // factor entries per lane
@@ -1172,6 +1174,12 @@ __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params 
             neg_row = neg_row || all;
         }
         zero_ok = __builtin_amdgcn_ballot_w64(neg_row) == 0;
+        if (PW) {
+            // the pair's conditioning window from its pack (kq_pack_factors)
+            const float* hdr = reinterpret_cast<const float*>(p.kpack + f * kPackBytes + 6 * 64 * 16);
+            zero_ok = __float_as_uint(ld_uniform(hdr, 2)) != 0u;
+            et.edge_t = __float_as_uint(ld_uniform(hdr, 3));
+        }
     }
     for (int it = 0; it < nsteps; ++it) {
         const int64_t row0 = (rb0 + it) * 64;
@@ -1188,7 +1196,7 @@ __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params 
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
         if (active)
-            unit_compute<Mapping::Column, NA, NB, false, WY, WY16, false, false, true>(
+            unit_compute<Mapping::Column, NA, NB, false, WY, WY16, false, PW, true>(
                 p, lds_x + kTileSlots * w, row0 * p.nb + jc, nrows, (uint32_t)p.nb, v, ks, zero_ok, et, Af, Bf,
                 TileSink{lds_c + kCodeSlots * w, &stmask[w], &sedges[w][it]});
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
@@ -1570,6 +1578,11 @@ static hipError_t launch_tile(const Params& p, int rg, hipStream_t st) {
     const dim3 g((unsigned)(((nrb + rg - 1) / rg) * ntc)), b(64 * kTileCols);
     const bool wy = p.y != nullptr, wy16 = LU && p.y16 != nullptr;
 #define KQ_TILE(WY, WY16) hipLaunchKernelGGL((kron_tile_kernel<NA, NB, LU, WY, WY16>), g, b, 0, st, p, rg)
+    if (!LU && p.kpack) {
+        if (wy) hipLaunchKernelGGL((kron_tile_kernel<NA, NB, false, true, false, true>), g, b, 0, st, p, rg);
+        else hipLaunchKernelGGL((kron_tile_kernel<NA, NB, false, false, false, true>), g, b, 0, st, p, rg);
+        return hipGetLastError();
+    }
     if (wy16) { if (wy) KQ_TILE(true, LU); else KQ_TILE(false, LU); }
     else { if (wy) KQ_TILE(true, false); else KQ_TILE(false, false); }
 #undef KQ_TILE
@@ -1611,7 +1624,7 @@ static hipError_t launch_build(const Params& p, Mapping map, hipStream_t st) {
 // The API layer has checked that every grid fits one launch.
 template <int NA, int NB>
 static hipError_t launch_mfma(const Params& p, Mapping map, hipStream_t st) {
-    if (map == Mapping::Column) return launch_tile<NA, NB, false>(p, tile_rows(p), st);  // the pack is not read
+    if (map == Mapping::Column) return launch_tile<NA, NB, false>(p, tile_rows(p), st);  // K built, window from the pack
     const int64_t units = (p.nblocks + 63) / 64;
     if (p.kpack) return launch_unit<Mapping::Flat, NA, NB>(p, units, units <= kInterleaveMaxUnits, st);
     return launch_build<NA, NB, false>(p, map, st);
