@@ -367,8 +367,13 @@ def main():
         return {"median_us": round(float(np.median(t)), 3), "p10_us": round(float(np.percentile(t, 10)), 3),
                 "p90_us": round(float(np.percentile(t, 90)), 3)}
 
-    # the single-launch ceiling of this traffic first (about 50 ms of GPU work, reported below), so that the
-    # GPU's clocks are at their working level, as inside a model's step, when the hot path is timed
+    # the other shapes and workloads first (several seconds of every quantizer, matrix-core kernels included),
+    # then the single-launch ceiling of this traffic (about 50 ms, reported below), so that the GPU's clocks
+    # are at their working level, as inside a model's step, when the hot path is timed
+    table2 = None if args.no_table2 else table2_shapes(kq, synth, dev, stream, sptr)
+    wl_cache = {WORKLOAD: w}
+    configs = None if args.no_configs else config_table(kq, synth, dev, stream, names=args.configs.split(","),
+                                                        cache=wl_cache)
     ceiling = launch_sweep(kq, Xs, Cs, Ss, nsets, int(min(2000, max(30, 20e9 // nbytes))), nbytes, stream)
     # timed region: exactly K steps of the hot path, after W warmup steps
     ms_kq, wall_kq = timed(run_kq, args.steps, args.warmup, name="kroquant")
@@ -395,10 +400,6 @@ def main():
 
     ms_copy, _ = timed(run_copy, args.steps, args.warmup)
     del copy_dst
-    table2 = None if args.no_table2 else table2_shapes(kq, synth, dev, stream, sptr)
-    wl_cache = {WORKLOAD: w}
-    configs = None if args.no_configs else config_table(kq, synth, dev, stream, names=args.configs.split(","),
-                                                        cache=wl_cache)
     gemm = None if args.no_gemm else gemm_timing(kq, synth, dev, stream, sptr, Cs[0], Ss[0], M, d)
     calib = None if args.no_calib else calib_timing(kq, synth, dev, stream, sptr, args.calib_samples)
     dist = per_launch(run_kq)
@@ -577,7 +578,7 @@ def config_table(kq, synth, dev, stream, names=CONFIG_WORKLOADS, graph_bytes=20e
     plain MXFP4 and the traffic-only kernel on identical inputs.  Each kernel's
     launches (about graph_bytes of traffic, 30 to 2000 launches) are captured
     once into a HIP graph over enough rotating buffer sets to exceed twice the
-    MALL, and the graph is replayed between HIP events."""
+    MALL, and the time per launch is read from device stamps around them."""
     import torch
     cache = {} if cache is None else cache
     out = {}
