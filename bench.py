@@ -719,10 +719,43 @@ def gemm_timing(kq, synth, dev, stream, sptr, xc, xs, M, K, steps=100):
         tf16 = 2.0 * M * N * K / us16 * 1e-6
         row["bf16_output"] = {"us": round(us16, 2), "tflops": round(tf16, 1),
                               "frac_fp4_peak": round(tf16 / FP4_PEAK_TFLOPS, 4)}
+        row["vendor_scaled_mm"] = vendor_gemm(xc, xs, wc, ws, C, stream, steps)
         out[f"{M}x{N}x{K}"] = row
         del W, Wd, wc, ws, C, C16
     out["peak_tflops"] = FP4_PEAK_TFLOPS
     return out
+
+
+def vendor_gemm(xc, xs, wc, ws, C, stream, steps):
+    """The same MXFP4 product through the vendor's library (torch._scaled_mm
+    on E2M1 codes with E8M0 scales per 32-element block, bf16 output), timed
+    as kq_mxfp4_gemm; a comparator, never used by the library.  `max_rel_diff`
+    is max |vendor - C| / max |C| against kq_mxfp4_gemm's fp32 C."""
+    import torch
+    M, N, K = xc.shape[0], wc.shape[0], 2 * xc.shape[1]
+    a, b = xc.view(torch.float4_e2m1fn_x2), wc.view(torch.float4_e2m1fn_x2)
+    sa, sb = xs.view(torch.float8_e8m0fnu), ws.view(torch.float8_e8m0fnu)
+    try:
+        with torch.cuda.stream(stream):
+            def run():
+                return torch._scaled_mm(a, b.t(), scale_a=sa, scale_b=sb, out_dtype=torch.bfloat16)
+            ref = run()
+            for _ in range(9):
+                run()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(steps):
+                run()
+            e1.record(stream)
+        torch.cuda.synchronize()
+    except (RuntimeError, TypeError, AttributeError) as e:
+        return {"error": repr(e)[:200]}
+    us = e0.elapsed_time(e1) / steps * 1e3
+    tf = 2.0 * M * N * K / us * 1e-6
+    diff = float((ref.float() - C).abs().max() / C.abs().max())
+    return {"us": round(us, 2), "tflops": round(tf, 1), "frac_fp4_peak": round(tf / FP4_PEAK_TFLOPS, 4),
+            "max_rel_diff": round(diff, 6)}
 
 
 def calib_timing(kq, synth, dev, stream, sptr, samples, steps=5, warmup=2):

@@ -650,6 +650,40 @@ def test_mxfp4_gemm_bf16_output(M, N, K):
     assert np.all(np.abs(got - ref) <= 2.0 ** -8 * (np.abs(ref) + tol) + tol)
 
 
+@pytest.mark.parametrize("M,N,K", [(256, 512, 1024), (1024, 768, 3072)])
+def test_vendor_mxfp4_gemm_reads_the_same_layout(M, N, K):
+    """An independent reading of the operand layout: the vendor's MXFP4
+    product (torch._scaled_mm on E2M1 codes, two per byte with element 2i in
+    the low nibble, and E8M0 scales per 32-element block, bf16 output) on the
+    codes and scales as the quantizers write them, against the oracle's fp64
+    product and against kq_mxfp4_gemm_bf16.  The vendor's bf16 results are
+    not the nearest bf16 of their sums (they sit up to one bf16 step from the
+    exact product, mostly toward zero: a median relative error of 2.6e-3 on
+    random operands, against kq_mxfp4_gemm_bf16's correctly rounded fp32
+    sums), so the bound is one bf16 step; a misread nibble order, scale or
+    row would be off by far more."""
+    if not (hasattr(torch, "float4_e2m1fn_x2") and hasattr(torch, "float8_e8m0fnu")):
+        pytest.skip("this torch has no MXFP4 dtypes")
+    ac, as_ = _rand_mx(M, K, seed=M + 7 * K)
+    bc, bs = _rand_mx(N, K, seed=N + 11 * K)
+    t = lambda a: torch.from_numpy(a).cuda()
+    try:
+        V = torch._scaled_mm(t(ac).view(torch.float4_e2m1fn_x2), t(bc).view(torch.float4_e2m1fn_x2).t(),
+                             scale_a=t(as_).view(torch.float8_e8m0fnu), scale_b=t(bs).view(torch.float8_e8m0fnu),
+                             out_dtype=torch.bfloat16)
+        torch.cuda.synchronize()
+    except RuntimeError as e:
+        pytest.skip(f"the vendor library has no MXFP4 product here: {e!r:.200}")
+    got = host(V.float()).astype(np.float64)
+    ref = oracle.mxfp4_gemm(ac, as_, bc, bs)
+    tol = _gemm_tolerance(ac, as_, bc, bs)
+    step = 2.0 ** -7 * (np.abs(ref) + tol)  # one bf16 step at |ref|, or more
+    assert np.all(np.abs(got - ref) <= step + tol), np.max(np.abs(got - ref) / (step + tol))
+    ours = oracle.bf16_to_f32(host(kq.mxfp4_gemm(t(ac), t(as_), t(bc), t(bs), out_dtype=torch.bfloat16)
+                                   .view(torch.int16)).view(np.uint16)).astype(np.float64)
+    assert np.all(np.abs(got - ours) <= 1.5 * step + 2 * tol)
+
+
 def test_w4a4_layer_end_to_end():
     """X -> kq_quantize_packed, W -> kq_weight_transform, then kq_mxfp4_gemm:
     the layer output against the oracle's W4A4 product, and E(T) (Sec. 3.1)
