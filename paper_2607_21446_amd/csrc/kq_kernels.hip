@@ -680,9 +680,17 @@ __device__ __forceinline__ void unit_compute(const Params& p, uint4* lds, int64_
     uint16_t* const y16_u = WY16 ? p.y16 + first * 32 : nullptr;
     // every chunk goes to LDS as soon as it arrives (those of missing blocks as zeros)
     if (!TILE) {
+        if (FULL || nvalid == 64) {
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-            lds[wslot + 64 * c] = (FULL || (64 * c + lane) / 4 < nvalid) ? v[c] : make_uint4(0u, 0u, 0u, 0u);
+            for (int c = 0; c < 4; ++c) lds[wslot + 64 * c] = v[c];
+        } else {
+            // a partial unit (uniform branch): the chunks of missing blocks as zeros, branch-free
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t m = (64 * c + lane) / 4 < nvalid ? ~0u : 0u;
+                lds[wslot + 64 * c] = make_uint4(v[c].x & m, v[c].y & m, v[c].z & m, v[c].w & m);
+            }
+        }
     }
     // lane (jl, h) reads chunks h and 2 + h of block 32 t + jl: slots 128 t + rslot
     // and 128 t + (rslot ^ 2)
@@ -1185,11 +1193,20 @@ __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params 
         const int64_t row0 = (rb0 + it) * 64;
         const int nrows = (int)min<int64_t>(64, p.M - row0);
         // stage: chunk (q & 3) of column block q / 4 goes to that wave's tile
+        if (nrows == 64 && ncols == kTileCols) {
+            // a full step (the common case, uniform): every chunk as loaded
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const int r = 8 * w + 2 * c + (lane >> 5);
-            const bool ok = r < nrows && (q >> 2) < ncols;
-            lds_x[kTileSlots * (q >> 2) + lds_slot(r, q & 3)] = ok ? v[c] : make_uint4(0u, 0u, 0u, 0u);
+            for (int c = 0; c < 4; ++c)
+                lds_x[kTileSlots * (q >> 2) + lds_slot(8 * w + 2 * c + (lane >> 5), q & 3)] = v[c];
+        } else {
+            // rows past M and column blocks past nb as zeros, branch-free
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int r = 8 * w + 2 * c + (lane >> 5);
+                const uint32_t m = (r < nrows && (q >> 2) < ncols) ? ~0u : 0u;
+                lds_x[kTileSlots * (q >> 2) + lds_slot(r, q & 3)] =
+                    make_uint4(v[c].x & m, v[c].y & m, v[c].z & m, v[c].w & m);
+            }
         }
         if (it + 1 < nsteps) issue(row0 + 64);
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
