@@ -554,13 +554,18 @@ __device__ __forceinline__ void exact_flagged(uint64_t edges, const uint4* unit_
 //   A[o][p] = prod_{k < na}  G_k[bit(p, na-1-k)][bit(o, na-1-k)],
 //   B[i][q] = prod_{k >= na} G_k[bit(q, 4-k)][bit(i, 4-k)],
 // so A (x) B = (G_1 (x) ... (x) G_5)^T; every product left to right, one fp32
-// rounding per multiply, g11 = fma(c, b, -(1/a)).  The wave writes A then B
-// (NA*NA + NB*NB floats) to `out`; the parameters come in as scalar loads.
-// The 2x2 factors G_k = [[g0, g1], [g2, g3]] from the parameters (wave-uniform, scalar loads).
-__device__ __forceinline__ void lu_g(const float* lu, float (&g)[5][4]) {
+// rounding per multiply, g11 = fma(c, b, -(1/a)).
+// The 15 parameters of a pair as wave-uniform values (scalar loads).
+__device__ __forceinline__ void lu_load(const float* lu, float (&pv)[15]) {
+#pragma unroll
+    for (int i = 0; i < 15; ++i) pv[i] = ld_uniform(lu, i);
+}
+
+// The 2x2 factors G_k = [[g0, g1], [g2, g3]] from the parameters.
+__device__ __forceinline__ void lu_g(const float (&pv)[15], float (&g)[5][4]) {
 #pragma unroll
     for (int k = 0; k < 5; ++k) {
-        const float pa = ld_uniform(lu, 3 * k), pb = ld_uniform(lu, 3 * k + 1), pc = ld_uniform(lu, 3 * k + 2);
+        const float pa = pv[3 * k], pb = pv[3 * k + 1], pc = pv[3 * k + 2];
         g[k][0] = pa;
         g[k][1] = pb;
         g[k][2] = pc * pa;
@@ -957,13 +962,21 @@ __global__ __launch_bounds__(256) void kron_build_unit_kernel(const Params p) {
             fv[q] = __builtin_nontemporal_load(src);
         }
     }
+    // LU: the parameter pointer is read with the other kernel arguments, before
+    // the input loads (an empty asm that takes it in scalar registers), so
+    // that fetching the parameters after the input loads is one scalar round
+    // trip, not two: where scalar loads are slow that saves the call 4-5%
+    const float* const lu_ptr = p.lu + f * 15;
+    if (LU) asm volatile("" ::"s"(lu_ptr), "s"(p.X), "s"(p.nblocks));
     uint4 v[4];
     load_unit_clamped<MAP>(p, first, nvalid, bstride, v);
     __builtin_amdgcn_sched_barrier(0);
     // phase 1: factors into LDS (LU: every thread decodes at most one entry)
     if (LU) {
         float g[5][4];
-        lu_g(p.lu + f * 15, g);
+        float pv[15];
+        lu_load(lu_ptr, pv);
+        lu_g(pv, g);
 #pragma unroll
         for (int q = 0; q < FPT; ++q) {
             const int i = threadIdx.x + 256 * q;
@@ -1146,7 +1159,9 @@ __global__ __launch_bounds__(64 * kTileCols) void kron_tile_kernel(const Params 
         float* const facw = fac + w * NF;
         if (LU) {
             float gm[5][4];
-            lu_g(p.lu + f * 15, gm);
+            float pv[15];
+            lu_load(p.lu + f * 15, pv);
+            lu_g(pv, gm);
 #pragma unroll
             for (int q2 = 0; q2 < FPL; ++q2) {
                 const int i = lane + 64 * q2;
