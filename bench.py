@@ -318,18 +318,18 @@ def main():
     replay_us = {}
 
     def timed(fn, steps, warmup, rotate=True, name=None):
-        """K launches captured once into a HIP graph before the timed region
-        (same kernels, arguments and buffer rotation as the eager loop), behind
-        the W warmup launches and between two device stamps of the 100 MHz
-        real-time counter (kq_timestamp); one replay between
-        torch.cuda.synchronize() calls.  The time per step is the stamp
-        difference over K: exactly the K back-to-back launches, without the
-        host's per-call cost and without the fixed cost of launching the graph
-        (which, spread over a short K, would read as a slower step).  HIP
-        events around the same replay (warmup steps and graph launch included)
-        are kept beside it in `replay_us`."""
-        for i in range(warmup):
-            fn(i % nsets if rotate else 0)
+        """K launches captured into a HIP graph, behind W warmup launches and
+        between two device stamps of the 100 MHz real-time counter
+        (kq_timestamp).  The graph is captured first, then the W warmup steps
+        run eagerly, the graph is replayed once untimed (the first replay
+        uploads it) and once more, timed, all queued back to back with one
+        torch.cuda.synchronize() at the end, so the GPU does not idle between
+        the warmup and the timed launches.  The time per step is the stamp
+        difference of the second replay over K: exactly the K back-to-back
+        launches, without the host's per-call cost and without the fixed cost
+        of launching the graph (which, spread over a short K, would read as a
+        slower step).  HIP events around the timed replay (its warmup launches
+        and the graph launch included) are kept beside it in `replay_us`."""
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
@@ -339,12 +339,14 @@ def main():
             for i in range(steps):
                 fn(i % nsets if rotate else 0)
             kq.timestamp(stamps, 1)
-        g.replay()  # untimed: first replay uploads the graph
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
-        t0 = time.perf_counter()
+        for i in range(warmup):
+            fn(i % nsets if rotate else 0)
+        g.replay()  # untimed: the first replay uploads the graph
         e0.record(stream)
+        t0 = time.perf_counter()  # host wall clock from queueing the timed replay to its end
         g.replay()
         e1.record(stream)
         torch.cuda.synchronize()
@@ -457,10 +459,12 @@ def main():
                 "materialised A(x)B packed offline)",
         "comparators": comparators,
         "timing": "value: the K launches captured into a HIP graph (before the timed region) behind the W warmup "
-                  "launches and between two kq_timestamp stamps of the 100 MHz device counter; one replay between "
-                  "synchronizations, time per step = stamp difference / K. replay_events_us_per_launch: HIP events "
-                  "around that replay (the W warmup steps and the graph launch included) / (W + K); eager_python: "
-                  "the same K launches from the Python loop (ctypes call per step)",
+                  "launches and between two kq_timestamp stamps of the 100 MHz device counter; the W warmup steps "
+                  "run eagerly, then the graph is replayed once untimed and once timed, queued back to back (no "
+                  "idle GPU before the timed launches); time per step = stamp difference of the timed replay / K. "
+                  "replay_events_us_per_launch: HIP events around the timed replay (its W warmup steps and the "
+                  "graph launch included) / (W + K); eager_python: the same K launches from the Python loop "
+                  "(ctypes call per step)",
         "replay_events_us_per_launch": replay_us,
         "eager_python": {"kroquant_us": round(ms_kq_eager * 1e3, 3), "stream_floor_us": round(ms_floor_eager * 1e3, 3)},
         "per_launch_events": dist,
