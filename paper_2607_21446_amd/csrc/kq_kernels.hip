@@ -966,7 +966,7 @@ __global__ __launch_bounds__(256) void kron_build_unit_kernel(const Params p) {
     // the input loads (an empty asm that takes it in scalar registers), so
     // that fetching the parameters after the input loads is one scalar round
     // trip, not two: where scalar loads are slow that saves the call 4-5%
-    const float* const lu_ptr = p.lu + f * 15;
+    const float* const lu_ptr = LU ? p.lu + f * 15 : nullptr;
     if (LU) asm volatile("" ::"s"(lu_ptr), "s"(p.X), "s"(p.nblocks));
     uint4 v[4];
     load_unit_clamped<MAP>(p, first, nvalid, bstride, v);
