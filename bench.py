@@ -97,7 +97,8 @@ def parse():
     ap.add_argument("--configs", default=",".join(CONFIG_WORKLOADS),
                     help="comma-separated workloads of the table (default: all)")
     ap.add_argument("--no-table2", action="store_true",
-                    help="skip the power-of-two-d comparison (Q4, Scale, K1, K2, FWHT) at the paper's Table 2 shapes")
+                    help="skip the paper's Table 2 (power-of-two d: Q4, Scale, K1, K2, FWHT) and Table 4 (production "
+                         "shapes: Q4, Scale, K1, K2) comparisons")
     return ap.parse_args()
 
 
@@ -375,6 +376,7 @@ def main():
     # the clock transient that follows memory-only work on some boxes
     ceiling = launch_sweep(kq, Xs, Cs, Ss, nsets, int(min(2000, max(30, 20e9 // nbytes))), nbytes, stream)
     table2 = None if args.no_table2 else table2_shapes(kq, synth, dev, stream, sptr)
+    table4 = None if args.no_table2 else table2_shapes(kq, synth, dev, stream, sptr, shapes=TABLE4_SHAPES, fwht=False)
     wl_cache = {WORKLOAD: w}
     configs = None if args.no_configs else config_table(kq, synth, dev, stream, names=args.configs.split(","),
                                                         cache=wl_cache, last=args.workload)
@@ -477,6 +479,7 @@ def main():
         "cpu_baseline": cpu,
         "configs": configs,
         "table2_pow2_d": table2,
+        "table4_production": table4,
         "w4a4_gemm": gemm,
         "calibration": calib,
     }
@@ -638,13 +641,24 @@ def config_table(kq, synth, dev, stream, names=CONFIG_WORKLOADS, graph_bytes=20e
 TABLE2_SHAPES = [(4096, 1024), (4096, 4096), (4096, 16384), (512, 4096), (512, 16384)]
 
 
-def table2_shapes(kq, synth, dev, stream, sptr, steps=500):
+# The paper's Table 4 production shapes (FLUX.1 / PixArt-Sigma layers), with the paper's own Scale/K1 and
+# Scale/K2 on an MI350 (fp16 activations, Triton) as context: not a target for this machine.
+TABLE4_SHAPES = [(512, 3072), (512, 12288), (4096, 1152), (4096, 3072), (4096, 3456), (4096, 4096), (4096, 4608),
+                 (4096, 12288)]
+TABLE4_PAPER_RATIOS = {(512, 3072): (1.18, 1.02), (512, 12288): (1.12, 0.86), (4096, 1152): (1.31, 0.96),
+                       (4096, 3072): (1.10, 0.91), (4096, 3456): (1.14, 0.95), (4096, 4096): (1.10, 0.95),
+                       (4096, 4608): (1.08, 0.94), (4096, 12288): (0.99, 0.94)}
+
+
+def table2_shapes(kq, synth, dev, stream, sptr, steps=500, shapes=None, fwht=True):
     """The paper's power-of-two-d comparison (Sec. 4.4, Table 2): Q4, Scale
     (SmoothQuant), K1 (kq_quantize_packed), K2 (kq_quantize_lu, 15 parameters
-    decoded on chip) and the full-row FWHT.  Several of these kernels take less
-    time than one Python-side launch, so each kernel's `steps` launches
-    (MALL-cold rotation over buffer sets) are captured once into a HIP graph
-    between two device stamps and the graph is replayed (_graph_us)."""
+    decoded on chip) and the full-row FWHT; with `shapes` = TABLE4_SHAPES and
+    fwht=False, the production shapes of Table 4 (Q4, Scale, K1, K2, and the
+    paper's own MI350 ratios beside ours as context).  Several of these kernels
+    take less time than one Python-side launch, so each kernel's `steps`
+    launches (MALL-cold rotation over buffer sets) are captured once into a HIP
+    graph between two device stamps and the graph is replayed (_graph_us)."""
     import torch
     A, B = synth.factors(4, 8, 1, seed=5)
     Ad, Bd = torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev)
@@ -652,7 +666,7 @@ def table2_shapes(kq, synth, dev, stream, sptr, steps=500):
     kpack = kq.pack_factors(Ad, Bd, stream=sptr)
     torch.cuda.synchronize()
     out = {}
-    for m, d in TABLE2_SHAPES:
+    for m, d in (shapes or TABLE2_SHAPES):
         X = synth.activations(m, d, "student_t3", seed=m + d, chan_frac=0.005, chan_factor=50.0)
         mult = torch.from_numpy(synth.smoothquant_multipliers(X)).to(dev)
         nbytes = algorithmic_bytes(m, d)
@@ -667,15 +681,19 @@ def table2_shapes(kq, synth, dev, stream, sptr, steps=500):
             "scale": lambda i: kq.smoothquant(Xs[i], mult, codes=Cs[i], scales=Ss[i]),
             "k1": lambda i: kq.quantize_packed(Xs[i], Ad, Bd, kpack, codes=Cs[i], scales=Ss[i]),
             "k2": lambda i: kq.quantize_lu(Xs[i], lu, 4, codes=Cs[i], scales=Ss[i]),
-            "fwht": lambda i: kq.fwht(Xs[i], codes=Cs[i], scales=Ss[i]),
         }
+        if fwht:
+            fns["fwht"] = lambda i: kq.fwht(Xs[i], codes=Cs[i], scales=Ss[i])
         row = {}
         for name, fn in fns.items():
             row[name + "_us"] = round(_graph_us(fn, nsets, steps, stream), 3)
         row["k1_gbs"] = round(nbytes / row["k1_us"] * 1e-3, 1)
         row["scale_over_k1"] = round(row["scale_us"] / row["k1_us"], 3)
         row["scale_over_k2"] = round(row["scale_us"] / row["k2_us"], 3)
-        row["fwht_over_k2"] = round(row["fwht_us"] / row["k2_us"], 3)
+        if fwht:
+            row["fwht_over_k2"] = round(row["fwht_us"] / row["k2_us"], 3)
+        if (m, d) in TABLE4_PAPER_RATIOS:
+            row["paper_mi350_scale_over_k1"], row["paper_mi350_scale_over_k2"] = TABLE4_PAPER_RATIOS[(m, d)]
         out[f"{m}x{d}"] = row
         del Xs, Cs, Ss, X0
         torch.cuda.empty_cache()
