@@ -761,6 +761,38 @@ def test_lu_form_full_size(name):
     assert np.array_equal(host(y16.view(torch.int16)).view(np.uint16), oracle.f32_to_bf16(y))
 
 
+@pytest.mark.parametrize("ab", [(2, 16), (8, 4), (1, 32)])
+def test_other_splits_full_size(ab):
+    """The (a, b) splits other than the workloads' (4, 8), at FLUX 4608x3072
+    (6912 full units) with one shared near-identity pair: every output of the
+    fixed-order path bit for bit; the on-the-fly and packed calls launched as
+    the benchmark launches the hot path (codes and scales only) and with the
+    fp32 output, identical codes and scales either way and within the
+    tolerance of the oracle; and the LU form with a = the split's a."""
+    a, b = ab
+    w = synth.workload("flux_4608x3072")
+    A, B = synth.factors(a, b, 1, seed=100 + a)
+    Xd, Ad, Bd = dev_bf16(w.X), dev_f32(A), dev_f32(B)
+    cr, sr, yr = oracle.quantize(w.X, A, B, want_y=True)
+    ye = oracle.transform_f64(w.X, A, B)
+    c, s, y = kq.quantize_exact(Xd, Ad, Bd, want_y=True)
+    assert_exact((host(c), host(s), host(y)), (cr, sr, yr), f"{ab} exact")
+    kp = kq.pack_factors(Ad, Bd)
+    for what, run in (("onthefly", lambda wy: kq.quantize(Xd, Ad, Bd, want_y=wy)),
+                      ("packed", lambda wy: kq.quantize_packed(Xd, Ad, Bd, kp, want_y=wy))):
+        c, s, _ = run(False)
+        c, s = host(c), host(s)
+        assert_mx_close((c, s, None), (cr, sr, yr), f"{ab} {what} (no y output)")
+        c2, s2, y = run(True)
+        assert np.array_equal(host(c2), c) and np.array_equal(host(s2), s), f"{ab} {what}: y on/off differ"
+        assert_mx_close((c, s, host(y)), (cr, sr, yr), f"{ab} {what}", ye)
+    lu = synth.lu_params(1, seed=200 + a)
+    cr, sr, yr, _ = oracle.quantize_lu(w.X, lu, a, want_y=True)
+    c, s, y, _ = kq.quantize_lu(Xd, dev_f32(lu), a, want_y=True)
+    assert_mx_close((host(c), host(s), host(y)), (cr, sr, yr), f"{ab} lu",
+                    oracle.transform_f64(w.X, *oracle.lu_factors_f32(lu, a)))
+
+
 def test_per_block_strips_ragged():
     """Per-block factors on a shape whose strips take two 64-row steps, whose
     last strip has one step, last row block two rows and last column strip
