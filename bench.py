@@ -73,10 +73,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2000)
     ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--only", choices=["kroquant", "kroquant_onthefly", "kroquant_lu", "kroquant_exact", "smoothquant",
-                                       "hadamard32", "mxfp4", "stream_floor", "copy", "calib", "gemm"],
+                                       "hadamard32", "mxfp4", "stream_floor", "copy", "calib", "gemm", "gemm_vendor"],
                     help="run only this kernel for --steps launches (for profiler runs); prints no JSON "
                          "(calib: only the calibration timing, printed as JSON; gemm: the W4A4 product of the "
-                         "headline activation with a 3072 x 3072 weight)")
+                         "headline activation with a 3072 x 3072 weight; gemm_vendor: that product with a bf16 "
+                         "output, then the vendor's MXFP4 GEMM on the same operands)")
     ap.add_argument("--summarize-pmc", metavar="DIR",
                     help="turn the FETCH_SIZE / WRITE_SIZE counter runs under DIR (DIR/<kernel>/p3, p4 from "
                          "rocprofv3 --pmc, kernels 'kroquant' and 'copy') into the traffic record read by the "
@@ -275,17 +276,28 @@ def main():
             "smoothquant": run_sq,
             "hadamard32": run_h32, "mxfp4": run_q4, "stream_floor": run_floor}
 
-    if args.only == "gemm":
+    if args.only in ("gemm", "gemm_vendor"):
         A_, B_ = synth.factors(4, 8, 1, seed=5)
         Wg = synth.activations(3072, d, "normal", seed=3072, chan_frac=0.0)
         Wgd = torch.from_numpy(Wg.view(np.int16)).view(torch.bfloat16).to(dev)
         _, wc, wsc = kq.weight_transform(Wgd, torch.from_numpy(A_), torch.from_numpy(B_))
         run_kq(0)
-        Cg = torch.empty((M, 3072), dtype=torch.float32, device=dev)
-        for i in range(args.steps):
-            kq.mxfp4_gemm(Cs[0], Ss[0], wc, wsc, C=Cg, stream=sptr)
+        if args.only == "gemm":
+            Cg = torch.empty((M, 3072), dtype=torch.float32, device=dev)
+            for i in range(args.steps):
+                kq.mxfp4_gemm(Cs[0], Ss[0], wc, wsc, C=Cg, stream=sptr)
+        else:
+            # the bf16-output product, then the vendor's MXFP4 GEMM on the same codes and scales
+            C16 = torch.empty((M, 3072), dtype=torch.bfloat16, device=dev)
+            for i in range(args.steps):
+                kq.mxfp4_gemm(Cs[0], Ss[0], wc, wsc, C=C16, stream=sptr)
+            a, b = Cs[0].view(torch.float4_e2m1fn_x2), wc.view(torch.float4_e2m1fn_x2)
+            sa, sb = Ss[0].view(torch.float8_e8m0fnu), wsc.view(torch.float8_e8m0fnu)
+            with torch.cuda.stream(stream):
+                for i in range(args.steps):
+                    torch._scaled_mm(a, b.t(), scale_a=sa, scale_b=sb, out_dtype=torch.bfloat16)
         torch.cuda.synchronize()
-        print(f"ran gemm x{args.steps} ({M} x 3072 x {d})", flush=True)
+        print(f"ran {args.only} x{args.steps} ({M} x 3072 x {d})", flush=True)
         return
     if args.only:
         if args.only in ("copy", "calib"):
